@@ -1,0 +1,223 @@
+"""CPU oracle for pattern-sparse 3x3 convolution (test infrastructure only).
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product (the HIP library and its
+Python binding) never does, and shares no code with it.
+
+The arithmetic lives in ``pso.c`` (plain C, fp64, OpenMP over output planes);
+this module compiles it on demand and wraps it with numpy.  Each wrapper names
+the passage of Gong et al., "A Privacy-Preserving-Oriented DNN Pruning and
+Mobile Acceleration Framework" (GLSVLSI'20), that it implements:
+
+  select_library  Sec. 4.2   pattern-library heuristic (centre + 3 largest)
+  project         Sec. 4.3   Eq. 6, projection onto the pattern set C_n
+  select          Sec. 4.4   connectivity pruning, at most beta_n kernels
+  pack / unpack   Sec. 3.4   filter kernel reorder + compressed weight storage
+  mask_weights    Sec. 3.2   M o W with dropped kernels zeroed
+  conv_sparse     Sec. 4.1   Eq. 1 layer, 3x3 stride 1 pad 1, from the storage
+  conv_dense      Sec. 4.1   the same layer as a textbook dense loop (witness)
+
+Pins (see tests/test_oracle_*.py): brute-force projections on tiny layers,
+closed forms, invariants, impulse responses and float64 torch.conv2d agreement.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "pso.c")
+_LIB_PATH = os.path.join(_HERE, "libpso.so")
+_lib = None
+
+F32, F16 = 0, 1
+
+
+def build(force: bool = True) -> str:
+    """Compile pso.c into oracle/libpso.so (gcc, OpenMP, no fast-math)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-ffp-contract=off",
+               "-fno-fast-math", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        build(force=True)
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    i32, i64 = ctypes.c_int32, ctypes.c_int64
+    lib.pso_num_threads.restype = ctypes.c_int
+    lib.pso_select_library.argtypes = [P, i32, i64, i32, P]
+    lib.pso_project.argtypes = [P, i32, i64, P, i32, P, P]
+    lib.pso_select.argtypes = [P, i64, i64, P]
+    lib.pso_pack.argtypes = [P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P]
+    lib.pso_mask_weights.argtypes = [P, i32, i64, P, i32, P, P, P]
+    lib.pso_unpack.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P, P]
+    lib.pso_conv_sparse.argtypes = [P, i32, i32, i32, i32, i32, i32, i32, P,
+                                    P, P, P, P, P, P, i32, P, P]
+    lib.pso_conv_dense.argtypes = [P, i32, i32, i32, i32, i32, P, i32, P, i32, P]
+    for name in ("pso_select_library", "pso_project", "pso_select", "pso_pack",
+                 "pso_mask_weights", "pso_unpack", "pso_conv_sparse",
+                 "pso_conv_dense"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _dtype_code(a: np.ndarray) -> int:
+    if a.dtype == np.float32:
+        return F32
+    if a.dtype == np.float16:
+        return F16
+    raise TypeError("oracle handles float32 and float16 arrays, got %s" % a.dtype)
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise ValueError("oracle %s rejected its arguments" % what)
+
+
+def num_threads() -> int:
+    return int(_load().pso_num_threads())
+
+
+def select_library(w: np.ndarray, m: int) -> np.ndarray:
+    """Sec. 4.2: library of m centre+3 masks (bit 3r+s) from every 3x3 kernel
+    in ``w`` (any shape ending in 3x3)."""
+    w = np.ascontiguousarray(w)
+    k = w.size // 9
+    out = np.zeros(m, dtype=np.uint16)
+    _check(_load().pso_select_library(_ptr(w), _dtype_code(w), k, m, _ptr(out)),
+           "select_library")
+    return out
+
+
+def project(w: np.ndarray, masks: np.ndarray):
+    """Sec. 4.3 Eq. 6: per kernel, the library index keeping the largest
+    energy, and that energy (fp64)."""
+    w = np.ascontiguousarray(w)
+    masks = np.ascontiguousarray(masks, dtype=np.uint16)
+    k = w.size // 9
+    pat = np.zeros(k, dtype=np.uint8)
+    energy = np.zeros(k, dtype=np.float64)
+    _check(_load().pso_project(_ptr(w), _dtype_code(w), k, _ptr(masks),
+                               len(masks), _ptr(pat), _ptr(energy)), "project")
+    return pat, energy
+
+
+def select(energy: np.ndarray, keep: int) -> np.ndarray:
+    """Sec. 4.4: keep mask with exactly ``keep`` ones (largest energies,
+    ties to the lower flat index)."""
+    energy = np.ascontiguousarray(energy, dtype=np.float64)
+    out = np.zeros(energy.size, dtype=np.uint8)
+    _check(_load().pso_select(_ptr(energy), energy.size, int(keep), _ptr(out)),
+           "select")
+    return out
+
+
+def pack(w: np.ndarray, masks: np.ndarray, pat: np.ndarray, keep: np.ndarray) -> dict:
+    """Sec. 3.4: reordered, compressed storage of the pruned layer ``w``
+    (OIHW, [cout][cin][3][3])."""
+    w = np.ascontiguousarray(w)
+    cout, cin = int(w.shape[0]), int(w.shape[1])
+    masks = np.ascontiguousarray(masks, dtype=np.uint16)
+    m = len(masks)
+    pat = np.ascontiguousarray(pat, dtype=np.uint8)
+    keep = np.ascontiguousarray(keep, dtype=np.uint8)
+    beta = int(keep.astype(np.int64).sum())
+    out = {
+        "filter_perm": np.zeros(cout, dtype=np.int32),
+        "filter_ptr": np.zeros(cout + 1, dtype=np.int32),
+        "seg_ptr": np.zeros(cout * (m + 1), dtype=np.int32),
+        "cin_idx": np.zeros(beta, dtype=np.int32),
+        "pat_id": np.zeros(beta, dtype=np.uint8),
+        "values": np.zeros(beta * 4, dtype=w.dtype),
+    }
+    _check(_load().pso_pack(_ptr(w), _dtype_code(w), cout, cin, m, _ptr(masks),
+                            _ptr(pat), _ptr(keep), _ptr(out["filter_perm"]),
+                            _ptr(out["filter_ptr"]), _ptr(out["seg_ptr"]),
+                            _ptr(out["cin_idx"]), _ptr(out["pat_id"]),
+                            _ptr(out["values"])), "pack")
+    return out
+
+
+def mask_weights(w, masks, pat, keep) -> np.ndarray:
+    """Sec. 3.2: M o W for the chosen patterns, dropped kernels zeroed."""
+    w = np.ascontiguousarray(w)
+    masks = np.ascontiguousarray(masks, dtype=np.uint16)
+    out = np.zeros_like(w)
+    _check(_load().pso_mask_weights(
+        _ptr(w), _dtype_code(w), w.size // 9, _ptr(masks), len(masks),
+        _ptr(np.ascontiguousarray(pat, dtype=np.uint8)),
+        _ptr(np.ascontiguousarray(keep, dtype=np.uint8)), _ptr(out)),
+        "mask_weights")
+    return out
+
+
+def unpack(packed: dict, masks, cout: int, cin: int) -> np.ndarray:
+    """Compressed storage back to dense OIHW in the original filter order."""
+    masks = np.ascontiguousarray(masks, dtype=np.uint16)
+    vals = np.ascontiguousarray(packed["values"])
+    out = np.zeros((cout, cin, 3, 3), dtype=vals.dtype)
+    _check(_load().pso_unpack(
+        _dtype_code(vals), cout, cin, len(masks), _ptr(masks),
+        _ptr(np.ascontiguousarray(packed["filter_perm"], dtype=np.int32)),
+        _ptr(np.ascontiguousarray(packed["filter_ptr"], dtype=np.int32)),
+        _ptr(np.ascontiguousarray(packed["cin_idx"], dtype=np.int32)),
+        _ptr(np.ascontiguousarray(packed["pat_id"], dtype=np.uint8)),
+        _ptr(vals), _ptr(out)), "unpack")
+    return out
+
+
+def conv_sparse(x: np.ndarray, packed: dict, masks, cout: int, bias=None,
+                relu: bool = False, want_scale: bool = False):
+    """Sec. 4.1 Eq. 1 with the compressed storage: fp64 NCHW output
+    (and, with ``want_scale``, the per-output sum of |v*x| plus |b|)."""
+    x = np.ascontiguousarray(x)
+    n, cin, h, w = (int(d) for d in x.shape)
+    masks = np.ascontiguousarray(masks, dtype=np.uint16)
+    vals = np.ascontiguousarray(packed["values"])
+    if vals.size and vals.dtype != x.dtype:
+        raise TypeError("weights and activations must share a dtype")
+    if bias is not None:
+        bias = np.ascontiguousarray(bias, dtype=x.dtype)
+    y = np.zeros((n, cout, h, w), dtype=np.float64)
+    s = np.zeros_like(y) if want_scale else None
+    _check(_load().pso_conv_sparse(
+        _ptr(x), _dtype_code(x), n, cin, h, w, cout, len(masks), _ptr(masks),
+        _ptr(np.ascontiguousarray(packed["filter_perm"], dtype=np.int32)),
+        _ptr(np.ascontiguousarray(packed["filter_ptr"], dtype=np.int32)),
+        _ptr(np.ascontiguousarray(packed["cin_idx"], dtype=np.int32)),
+        _ptr(np.ascontiguousarray(packed["pat_id"], dtype=np.uint8)),
+        _ptr(vals), _ptr(bias), int(bool(relu)), _ptr(y), _ptr(s)),
+        "conv_sparse")
+    return (y, s) if want_scale else y
+
+
+def conv_dense(x: np.ndarray, wdense: np.ndarray, bias=None, relu: bool = False):
+    """Witness: textbook dense 3x3 convolution of OIHW weights, fp64 output."""
+    x = np.ascontiguousarray(x)
+    wdense = np.ascontiguousarray(wdense, dtype=x.dtype)
+    n, cin, h, w = (int(d) for d in x.shape)
+    cout = int(wdense.shape[0])
+    if bias is not None:
+        bias = np.ascontiguousarray(bias, dtype=x.dtype)
+    y = np.zeros((n, cout, h, w), dtype=np.float64)
+    _check(_load().pso_conv_dense(_ptr(x), _dtype_code(x), n, cin, h, w,
+                                  _ptr(wdense), cout, _ptr(bias),
+                                  int(bool(relu)), _ptr(y)), "conv_dense")
+    return y
