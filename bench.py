@@ -1,0 +1,223 @@
+"""Benchmark of the pattern-sparse 3x3 convolution forward on one MI355X.
+
+A step is one forward pass of the whole workload through the HIP path: for
+the VGG-16 stack (default) the 13 pattern-sparse conv layers with fused ReLU
+and the four 2x2 max-pools on a 1x3x224x224 synthetic image; for the other
+workloads every listed layer on its own resident input.  Weights are pruned
+and packed on the GPU (projection, selection, packing) before timing.
+
+Prints ONE JSON line: nonzero-MAC GFLOP/s of the step, ms/step, per-layer
+ms, the roofline of the conv kernel (measured with HIP events on the stream
+it runs on) and the CPU oracle as a baseline.  --details writes per-layer
+comparisons with the dense comparators (our dense HIP conv, MIOpen through
+torch) to a JSON file.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "nonzero-MAC GFLOP/s + ms/layer, pattern-sparse 3x3 conv fwd, batch 1 and 32"
+PEAK_VALU_TFLOPS = 157.3     # MI355X fp32 vector peak (256 CU x 2.4 GHz x 256 flop/clk)
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="vgg16_224_b1_f32")
+    ap.add_argument("--algo", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--details", default=None, help="write per-layer comparisons to this JSON file")
+    ap.add_argument("--list", action="store_true")
+    return ap.parse_args()
+
+
+def find_workload(name):
+    from paper_2003_06513_amd import inputs
+    for wl in inputs.all_workloads():
+        if wl.name == name:
+            return wl
+    raise SystemExit("unknown workload %s; --list shows the names" % name)
+
+
+class Net:
+    """Prepared layers + resident activations of one workload."""
+
+    def __init__(self, wl, algo):
+        import torch
+        from paper_2003_06513_amd import binding as B
+        from paper_2003_06513_amd import inputs
+        self.wl, self.algo = wl, algo
+        tdt = torch.float16 if wl.dtype == "f16" else torch.float32
+        self.tdt = tdt
+        allk = inputs.all_kernels(wl)
+        self.masks = B.select_library(allk, wl.m)
+        self.layers = []
+        n = wl.batch
+        x = torch.from_numpy(inputs.layer_input(wl, 0)).cuda()
+        for li, lay in enumerate(wl.layers):
+            w = torch.from_numpy(inputs.layer_weights(wl, li)).cuda()
+            prep = B.prepare(w, self.masks, lay.keep)
+            if not wl.chained and li > 0:
+                x = torch.from_numpy(inputs.layer_input(wl, li)).cuda()
+            y = torch.empty((n, lay.cout, lay.h, lay.w), dtype=tdt, device="cuda")
+            pooled = None
+            if lay.pool_after:
+                pooled = torch.empty((n, lay.cout, lay.h // 2, lay.w // 2), dtype=tdt, device="cuda")
+            self.layers.append(dict(lay=lay, w=w, prep=prep, x=x, y=y, pooled=pooled))
+            if wl.chained:
+                x = pooled if pooled is not None else y
+        torch.cuda.synchronize()
+
+    def step(self, events=None):
+        from paper_2003_06513_amd import binding as B
+        for li, L in enumerate(self.layers):
+            if events is not None:
+                events[li][0].record()
+            B.conv3x3_fwd(L["prep"].layer, L["prep"].packed, L["x"], L["y"], relu=L["lay"].relu,
+                          algo=self.algo)
+            if events is not None:
+                events[li][1].record()
+            if L["pooled"] is not None:
+                B.maxpool2x2(L["y"], L["pooled"])
+
+    def nz_flops(self, li):
+        lay = self.layers[li]["lay"]
+        return 8.0 * self.wl.batch * lay.h * lay.w * lay.keep
+
+
+def cpu_baseline(net):
+    """The oracle's sparse conv, as it stands, on the host cores."""
+    import oracle
+    oracle.build(force=False)
+    wl = net.wl
+    # bounded sample: whole layers in order until ~10 s of CPU work, at most
+    # one image of the batch
+    flops, secs, used = 0.0, 0.0, []
+    for li, L in enumerate(net.layers):
+        lay = L["lay"]
+        packed = L["prep"].packed.to_host()
+        x = L["x"][:1].cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.conv_sparse(x, packed, net.masks, lay.cout, relu=lay.relu)
+        secs += time.perf_counter() - t0
+        flops += 8.0 * lay.h * lay.w * lay.keep
+        used.append(lay.name)
+        if secs > 10.0:
+            break
+    return {"value": flops / secs / 1e9, "unit": "GFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": "fp64 oracle sparse conv, image 0 of the batch, layers %s (%.2f GFLOP in %.2f s)"
+                      % (",".join(used), flops / 1e9, secs)}
+
+
+def compare_dense(net, reps=20):
+    """Per-layer times of the dense comparators on the masked weights."""
+    import torch
+    from paper_2003_06513_amd import binding as B
+    out = []
+    for L in net.layers:
+        lay, prep = L["lay"], L["prep"]
+        wd = torch.empty(L["w"].shape, dtype=net.tdt, device="cuda")
+        B.unpack_dense(prep.layer, prep.packed, wd)
+        yd = torch.empty_like(L["y"])
+
+        def timeit(fn):
+            for _ in range(3):
+                fn()
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            s.record()
+            for _ in range(reps):
+                fn()
+            e.record()
+            torch.cuda.synchronize()
+            return s.elapsed_time(e) / reps
+
+        t_sparse = timeit(lambda: B.conv3x3_fwd(prep.layer, prep.packed, L["x"], L["y"], relu=lay.relu))
+        t_dense = timeit(lambda: B.dense3x3_fwd(L["x"], wd, yd, relu=lay.relu))
+        t_miopen = timeit(lambda: torch.relu_(torch.nn.functional.conv2d(L["x"], wd, padding=1))
+                          if lay.relu else torch.nn.functional.conv2d(L["x"], wd, padding=1))
+        out.append(dict(layer=lay.name, cin=lay.cin, cout=lay.cout, h=lay.h, w=lay.w, keep=lay.keep,
+                        sparse_ms=t_sparse, dense_hip_ms=t_dense, miopen_ms=t_miopen,
+                        nz_gflops=8.0 * net.wl.batch * lay.h * lay.w * lay.keep / t_sparse / 1e6))
+    return out
+
+
+def main():
+    args = parse()
+    if args.list:
+        from paper_2003_06513_amd import inputs
+        for wl in inputs.all_workloads():
+            print(wl.name)
+        return
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the pattern-sparse layer shards by batch with no "
+              "exchange, so multi-GPU runs are not part of this build", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2003_06513_amd import binding as B
+    torch.cuda.set_device(0)
+    B.lib()
+    wl = find_workload(args.workload)
+    net = Net(wl, args.algo)
+
+    for _ in range(args.warmup):
+        net.step()
+    torch.cuda.synchronize()
+    K = args.steps
+    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
+           for _ in net.layers] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        net.step(ev[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / K
+    layer_ms = [float(np.median([ev[k][li][0].elapsed_time(ev[k][li][1]) for k in range(K)]))
+                for li in range(len(net.layers))]
+    layer_mean_ms = [float(np.mean([ev[k][li][0].elapsed_time(ev[k][li][1]) for k in range(K)]))
+                     for li in range(len(net.layers))]
+    nz = [net.nz_flops(li) for li in range(len(net.layers))]
+    total_nz = sum(nz)
+    conv_ms = sum(layer_mean_ms)
+    achieved_tf = total_nz / (conv_ms * 1e-3) / 1e12
+    roof = {"bound": "alu", "achieved": round(achieved_tf, 3), "peak": PEAK_VALU_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved_tf / PEAK_VALU_TFLOPS, 4), "traffic": None,
+            "kernel": "k_conv_tiled", "per_launch": "8*N*H*W*keep nonzero-MAC flops, summed over the "
+                      "%d conv launches of a step / their summed mean duration" % len(net.layers)}
+    line = {
+        "metric": METRIC, "value": round(total_nz / (ms_step * 1e-3) / 1e9, 2), "unit": "GFLOP/s",
+        "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.batch, "layers": len(wl.layers), "m": wl.m,
+                   "stack": "conv+relu, 2x2 max-pool after conv2/4/7/10" if wl.chained else "independent layers"},
+        "ms_per_layer": {L["lay"].name: round(t, 4) for L, t in zip(net.layers, layer_ms)},
+        "conv_ms_per_step": round(conv_ms, 4),
+        "roofline": roof,
+    }
+    details = {}
+    if args.details:
+        details["dense_compare"] = compare_dense(net)
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(net)
+    print(json.dumps(line), flush=True)
+    if args.details:
+        details["line"] = line
+        with open(args.details, "w") as f:
+            json.dump(details, f, indent=1)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,176 @@
+/*
+ * psc.h -- pattern-sparse 3x3 convolution for AMD MI355X (gfx950).
+ *
+ * A C ABI over hand-written HIP kernels implementing the inference path of
+ * Gong et al., "A Privacy-Preserving-Oriented DNN Pruning and Mobile
+ * Acceleration Framework" (GLSVLSI'20):
+ *
+ *   psc_select_library  pattern-library heuristic                 Sec. 4.2
+ *   psc_project         projection of each kernel onto the
+ *                       pattern set C_n                           Sec. 4.3, Eq. 6
+ *   psc_select          connectivity pruning (constraint C'_n)    Sec. 4.4
+ *   psc_pack            filter kernel reorder + compressed
+ *                       weight storage                            Sec. 3.4
+ *   psc_conv3x3_fwd     the pruned layer X_n = sigma(W_n X + b_n) Sec. 4.1, Eq. 1
+ *
+ * plus a dense comparator, a dense unpacker and the 2x2 max-pool of the
+ * VGG-16 stack.
+ *
+ * Conventions for every entry point:
+ *  - "d_" pointers are device memory, "h_" pointers host memory; all of it is
+ *    owned and allocated by the caller.  The library never allocates or frees
+ *    device memory and never synchronises a stream: work is enqueued on
+ *    `stream` (a hipStream_t, NULL = the null stream) and the caller keeps
+ *    every buffer alive until that stream has drained it.
+ *  - Weights are contiguous OIHW [cout][cin][3][3]; activations contiguous
+ *    NCHW.  Masks are 9-bit codes, bit 3r+s for kernel row r, column s.
+ *  - Arguments are validated synchronously, before any HIP call, so errors
+ *    are reported the same way with or without a device.  A failed launch is
+ *    returned as PSC_ERR_DEVICE.  No C++ exception crosses the ABI.
+ *  - On any status other than PSC_OK, psc_last_error() returns a message for
+ *    the calling thread.  The library keeps no other global mutable state.
+ */
+#ifndef PSC_H
+#define PSC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PSC_MAX_PATTERNS 126      /* C(9,4): every distinct 4-of-9 mask */
+#define PSC_MAX_LIBRARY_HEURISTIC 56 /* C(8,3): centre + 3 neighbours */
+
+typedef enum {
+    PSC_OK = 0,
+    PSC_ERR_ARG = 1,          /* a null pointer, bad size, bad mask, ... */
+    PSC_ERR_UNSUPPORTED = 2,  /* a valid request this build does not run */
+    PSC_ERR_WORKSPACE = 3,    /* workspace pointer missing or too small */
+    PSC_ERR_DEVICE = 4,       /* a HIP call or kernel launch failed */
+    PSC_ERR_INTERNAL = 5
+} psc_status;
+
+typedef enum { PSC_F32 = 0, PSC_F16 = 1 } psc_dtype;
+
+/* Operations that take a workspace (psc_workspace_size). */
+typedef enum { PSC_OP_SELECT = 0, PSC_OP_PACK = 1 } psc_op;
+
+/* The per-layer representation the compiler optimisations work on (Sec. 3.4:
+ * layer shape, pattern style, connectivity).  Plain data, host memory. */
+typedef struct psc_layer {
+    int32_t cout;       /* output channels (filters), >= 1 */
+    int32_t cin;        /* input channels, >= 1 */
+    int32_t m;          /* pattern-library size, 1..PSC_MAX_PATTERNS (Sec. 3.2) */
+    int32_t wdtype;     /* psc_dtype of weights (and of activations) */
+    int64_t keep;       /* beta_n (Sec. 4.4): exact number of kernels kept,
+                           0..cout*cin */
+    uint16_t masks[PSC_MAX_PATTERNS]; /* masks[0..m-1]: pairwise distinct
+                           9-bit codes with exactly 4 bits set (Sec. 3.2) */
+} psc_layer;
+
+/* Compressed weight storage (Sec. 3.4), device pointers, caller-owned.
+ * Filters appear in reordered position i = 0..cout-1; inside a filter, kept
+ * kernels are sorted by (pattern id ascending, input channel ascending).
+ * Sizes follow from (cout, m, keep) alone. */
+typedef struct psc_packed {
+    int32_t *filter_perm; /* [cout]          reordered position -> original filter */
+    int32_t *filter_ptr;  /* [cout+1]        first kernel of position i; [cout] = keep */
+    int32_t *seg_ptr;     /* [cout*(m+1)]    seg_ptr[i*(m+1)+p]: first kernel of
+                                              pattern p in position i;
+                                              seg_ptr[i*(m+1)+m] = filter_ptr[i+1] */
+    int32_t *cin_idx;     /* [keep]          input channel of each kept kernel */
+    uint8_t *pat_id;      /* [keep]          library index of each kept kernel */
+    void *values;         /* [keep*4]        the 4 kept weights in ascending
+                                              3r+s order, wdtype; 16-byte aligned */
+} psc_packed;
+
+/* Message for the last failure on the calling thread ("" if none). */
+const char *psc_last_error(void);
+/* Constant name of a status code. */
+const char *psc_status_string(psc_status s);
+/* ABI version; bumped on any incompatible change. */
+int32_t psc_abi_version(void);
+
+/* Sec. 4.2: for each of the n_kernels 3x3 kernels in h_w (host, dtype),
+ * take the positions of its 3 largest-magnitude non-centre weights (ties to
+ * the lower position) plus the centre; the library is the m codes that occur
+ * most often, ordered by count descending then code ascending, filled with
+ * unseen centre+3 codes in ascending order.  Host only, no device work.
+ * m must be 1..PSC_MAX_LIBRARY_HEURISTIC.  h_masks_out receives m codes. */
+psc_status psc_select_library(const void *h_w, int32_t dtype, int64_t n_kernels,
+                              int32_t m, uint16_t *h_masks_out);
+
+/* Bytes of device workspace `op` needs for `layer` (0 is a valid answer).
+ * The workspace must be 256-byte aligned. */
+psc_status psc_workspace_size(const psc_layer *layer, int32_t op, size_t *bytes);
+
+/* Sec. 4.3, Eq. 6: projection of every kernel of d_w (cout*cin kernels) onto
+ * the pattern set.  For kernel k and library pattern p the energy is the fp64
+ * sum of the squares of the 4 kept weights, added in ascending position
+ * order; d_pat[k] is the first p of largest energy and d_energy[k] that
+ * energy.  Bit-exact and deterministic.  layer->keep is not read. */
+psc_status psc_project(const psc_layer *layer, const void *d_w, uint8_t *d_pat,
+                       double *d_energy, void *stream);
+
+/* Sec. 4.4: connectivity pruning.  d_keep[k] = 1 for exactly layer->keep
+ * kernels -- the largest energies, equal energies broken by the lower flat
+ * index k = co*cin+ci -- and 0 otherwise.  Energies must be non-negative
+ * (as psc_project writes them).  Needs PSC_OP_SELECT workspace. */
+psc_status psc_select(const psc_layer *layer, const double *d_energy,
+                      uint8_t *d_keep, void *d_ws, size_t ws_bytes, void *stream);
+
+/* Sec. 3.4: filter kernel reorder + compressed weight storage.  Filters are
+ * ordered by (kept-kernel count descending, per-pattern counts
+ * lexicographically descending, filter index ascending); values are bit
+ * copies of d_w.  d_keep must hold exactly layer->keep ones, d_pat entries
+ * must be < m (else the result is undefined).  Needs PSC_OP_PACK workspace.
+ * Every array of *out is written. */
+psc_status psc_pack(const psc_layer *layer, const void *d_w, const uint8_t *d_pat,
+                    const uint8_t *d_keep, const psc_packed *out, void *d_ws,
+                    size_t ws_bytes, void *stream);
+
+/* Compressed storage -> dense OIHW weights in the original filter order,
+ * zeros outside the kept patterns (bit copies of the stored values). */
+psc_status psc_unpack_dense(const psc_layer *layer, const psc_packed *packed,
+                            void *d_w_dense, void *stream);
+
+/* Sec. 4.1, Eq. 1: y = sigma(W x + b) for the pruned 3x3 layer, stride 1,
+ * zero padding 1, cross-correlation:
+ *   y[n,f,h,w] = b[f] + sum over kept kernels (ci, p) of filter f of
+ *                sum_j v_j * x[n, ci, h + r_j - 1, w + s_j - 1]
+ * with sigma = ReLU when relu != 0.  d_x is [n][cin][h][w], d_y is
+ * [n][cout][h][w] in the original filter order, both of dtype act_dtype,
+ * which must equal layer->wdtype.  fp16 data is accumulated in fp32 and the
+ * result rounded to nearest-even once.  d_bias ([cout], same dtype) may be
+ * NULL.  d_y must not overlap d_x.  n == 0 is a no-op. */
+psc_status psc_conv3x3_fwd(const psc_layer *layer, const psc_packed *packed,
+                           int32_t act_dtype, const void *d_x, int32_t n,
+                           int32_t h, int32_t w, const void *d_bias,
+                           int32_t relu, void *d_y, void *stream);
+
+/* Same as psc_conv3x3_fwd with an explicit kernel choice: algo 0 = the
+ * default tuned kernel, 1 = the simple one-output-per-lane kernel (kept as a
+ * second implementation for testing). */
+psc_status psc_conv3x3_fwd_algo(const psc_layer *layer, const psc_packed *packed,
+                                int32_t act_dtype, const void *d_x, int32_t n,
+                                int32_t h, int32_t w, const void *d_bias,
+                                int32_t relu, void *d_y, int32_t algo, void *stream);
+
+/* Comparator: the dense 3x3 convolution (stride 1, pad 1) of dense OIHW
+ * weights d_w [cout][cin][3][3] on the vector ALUs, same conventions and
+ * accumulation as psc_conv3x3_fwd. */
+psc_status psc_dense3x3_fwd(int32_t dtype, const void *d_x, int32_t n, int32_t cin,
+                            int32_t h, int32_t w, const void *d_w, int32_t cout,
+                            const void *d_bias, int32_t relu, void *d_y, void *stream);
+
+/* 2x2 max-pool, stride 2 (the pooling of the VGG-16 stack): d_x
+ * [n][c][h][w] -> d_y [n][c][h/2][w/2]; h and w must be even. */
+psc_status psc_maxpool2x2(int32_t dtype, const void *d_x, int32_t n, int32_t c,
+                          int32_t h, int32_t w, void *d_y, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PSC_H */

@@ -16,6 +16,7 @@ Mobile Acceleration Framework" (GLSVLSI'20), that it implements:
   mask_weights    Sec. 3.2   M o W with dropped kernels zeroed
   conv_sparse     Sec. 4.1   Eq. 1 layer, 3x3 stride 1 pad 1, from the storage
   conv_dense      Sec. 4.1   the same layer as a textbook dense loop (witness)
+  maxpool2x2                 2x2/2 max-pool between the VGG-16 layers
 
 Pins (see tests/test_oracle_*.py): brute-force projections on tiny layers,
 closed forms, invariants, impulse responses and float64 torch.conv2d agreement.
@@ -66,9 +67,10 @@ def _load():
     lib.pso_conv_sparse.argtypes = [P, i32, i32, i32, i32, i32, i32, i32, P,
                                     P, P, P, P, P, P, i32, P, P]
     lib.pso_conv_dense.argtypes = [P, i32, i32, i32, i32, i32, P, i32, P, i32, P]
+    lib.pso_maxpool2x2.argtypes = [P, i64, i32, i32, P]
     for name in ("pso_select_library", "pso_project", "pso_select", "pso_pack",
                  "pso_mask_weights", "pso_unpack", "pso_conv_sparse",
-                 "pso_conv_dense"):
+                 "pso_conv_dense", "pso_maxpool2x2"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -221,3 +223,12 @@ def conv_dense(x: np.ndarray, wdense: np.ndarray, bias=None, relu: bool = False)
                                   _ptr(wdense), cout, _ptr(bias),
                                   int(bool(relu)), _ptr(y)), "conv_dense")
     return y
+
+
+def maxpool2x2(y: np.ndarray) -> np.ndarray:
+    """2x2/2 max-pool of an fp64 NCHW array (the VGG-16 pooling)."""
+    y = np.ascontiguousarray(y, dtype=np.float64)
+    n, c, h, w = (int(d) for d in y.shape)
+    out = np.zeros((n, c, h // 2, w // 2), dtype=np.float64)
+    _check(_load().pso_maxpool2x2(_ptr(y), n * c, h, w, _ptr(out)), "maxpool2x2")
+    return out

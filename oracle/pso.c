@@ -20,6 +20,7 @@
  *                       the compressed storage               (Sec. 4.1, Eq. 1)
  *   pso_conv_dense      textbook dense direct convolution of
  *                       zero-masked OIHW weights (witness)   (Sec. 4.1, Eq. 1)
+ *   pso_maxpool2x2      2x2/2 max-pool between VGG-16 layers
  *
  * Arithmetic is fp64 throughout.  fp16 (IEEE binary16) and fp32 inputs are
  * converted to double exactly.
@@ -474,5 +475,24 @@ int pso_conv_dense(const void *x, int dtype, int n, int cin, int h, int w,
             }
         }
     }
+    return 0;
+}
+
+/* 2x2 max-pool with stride 2 on fp64 planes (the pooling between the VGG-16
+ * layers).  x is [nc][h][w], y is [nc][h/2][w/2]; h and w must be even. */
+int pso_maxpool2x2(const double *x, int64_t nc, int h, int w, double *y)
+{
+    if (nc < 0 || h < 2 || w < 2 || (h & 1) || (w & 1))
+        return -1;
+    for (int64_t c = 0; c < nc; ++c)
+        for (int oh = 0; oh < h / 2; ++oh)
+            for (int ow = 0; ow < w / 2; ++ow) {
+                const double *p = x + ((size_t)c * h + 2 * oh) * (size_t)w + 2 * ow;
+                double v = p[0];
+                if (p[1] > v) v = p[1];
+                if (p[w] > v) v = p[w];
+                if (p[w + 1] > v) v = p[w + 1];
+                y[((size_t)c * (h / 2) + oh) * (size_t)(w / 2) + ow] = v;
+            }
     return 0;
 }

@@ -1,0 +1,295 @@
+"""Python binding of libpsc (ctypes).  Argument marshalling only: every step
+of the path runs in the library's HIP kernels; torch supplies device memory
+and the stream.
+
+Function names follow the C entry points of include/psc.h without the
+``psc_`` prefix.  If the shared library is missing it is built with hipcc; if
+it cannot be loaded an ImportError is raised -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional
+
+import numpy as np
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libpsc.so")
+HEADER = os.path.join(os.path.dirname(PKG), "include", "psc.h")
+
+PSC_OK, PSC_ERR_ARG, PSC_ERR_UNSUPPORTED, PSC_ERR_WORKSPACE, PSC_ERR_DEVICE, PSC_ERR_INTERNAL = range(6)
+PSC_F32, PSC_F16 = 0, 1
+PSC_OP_SELECT, PSC_OP_PACK = 0, 1
+MAX_PATTERNS = 126
+
+STATUS_NAMES = {0: "PSC_OK", 1: "PSC_ERR_ARG", 2: "PSC_ERR_UNSUPPORTED", 3: "PSC_ERR_WORKSPACE",
+                4: "PSC_ERR_DEVICE", 5: "PSC_ERR_INTERNAL"}
+
+
+class PscError(RuntimeError):
+    def __init__(self, status: int, message: str, where: str):
+        super().__init__("%s: %s (%s)" % (where, STATUS_NAMES.get(status, status), message))
+        self.status = status
+        self.message = message
+
+
+class CLayer(ctypes.Structure):
+    _fields_ = [("cout", ctypes.c_int32), ("cin", ctypes.c_int32), ("m", ctypes.c_int32),
+                ("wdtype", ctypes.c_int32), ("keep", ctypes.c_int64),
+                ("masks", ctypes.c_uint16 * MAX_PATTERNS)]
+
+
+PACKED_FIELDS = ("filter_perm", "filter_ptr", "seg_ptr", "cin_idx", "pat_id", "values")
+
+
+class CPacked(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in PACKED_FIELDS]
+
+
+_lib = None
+
+
+def exported_names():
+    """Function names declared in include/psc.h."""
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(psc_[a-z0-9_]+)\s*\(", text)))
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        from . import build as _build
+        _build.build()
+    try:
+        L = ctypes.CDLL(LIB_PATH)
+    except OSError as e:
+        raise ImportError("cannot load %s: %s" % (LIB_PATH, e)) from e
+    P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    LP, PP = ctypes.POINTER(CLayer), ctypes.POINTER(CPacked)
+    sig = {
+        "psc_last_error": ([], ctypes.c_char_p),
+        "psc_status_string": ([ctypes.c_int], ctypes.c_char_p),
+        "psc_abi_version": ([], i32),
+        "psc_select_library": ([P, i32, i64, i32, P], ctypes.c_int),
+        "psc_workspace_size": ([LP, i32, ctypes.POINTER(sz)], ctypes.c_int),
+        "psc_project": ([LP, P, P, P, P], ctypes.c_int),
+        "psc_select": ([LP, P, P, P, sz, P], ctypes.c_int),
+        "psc_pack": ([LP, P, P, P, PP, P, sz, P], ctypes.c_int),
+        "psc_unpack_dense": ([LP, PP, P, P], ctypes.c_int),
+        "psc_conv3x3_fwd": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, P], ctypes.c_int),
+        "psc_conv3x3_fwd_algo": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, P], ctypes.c_int),
+        "psc_dense3x3_fwd": ([i32, P, i32, i32, i32, i32, P, i32, P, i32, P, P], ctypes.c_int),
+        "psc_maxpool2x2": ([i32, P, i32, i32, i32, i32, P, P], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = L
+    return L
+
+
+def last_error() -> str:
+    return lib().psc_last_error().decode()
+
+
+def _check(rc: int, where: str):
+    if rc != PSC_OK:
+        raise PscError(rc, last_error(), where)
+
+
+# ------------------------------------------------------------------ helpers
+def _torch():
+    import torch
+    return torch
+
+
+def dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return PSC_F32
+    if t.dtype == torch.float16:
+        return PSC_F16
+    raise TypeError("only float32 and float16 tensors are supported, got %s" % t.dtype)
+
+
+def _dev(t, name):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return ctypes.c_void_p(t.data_ptr()) if t.numel() else None
+
+
+def _stream(stream):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Layer:
+    """The per-layer representation (psc_layer)."""
+
+    def __init__(self, cout: int, cin: int, masks, keep: int, dtype: int):
+        masks = [int(v) for v in np.asarray(masks).reshape(-1)]
+        self.c = CLayer()
+        self.c.cout, self.c.cin, self.c.m = int(cout), int(cin), len(masks)
+        self.c.wdtype = int(dtype)
+        self.c.keep = int(keep)
+        for i, v in enumerate(masks[:MAX_PATTERNS]):
+            self.c.masks[i] = v
+        self.masks = np.array(masks, dtype=np.uint16)
+
+    cout = property(lambda self: self.c.cout)
+    cin = property(lambda self: self.c.cin)
+    m = property(lambda self: self.c.m)
+    keep = property(lambda self: self.c.keep)
+    dtype = property(lambda self: self.c.wdtype)
+
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+class Packed:
+    """Compressed weight storage held in device tensors (psc_packed)."""
+
+    def __init__(self, layer: Layer, device="cuda"):
+        torch = _torch()
+        cout, m, keep = layer.cout, layer.m, layer.keep
+        vdt = torch.float16 if layer.dtype == PSC_F16 else torch.float32
+        self.filter_perm = torch.empty(cout, dtype=torch.int32, device=device)
+        self.filter_ptr = torch.empty(cout + 1, dtype=torch.int32, device=device)
+        self.seg_ptr = torch.empty(cout * (m + 1), dtype=torch.int32, device=device)
+        self.cin_idx = torch.empty(keep, dtype=torch.int32, device=device)
+        self.pat_id = torch.empty(keep, dtype=torch.uint8, device=device)
+        self.values = torch.empty(keep * 4, dtype=vdt, device=device)
+
+    def c(self) -> CPacked:
+        cp = CPacked()
+        for n in PACKED_FIELDS:
+            t = getattr(self, n)
+            setattr(cp, n, t.data_ptr() if t.numel() else None)
+        return cp
+
+    def to_host(self) -> dict:
+        return {n: getattr(self, n).cpu().numpy() for n in PACKED_FIELDS}
+
+
+# ------------------------------------------------------------------ entry points
+def select_library(w: np.ndarray, m: int) -> np.ndarray:
+    """Sec. 4.2 pattern library over every 3x3 kernel of ``w`` (host array)."""
+    w = np.ascontiguousarray(w)
+    if w.dtype == np.float32:
+        dt = PSC_F32
+    elif w.dtype == np.float16:
+        dt = PSC_F16
+    else:
+        raise TypeError("w must be float32 or float16")
+    out = np.zeros(m, dtype=np.uint16)
+    _check(lib().psc_select_library(w.ctypes.data_as(ctypes.c_void_p), dt, w.size // 9, m,
+                                    out.ctypes.data_as(ctypes.c_void_p)), "psc_select_library")
+    return out
+
+
+def workspace_size(layer: Layer, op: int) -> int:
+    b = ctypes.c_size_t(0)
+    _check(lib().psc_workspace_size(layer.ref(), op, ctypes.byref(b)), "psc_workspace_size")
+    return int(b.value)
+
+
+def workspace(layer: Layer, op: int, device="cuda"):
+    torch = _torch()
+    n = workspace_size(layer, op)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+
+
+def project(layer: Layer, w, pat, energy, stream=None):
+    _check(lib().psc_project(layer.ref(), _dev(w, "w"), _dev(pat, "pat"), _dev(energy, "energy"),
+                             _stream(stream)), "psc_project")
+
+
+def select(layer: Layer, energy, keep_mask, ws, stream=None):
+    _check(lib().psc_select(layer.ref(), _dev(energy, "energy"), _dev(keep_mask, "keep"),
+                            _dev(ws, "ws"), ws.numel(), _stream(stream)), "psc_select")
+
+
+def pack(layer: Layer, w, pat, keep_mask, packed: Packed, ws, stream=None):
+    cp = packed.c()
+    _check(lib().psc_pack(layer.ref(), _dev(w, "w"), _dev(pat, "pat"), _dev(keep_mask, "keep"),
+                          ctypes.byref(cp), _dev(ws, "ws"), ws.numel(), _stream(stream)), "psc_pack")
+
+
+def unpack_dense(layer: Layer, packed: Packed, w_dense, stream=None):
+    cp = packed.c()
+    _check(lib().psc_unpack_dense(layer.ref(), ctypes.byref(cp), _dev(w_dense, "w_dense"),
+                                  _stream(stream)), "psc_unpack_dense")
+
+
+def conv3x3_fwd(layer: Layer, packed: Packed, x, y, bias=None, relu: bool = False, algo: int = 0,
+                stream=None):
+    n, cin, h, w = (int(d) for d in x.shape)
+    if cin != layer.cin or tuple(y.shape) != (n, layer.cout, h, w):
+        raise ValueError("x/y shapes do not match the layer")
+    cp = packed.c()
+    _check(lib().psc_conv3x3_fwd_algo(layer.ref(), ctypes.byref(cp), dtype_code(x), _dev(x, "x"), n, h,
+                                      w, _dev(bias, "bias"), int(bool(relu)), _dev(y, "y"), int(algo),
+                                      _stream(stream)), "psc_conv3x3_fwd")
+
+
+def dense3x3_fwd(x, wd, y, bias=None, relu: bool = False, stream=None):
+    n, cin, h, w = (int(d) for d in x.shape)
+    cout = int(wd.shape[0])
+    if tuple(wd.shape) != (cout, cin, 3, 3) or tuple(y.shape) != (n, cout, h, w):
+        raise ValueError("shape mismatch")
+    _check(lib().psc_dense3x3_fwd(dtype_code(x), _dev(x, "x"), n, cin, h, w, _dev(wd, "w"), cout,
+                                  _dev(bias, "bias"), int(bool(relu)), _dev(y, "y"), _stream(stream)),
+           "psc_dense3x3_fwd")
+
+
+def maxpool2x2(x, y, stream=None):
+    n, c, h, w = (int(d) for d in x.shape)
+    if tuple(y.shape) != (n, c, h // 2, w // 2):
+        raise ValueError("shape mismatch")
+    _check(lib().psc_maxpool2x2(dtype_code(x), _dev(x, "x"), n, c, h, w, _dev(y, "y"), _stream(stream)),
+           "psc_maxpool2x2")
+
+
+# ------------------------------------------------------------------ conveniences
+class Prepared:
+    """A pruned, packed layer: the result of project -> select -> pack."""
+
+    def __init__(self, layer: Layer, packed: Packed, pat, energy, keep_mask):
+        self.layer, self.packed = layer, packed
+        self.pat, self.energy, self.keep_mask = pat, energy, keep_mask
+
+
+def prepare(w, masks, keep: int, stream=None) -> Prepared:
+    """Project (Eq. 6), prune connectivity (Sec. 4.4) and pack (Sec. 3.4) the
+    OIHW device tensor ``w``; device buffers are allocated with torch."""
+    torch = _torch()
+    cout, cin = int(w.shape[0]), int(w.shape[1])
+    layer = Layer(cout, cin, masks, keep, dtype_code(w))
+    K = cout * cin
+    pat = torch.empty(K, dtype=torch.uint8, device=w.device)
+    energy = torch.empty(K, dtype=torch.float64, device=w.device)
+    keep_mask = torch.empty(K, dtype=torch.uint8, device=w.device)
+    packed = Packed(layer, w.device)
+    project(layer, w, pat, energy, stream)
+    select(layer, energy, keep_mask, workspace(layer, PSC_OP_SELECT, w.device), stream)
+    pack(layer, w, pat, keep_mask, packed, workspace(layer, PSC_OP_PACK, w.device), stream)
+    return Prepared(layer, packed, pat, energy, keep_mask)
+
+
+def conv(prep: Prepared, x, bias=None, relu: bool = False, algo: int = 0, out=None, stream=None):
+    torch = _torch()
+    n, _, h, w = x.shape
+    y = out if out is not None else torch.empty((n, prep.layer.cout, h, w), dtype=x.dtype, device=x.device)
+    conv3x3_fwd(prep.layer, prep.packed, x, y, bias=bias, relu=relu, algo=algo, stream=stream)
+    return y

@@ -1,0 +1,183 @@
+// Straightforward kernels: the one-output-per-lane pattern-sparse conv (a
+// second implementation of Sec. 4.1 Eq. 1 for testing the tuned kernel), the
+// dense vector-ALU 3x3 comparator and the 2x2 max-pool of the VGG-16 stack.
+#include "common.h"
+#include "launch.h"
+
+namespace psc {
+
+hipError_t launch_conv_tiled(const PatTable& tab, const PackedView& pk, const ConvArgs& a,
+                             hipStream_t stream);
+
+namespace {
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_conv_simple(const typename Elt<DT>::T* __restrict__ x, int cin,
+                                                     int H, int W, int cout, PatTable tab,
+                                                     const int32_t* __restrict__ perm,
+                                                     const int32_t* __restrict__ fptr,
+                                                     const int32_t* __restrict__ cin_idx,
+                                                     const uint8_t* __restrict__ pat_id,
+                                                     const typename Elt<DT>::T* __restrict__ values,
+                                                     const typename Elt<DT>::T* __restrict__ bias,
+                                                     int relu, typename Elt<DT>::T* __restrict__ y) {
+    using E = Elt<DT>;
+    __shared__ uint16_t msk[kMaxPatterns];
+    for (int p = threadIdx.x; p < tab.m; p += 256) msk[p] = tab.mask[p];
+    __syncthreads();
+    const int i = blockIdx.y, n = blockIdx.z;
+    const int plane = H * W;
+    const int pix = blockIdx.x * 256 + threadIdx.x;
+    if (pix >= plane) return;
+    const int oh = pix / W, ow = pix - oh * W;
+    const int f = perm[i];
+    const typename E::T* xn = x + int64_t(n) * cin * plane;
+    float acc = 0.f;
+    for (int k = fptr[i]; k < fptr[i + 1]; ++k) {
+        const int ci = cin_idx[k], p = pat_id[k];
+        if (unsigned(ci) >= unsigned(cin) || p >= tab.m) continue;   // malformed storage
+        const typename E::T* xc = xn + int64_t(ci) * plane;
+        const unsigned mk = msk[p];
+        int j = 0;
+        for (int q = 0; q < 9; ++q) {
+            if (!((mk >> q) & 1u)) continue;
+            const float v = E::load(values, int64_t(k) * 4 + j);
+            ++j;
+            const int ih = oh + q / 3 - 1, iw = ow + q % 3 - 1;
+            if (ih >= 0 && ih < H && iw >= 0 && iw < W) acc = fmaf(v, E::load(xc, ih * W + iw), acc);
+        }
+    }
+    if (bias) acc += E::load(bias, f);
+    if (relu) acc = acc > 0.f ? acc : 0.f;
+    y[(int64_t(n) * cout + f) * plane + pix] = E::from_f(acc);
+}
+
+// Dense comparator: a block computes a 16x16 output tile for 4 filters of
+// one image; input channels are staged through LDS with a 1-pixel halo.
+constexpr int kDT = 16;   // tile edge
+constexpr int kDF = 4;    // filters per block
+constexpr int kDC = 8;    // channels per stage
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_dense(const typename Elt<DT>::T* __restrict__ x, int cin, int H,
+                                               int W, const typename Elt<DT>::T* __restrict__ wd,
+                                               int cout, const typename Elt<DT>::T* __restrict__ bias,
+                                               int relu, typename Elt<DT>::T* __restrict__ y) {
+    using E = Elt<DT>;
+    __shared__ float xs[kDC][kDT + 2][kDT + 2];
+    __shared__ float ws[kDF][kDC][9];
+    const int tiles_w = (W + kDT - 1) / kDT;
+    const int th0 = (blockIdx.x / tiles_w) * kDT, tw0 = (blockIdx.x % tiles_w) * kDT;
+    const int f0 = blockIdx.y * kDF, n = blockIdx.z;
+    const int ty = threadIdx.x / kDT, tx = threadIdx.x % kDT;
+    const int plane = H * W;
+    const typename E::T* xn = x + int64_t(n) * cin * plane;
+    float acc[kDF];
+#pragma unroll
+    for (int g = 0; g < kDF; ++g) acc[g] = 0.f;
+    for (int c0 = 0; c0 < cin; c0 += kDC) {
+        for (int e = threadIdx.x; e < kDC * (kDT + 2) * (kDT + 2); e += 256) {
+            const int c = e / ((kDT + 2) * (kDT + 2));
+            const int r = (e / (kDT + 2)) % (kDT + 2);
+            const int s = e % (kDT + 2);
+            const int ih = th0 + r - 1, iw = tw0 + s - 1;
+            float v = 0.f;
+            if (c0 + c < cin && ih >= 0 && ih < H && iw >= 0 && iw < W)
+                v = E::load(xn, int64_t(c0 + c) * plane + ih * W + iw);
+            xs[c][r][s] = v;
+        }
+        for (int e = threadIdx.x; e < kDF * kDC * 9; e += 256) {
+            const int g = e / (kDC * 9), c = (e / 9) % kDC, q = e % 9;
+            float v = 0.f;
+            if (f0 + g < cout && c0 + c < cin) v = E::load(wd, (int64_t(f0 + g) * cin + c0 + c) * 9 + q);
+            ws[g][c][q] = v;
+        }
+        __syncthreads();
+        for (int c = 0; c < kDC; ++c)
+#pragma unroll
+            for (int q = 0; q < 9; ++q) {
+                const float xv = xs[c][ty + q / 3][tx + q % 3];
+#pragma unroll
+                for (int g = 0; g < kDF; ++g) acc[g] = fmaf(ws[g][c][q], xv, acc[g]);
+            }
+        __syncthreads();
+    }
+    const int oh = th0 + ty, ow = tw0 + tx;
+    if (oh >= H || ow >= W) return;
+#pragma unroll
+    for (int g = 0; g < kDF; ++g) {
+        const int f = f0 + g;
+        if (f >= cout) break;
+        float v = acc[g];
+        if (bias) v += E::load(bias, f);
+        if (relu) v = v > 0.f ? v : 0.f;
+        y[(int64_t(n) * cout + f) * plane + oh * W + ow] = E::from_f(v);
+    }
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_maxpool(const typename Elt<DT>::T* __restrict__ x, int64_t total,
+                                                 int H, int W, typename Elt<DT>::T* __restrict__ y) {
+    using E = Elt<DT>;
+    const int Ho = H / 2, Wo = W / 2;
+    for (int64_t o = int64_t(blockIdx.x) * 256 + threadIdx.x; o < total; o += int64_t(gridDim.x) * 256) {
+        const int64_t nc = o / (int64_t(Ho) * Wo);
+        const int r = int(o % (int64_t(Ho) * Wo));
+        const int oh = r / Wo, ow = r % Wo;
+        const typename E::T* p = x + nc * H * W + int64_t(2 * oh) * W + 2 * ow;
+        const float a = fmaxf(E::load(p, 0), E::load(p, 1));
+        const float b = fmaxf(E::load(p, W), E::load(p, W + 1));
+        y[o] = E::from_f(fmaxf(a, b));
+    }
+}
+
+template <int DT>
+hipError_t conv_simple(const PatTable& tab, const PackedView& pk, const ConvArgs& a, hipStream_t s) {
+    using T = typename Elt<DT>::T;
+    const dim3 grid(unsigned((a.h * a.w + 255) / 256), unsigned(a.cout), unsigned(a.n));
+    hipLaunchKernelGGL(k_conv_simple<DT>, grid, dim3(256), 0, s, static_cast<const T*>(a.x), a.cin, a.h,
+                       a.w, a.cout, tab, pk.filter_perm, pk.filter_ptr, pk.cin_idx, pk.pat_id,
+                       static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), a.relu,
+                       static_cast<T*>(a.y));
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs& a, int algo,
+                       hipStream_t stream) {
+    if (algo == 0) return launch_conv_tiled(tab, pk, a, stream);
+    return a.dtype == DT_F16 ? conv_simple<DT_F16>(tab, pk, a, stream)
+                             : conv_simple<DT_F32>(tab, pk, a, stream);
+}
+
+hipError_t launch_dense(int dtype, const void* x, int n, int cin, int h, int w, const void* wd, int cout,
+                        const void* bias, int relu, void* y, hipStream_t stream) {
+    const dim3 grid(unsigned(((h + kDT - 1) / kDT) * ((w + kDT - 1) / kDT)),
+                    unsigned((cout + kDF - 1) / kDF), unsigned(n));
+    if (dtype == DT_F16)
+        hipLaunchKernelGGL(k_dense<DT_F16>, grid, dim3(256), 0, stream, static_cast<const uint16_t*>(x), cin,
+                           h, w, static_cast<const uint16_t*>(wd), cout,
+                           static_cast<const uint16_t*>(bias), relu, static_cast<uint16_t*>(y));
+    else
+        hipLaunchKernelGGL(k_dense<DT_F32>, grid, dim3(256), 0, stream, static_cast<const float*>(x), cin, h,
+                           w, static_cast<const float*>(wd), cout, static_cast<const float*>(bias), relu,
+                           static_cast<float*>(y));
+    return hipGetLastError();
+}
+
+hipError_t launch_maxpool(int dtype, const void* x, int n, int c, int h, int w, void* y,
+                          hipStream_t stream) {
+    const int64_t total = int64_t(n) * c * (h / 2) * (w / 2);
+    const int64_t g = (total + 255) / 256;
+    const dim3 grid(unsigned(g > 65536 ? 65536 : g));
+    if (dtype == DT_F16)
+        hipLaunchKernelGGL(k_maxpool<DT_F16>, grid, dim3(256), 0, stream, static_cast<const uint16_t*>(x),
+                           total, h, w, static_cast<uint16_t*>(y));
+    else
+        hipLaunchKernelGGL(k_maxpool<DT_F32>, grid, dim3(256), 0, stream, static_cast<const float*>(x), total,
+                           h, w, static_cast<float*>(y));
+    return hipGetLastError();
+}
+
+}  // namespace psc

@@ -1,0 +1,65 @@
+// Internal launcher interface between the C ABI (psc_api.cpp) and the HIP
+// kernels.  Arguments arrive here already validated; launchers only enqueue
+// work on `stream` and return the launch status.
+#pragma once
+#include <hip/hip_runtime_api.h>
+#include <cstddef>
+#include <cstdint>
+
+namespace psc {
+
+struct PatTable;
+
+struct PackedView {
+    const int32_t* filter_perm;
+    const int32_t* filter_ptr;
+    const int32_t* seg_ptr;
+    const int32_t* cin_idx;
+    const uint8_t* pat_id;
+    const void* values;
+};
+
+struct PackedOut {
+    int32_t* filter_perm;
+    int32_t* filter_ptr;
+    int32_t* seg_ptr;
+    int32_t* cin_idx;
+    uint8_t* pat_id;
+    void* values;
+};
+
+// Sec. 4.3 Eq. 6
+hipError_t launch_project(const PatTable& tab, int dtype, const void* w, int64_t n_kernels,
+                          uint8_t* pat, double* energy, hipStream_t stream);
+
+// Sec. 4.4
+size_t select_workspace_bytes(int64_t n_kernels);
+hipError_t launch_select(int64_t n_kernels, int64_t keep, const double* energy, uint8_t* keep_out,
+                         void* ws, hipStream_t stream);
+
+// Sec. 3.4
+size_t pack_workspace_bytes(int cout, int m);
+hipError_t launch_pack(const PatTable& tab, int dtype, int cout, int cin, int64_t n_keep, const void* w,
+                       const uint8_t* pat, const uint8_t* keep, const PackedOut& out, void* ws,
+                       hipStream_t stream);
+hipError_t launch_unpack(const PatTable& tab, int dtype, int cout, int cin, int64_t keep,
+                         const PackedView& pk, void* dense, hipStream_t stream);
+
+// Sec. 4.1 Eq. 1
+struct ConvArgs {
+    int dtype;
+    int n, cin, h, w, cout;
+    int64_t keep;
+    const void* x;
+    const void* bias;
+    int relu;
+    void* y;
+};
+hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs& a, int algo,
+                       hipStream_t stream);
+hipError_t launch_dense(int dtype, const void* x, int n, int cin, int h, int w, const void* wd,
+                        int cout, const void* bias, int relu, void* y, hipStream_t stream);
+hipError_t launch_maxpool(int dtype, const void* x, int n, int c, int h, int w, void* y,
+                          hipStream_t stream);
+
+}  // namespace psc

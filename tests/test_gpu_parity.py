@@ -1,0 +1,215 @@
+"""GPU parity: every HIP entry point against the CPU oracle on the same
+seeded inputs.  Preparation (projection, selection, packing, unpacking) must
+be bit-exact; convolution outputs must be within a normwise relative error of
+1e-4 (fp32) or 1e-2 (fp16 storage, fp32 accumulation)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2003_06513_amd import binding as B
+from paper_2003_06513_amd import inputs
+from gpu_cases import (TOL, check_conv, compare_prepared, dev, gpu_prepare, host_prepare, norm_err,
+                       note, torch_mod)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    B.lib()
+
+
+def _case(seed, cout, cin, m, drop, dtype, masks=None):
+    w = inputs.he_weights(seed, cout, cin, dtype)
+    if masks is None:
+        masks = oracle.select_library(w, m)
+    keep = inputs.keep_after_drop(cout * cin, drop)
+    return w, np.asarray(masks, dtype=np.uint16), keep
+
+
+# ---------------------------------------------------------------- preparation
+PREP_CASES = [
+    (4, 3, 8, 0, np.float32), (64, 64, 8, 50, np.float32), (33, 17, 6, 70, np.float16),
+    (128, 64, 12, 60, np.float16), (7, 5, 1, 40, np.float32), (16, 16, 56, 30, np.float32),
+    (8, 8, 4, 100, np.float32), (3, 2, 4, 50, np.float16), (200, 3, 8, 0, np.float32),
+    (512, 512, 8, 60, np.float16), (256, 512, 8, 67, np.float32),
+]
+
+
+@pytest.mark.parametrize("cout,cin,m,drop,dtype", PREP_CASES)
+def test_prepare_bitexact(cout, cin, m, drop, dtype):
+    w, masks, keep = _case(cout * 7 + cin, cout, cin, m, drop, dtype)
+    note("prepare %dx%d m=%d keep=%d %s" % (cout, cin, m, keep, np.dtype(dtype).name))
+    prep = gpu_prepare(w, masks, keep)
+    compare_prepared(prep, w, masks, keep)
+
+
+def test_prepare_adversarial_ties():
+    rng = np.random.default_rng(17)
+    cases = []
+    # all-zero layer: every energy ties at 0
+    cases.append((np.zeros((16, 8, 3, 3), dtype=np.float32), 8, 50))
+    # small integers: many equal energies across the keep boundary
+    cases.append((rng.integers(-2, 3, size=(40, 30, 3, 3)).astype(np.float32), 6, 45))
+    # duplicated kernels
+    base = inputs.he_weights(3, 1, 1)
+    cases.append((np.repeat(np.repeat(base, 12, axis=0), 10, axis=1).astype(np.float32), 8, 30))
+    # equal-magnitude neighbours with mixed signs
+    k = np.array([[1, -1, 1], [-1, 2, 1], [1, 1, -1]], dtype=np.float16)
+    cases.append((np.tile(k, (9, 11, 1, 1)), 8, 60))
+    for w, m, drop in cases:
+        cout, cin = w.shape[:2]
+        masks = oracle.select_library(w, m)
+        keep = inputs.keep_after_drop(cout * cin, drop)
+        note("adversarial prepare %dx%d keep=%d" % (cout, cin, keep))
+        compare_prepared(gpu_prepare(w, masks, keep), w, masks, keep)
+
+
+@pytest.mark.parametrize("keep_mode", ["zero", "one", "all", "last"])
+def test_prepare_keep_extremes(keep_mode):
+    cout, cin = 12, 9
+    K = cout * cin
+    keep = {"zero": 0, "one": 1, "all": K, "last": K - 1}[keep_mode]
+    w, masks, _ = _case(5, cout, cin, 8, 0, np.float32)
+    note("prepare keep=%d" % keep)
+    compare_prepared(gpu_prepare(w, masks, keep), w, masks, keep)
+
+
+def test_prepare_non_centre_masks():
+    w = inputs.he_weights(77, 24, 20)
+    masks = inputs.random_masks(3, 10, centre=False)
+    note("prepare non-centre masks")
+    compare_prepared(gpu_prepare(w, masks, 150), w, masks, 150)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_unpack_dense_bitexact(dtype):
+    torch = torch_mod()
+    w, masks, keep = _case(31, 40, 24, 8, 55, dtype)
+    prep = gpu_prepare(w, masks, keep)
+    pat, _, keep_mask, _ = host_prepare(w, masks, keep)
+    wd = torch.empty(w.shape, dtype=getattr(torch, np.dtype(dtype).name), device="cuda")
+    note("unpack %s" % np.dtype(dtype).name)
+    B.unpack_dense(prep.layer, prep.packed, wd)
+    torch.cuda.synchronize()
+    assert wd.cpu().numpy().tobytes() == oracle.mask_weights(w, masks, pat, keep_mask).tobytes()
+
+
+def test_library_host_matches_oracle_on_workloads():
+    for wl in (inputs.vgg16_stack(1), inputs.resnet18_cifar_3x3(256)):
+        allk = inputs.all_kernels(wl)
+        assert np.array_equal(B.select_library(allk, wl.m), oracle.select_library(allk, wl.m))
+
+
+# ---------------------------------------------------------------- convolution
+CONV_SHAPES = [
+    # n, cin, cout, h, w
+    (1, 3, 8, 5, 5), (2, 5, 7, 9, 11), (1, 16, 16, 1, 1), (1, 8, 8, 2, 3), (3, 4, 5, 3, 4),
+    (1, 8, 16, 4, 4), (2, 6, 9, 7, 7), (1, 5, 4, 13, 13), (1, 4, 8, 6, 130), (1, 8, 8, 10, 32),
+    (1, 4, 4, 3, 63), (1, 4, 4, 3, 64), (2, 3, 6, 8, 62), (1, 6, 10, 17, 16), (5, 7, 3, 4, 8),
+    (1, 3, 8, 9, 224),
+]
+
+
+@pytest.mark.parametrize("algo", [0, 1])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("shape", CONV_SHAPES)
+def test_conv_shapes(shape, dtype, algo):
+    n, cin, cout, h, w = shape
+    wt, masks, keep = _case(n * 1000 + cin * 31 + cout, cout, cin, 8, 40, dtype)
+    prep = gpu_prepare(wt, masks, keep)
+    x = inputs.normal_activations(h * w + cin, (n, cin, h, w), dtype)
+    bias = inputs.bias_vector(cout, cout, dtype) if (h + w) % 2 else None
+    note("conv %s %s algo=%d" % (shape, np.dtype(dtype).name, algo))
+    check_conv(prep, x, masks, bias=bias, relu=bool(cin % 2), algo=algo, dtype=dtype)
+
+
+@pytest.mark.parametrize("algo", [0, 1])
+@pytest.mark.parametrize("m,centre", [(1, True), (4, True), (6, True), (12, True), (56, True),
+                                      (6, False), (20, False)])
+def test_conv_library_sizes(m, centre, algo):
+    cin, cout = 24, 20
+    masks = inputs.random_masks(m + 100, m, centre=centre)
+    wt = inputs.he_weights(m, cout, cin)
+    keep = inputs.keep_after_drop(cout * cin, 30)
+    prep = gpu_prepare(wt, masks, keep)
+    x = inputs.normal_activations(m, (2, cin, 12, 14))
+    note("conv m=%d centre=%s algo=%d" % (m, centre, algo))
+    check_conv(prep, x, masks, algo=algo)
+
+
+@pytest.mark.parametrize("algo", [0, 1])
+@pytest.mark.parametrize("keep_mode", ["zero", "one", "all"])
+def test_conv_keep_extremes(keep_mode, algo):
+    cin, cout = 9, 11
+    keep = {"zero": 0, "one": 1, "all": cin * cout}[keep_mode]
+    wt, masks, _ = _case(8, cout, cin, 8, 0, np.float32)
+    prep = gpu_prepare(wt, masks, keep)
+    x = inputs.normal_activations(9, (2, cin, 6, 7))
+    bias = inputs.bias_vector(10, cout)
+    note("conv keep=%d algo=%d" % (keep, algo))
+    check_conv(prep, x, masks, bias=bias, relu=True, algo=algo)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_conv_many_channel_chunks(dtype):
+    # cin well above one LDS chunk, cout not a multiple of the filter group
+    n, cin, cout, h, w = 2, 300, 70, 9, 10
+    wt, masks, keep = _case(123, cout, cin, 8, 60, dtype)
+    prep = gpu_prepare(wt, masks, keep)
+    x = inputs.normal_activations(5, (n, cin, h, w), dtype)
+    note("conv many chunks %s" % np.dtype(dtype).name)
+    check_conv(prep, x, masks, dtype=dtype)
+
+
+def test_conv_deterministic_and_in_bounds():
+    torch = torch_mod()
+    n, cin, cout, h, w = 2, 40, 24, 14, 14
+    wt, masks, keep = _case(55, cout, cin, 8, 50, np.float32)
+    prep = gpu_prepare(wt, masks, keep)
+    x = dev(inputs.normal_activations(6, (n, cin, h, w)))
+    guard = 4096
+    numel = n * cout * h * w
+    buf = torch.full((numel + 2 * guard,), 1234.5, dtype=torch.float32, device="cuda")
+    y1 = buf[guard:guard + numel].view(n, cout, h, w)
+    note("determinism/guard")
+    B.conv3x3_fwd(prep.layer, prep.packed, x, y1)
+    first = y1.clone()
+    B.conv3x3_fwd(prep.layer, prep.packed, x, y1)
+    torch.cuda.synchronize()
+    assert torch.equal(first, y1)
+    assert bool((buf[:guard] == 1234.5).all()) and bool((buf[guard + numel:] == 1234.5).all())
+
+
+# ---------------------------------------------------------------- comparators
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("shape", [(1, 3, 8, 5, 5), (2, 20, 17, 19, 23), (1, 64, 64, 32, 32)])
+def test_dense_comparator(shape, dtype):
+    torch = torch_mod()
+    n, cin, cout, h, w = shape
+    wt, masks, keep = _case(9, cout, cin, 8, 50, dtype)
+    pat, _, keep_mask, _ = host_prepare(wt, masks, keep)
+    wm = oracle.mask_weights(wt, masks, pat, keep_mask)
+    x = inputs.normal_activations(4, shape[:1] + (cin, h, w), dtype)
+    bias = inputs.bias_vector(3, cout, dtype)
+    y = torch.empty((n, cout, h, w), dtype=getattr(torch, np.dtype(dtype).name), device="cuda")
+    note("dense %s" % (shape,))
+    B.dense3x3_fwd(dev(x), dev(wm), y, bias=dev(bias), relu=True)
+    torch.cuda.synchronize()
+    ref = oracle.conv_dense(x, wm, bias=bias, relu=True)
+    assert norm_err(y.cpu().numpy(), ref) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_maxpool(dtype):
+    torch = torch_mod()
+    x = inputs.normal_activations(2, (3, 5, 8, 12), dtype)
+    y = torch.empty((3, 5, 4, 6), dtype=getattr(torch, np.dtype(dtype).name), device="cuda")
+    note("maxpool")
+    B.maxpool2x2(dev(x), y)
+    torch.cuda.synchronize()
+    ref = oracle.maxpool2x2(x.astype(np.float64))
+    assert np.array_equal(y.cpu().numpy().astype(np.float64), ref)

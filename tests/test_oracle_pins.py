@@ -426,3 +426,11 @@ def test_non_centre_library_masks_supported():
     y = oracle.conv_sparse(x, packed, masks, 5)
     yd = oracle.conv_dense(x, masked)
     assert np.abs(y - yd).max() <= 1e-12 * max(1.0, np.abs(yd).max())
+
+
+def test_maxpool_matches_block_max():
+    x = np.random.default_rng(0).standard_normal((2, 3, 6, 8))
+    y = oracle.maxpool2x2(x)
+    assert np.array_equal(y, x.reshape(2, 3, 3, 2, 4, 2).max(axis=(3, 5)))
+    with pytest.raises(ValueError):
+        oracle.maxpool2x2(np.zeros((1, 1, 3, 4)))
