@@ -6,8 +6,8 @@
 
 namespace psc {
 
-hipError_t launch_conv_tiled(const PatTable& tab, const PackedView& pk, const ConvArgs& a,
-                             hipStream_t stream);
+hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const ConvArgs& a,
+                              hipStream_t stream);
 
 namespace {
 
@@ -146,7 +146,12 @@ hipError_t conv_simple(const PatTable& tab, const PackedView& pk, const ConvArgs
 
 hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs& a, int algo,
                        hipStream_t stream) {
-    if (algo == 0) return launch_conv_tiled(tab, pk, a, stream);
+    if (algo == 0) {
+        const hipError_t e = launch_conv_stream(tab, pk, a, stream);
+        if (e != hipErrorNotSupported) return e;
+        // inputs beyond the 2 GiB one buffer descriptor covers take the
+        // one-output-per-lane kernel
+    }
     return a.dtype == DT_F16 ? conv_simple<DT_F16>(tab, pk, a, stream)
                              : conv_simple<DT_F32>(tab, pk, a, stream);
 }
