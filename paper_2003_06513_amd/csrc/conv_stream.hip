@@ -28,9 +28,9 @@
 // on both sides.  Otherwise a segment is [halo][Wt columns][halo], the halo
 // lanes holding the real neighbouring columns (or zero at the image border).
 //
-// Small grids split each filter over KS waves: wave s takes the s-th share
-// (by index) of every pattern segment, so the shares are equal; the partial
-// sums are added in share order through LDS, so results are deterministic.
+// Small grids split each filter over KS waves: wave s takes the s-th of KS
+// equal contiguous ranges of the filter's kernels; the partial sums are
+// added in share order through LDS, so results are deterministic.
 #include <cstdlib>
 #include <cstring>
 
@@ -378,12 +378,15 @@ __global__ __launch_bounds__(512) void k_conv_stream(const typename Elt<DT>::T* 
                                                                g.x_bytes, 0x00020000),
                              __builtin_amdgcn_readfirstlane(plane * int(sizeof(typename E::T))), g.cin - 1};
         const int* segp = seg_ptr + i * (g.m + 1);
-        const int f1 = segp[g.m];
+        const int f0 = segp[0], f1 = segp[g.m];
+        // share sp: the sp-th of KS equal contiguous ranges of the filter's
+        // kernels, which crosses few pattern segments
+        const int len = f1 - f0;
+        const int s0 = f0 + len * sp / g.KS, s1 = f0 + len * (sp + 1) / g.KS;
         for (int p = 0; p < g.m; ++p) {
-            const int a = segp[p], e = segp[p + 1];
-            const int len = e - a;
-            int k0 = a + len * sp / g.KS, k1 = a + len * (sp + 1) / g.KS;
-            k1 = k1 > f1 ? f1 : k1;                         // malformed pointers stay in the filter
+            int k0 = segp[p], k1 = segp[p + 1];
+            k0 = k0 < s0 ? s0 : k0;
+            k1 = k1 > s1 ? s1 : k1;                         // malformed pointers stay in the share
             if (k0 < k1) run_pattern<DT, R>(g.shape[p], g.mask[p], ctx, vo, k0, k1, acc);
         }
     }
