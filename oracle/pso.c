@@ -25,8 +25,7 @@
  * Arithmetic is fp64 throughout.  fp16 (IEEE binary16) and fp32 inputs are
  * converted to double exactly.
  *
- * Readings of points the paper leaves open (each one is listed in the design
- * notes of the repository):
+ * Readings of points the paper leaves open:
  *  - "3 largest weights" means largest magnitude; ties go to the lower
  *    position index 3r+s.
  *  - library order: code frequency descending, then code ascending; when
