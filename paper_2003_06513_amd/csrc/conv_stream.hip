@@ -18,9 +18,15 @@
 //    offsets of padding rows and columns are placed past its range, where a
 //    buffer load returns zero, so the zero padding costs nothing.
 //
-// There is no LDS staging and no barrier in the main loop: reuse of an input
-// row across the filters that touch it happens in the L1/L2 caches (filters
-// of one spatial tile run on the same XCD).
+// Input rows reach the registers one of two ways.  Direct: buffer loads
+// straight into registers.  Staged (full-row segments, throughput-bound
+// grids): the wave copies the contiguous rows its segments need into its own
+// LDS area with 64-byte-aligned 1 KiB buffer-to-LDS loads, two copies in
+// turn, and reads its rows from there -- a row load that straddles 128-byte
+// lines costs the vector memory path twice as much as an aligned one, and
+// image rows rarely start on a line.  Neither form has a barrier in the main
+// loop; reuse of an input row across the filters that touch it happens in
+// the L1/L2 caches (filters of one spatial tile run on the same XCD).
 //
 // Lane layout: a wave's 64 lanes hold S independent segments.  If the image
 // row fits (W <= 63), a segment is one full row band [W columns] and the
@@ -69,6 +75,9 @@ struct Geo {
     int nblocks;    // total workgroups
     int x_bytes;    // bytes of x (the buffer range), at most 2^31
     int relu;
+    int lds;        // 1: input rows staged through per-wave LDS (full-row segments only)
+    int region;     // LDS bytes reserved per run of rows
+    int wave_bytes; // LDS bytes per wave: nruns regions + a zero area
     int8_t shape[kMaxPatterns];  // centre+3 shape index of each library pattern, -1 = generic
     uint16_t mask[kMaxPatterns];
 };
@@ -285,6 +294,178 @@ __device__ __forceinline__ void run_generic(unsigned mask, const RunCtx<DT>& c, 
     });
 }
 
+// ------------------------------------------------------------------ LDS-staged rows
+// A 64-lane dword load runs at full rate only when every quarter-wave's 64
+// bytes lie in one 128-byte line.  Image rows start at arbitrary 4-byte
+// offsets, so a direct row load usually straddles lines and costs about twice
+// as much.  In the staged form a wave copies, per kernel, the input rows its
+// segments need -- for full-row segments these are contiguous "runs" of the
+// channel plane, one per image the wave touches -- into its own LDS area with
+// buffer-to-LDS loads that start on 64-byte boundaries, and then each lane
+// reads its rows from LDS.  The copy of the next kernel's rows overlaps the
+// current kernel's FMAs; no other wave touches the area, so no barrier is
+// needed.
+constexpr int kMaxRuns = 4;
+constexpr int kMaxDma = 4;     // buffer-to-LDS loads (1 KiB each: 16 bytes a lane) per run
+constexpr int kLdsCopy = 4096; // bytes between the two copies of a wave's runs
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <int DT>
+struct LdsCtx {
+    __amdgpu_buffer_rsrc_t xr;            // x, bounded to its size
+    const int32_t* __restrict__ cin_idx;
+    const typename Elt<DT>::T* __restrict__ vals;
+    int chan_bytes;                       // bytes of one input channel plane
+    int cmax;                             // last input channel
+    int nruns;
+    int run_base[kMaxRuns];               // byte offset in x of run j, channel 0
+    int run_lds[kMaxRuns];                // LDS address of run j's first byte
+    int run_len[kMaxRuns];                // bytes of run j
+    uint32_t vlane;                       // lane * 16
+};
+
+// s_waitcnt immediates (GFX9 encoding): wait on one counter only.
+constexpr int kWaitVm0 = 0x0F70;          // vmcnt(0)
+constexpr int kWaitLgkm0 = 0xC07F;        // lgkmcnt(0)
+
+#define PSC_DMA(Q) \
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(c.xr, dst, 16, c.vlane, soff, (Q) * 1024, 0)
+
+// Copy the runs of channel ci into this wave's LDS area.  Each load moves
+// 1 KiB (16 bytes a lane) from a 64-byte boundary on; the LDS destination is
+// shifted back by the same misalignment, so byte t of run j always lands at
+// run_lds[j] + t.  Bytes past the end of x read as zero (every offset of a
+// buffer load is range-checked).
+template <int DT>
+__device__ __forceinline__ void dma_rows(const LdsCtx<DT>& c, int ci, int buf) {
+#if defined(__HIP_DEVICE_COMPILE__)   // the 16-byte form exists only for the gfx950 device pass
+    ci = ci < 0 ? 0 : (ci > c.cmax ? c.cmax : ci);        // a malformed index stays inside x
+    const int coff = ci * c.chan_bytes;
+#pragma unroll
+    for (int j = 0; j < kMaxRuns; ++j) {
+        if (j < c.nruns) {
+            const int start = c.run_base[j] + coff;
+            const int mis = start & 63;
+            const int soff = start - mis;
+            lds_void_t* dst = (lds_void_t*)(uintptr_t)(uint32_t)(c.run_lds[j] + buf * kLdsCopy - mis);
+            const int cnt = (mis + c.run_len[j] + 1023) >> 10;
+            PSC_DMA(0);
+            if (cnt > 1) PSC_DMA(1);
+            if (cnt > 2) PSC_DMA(2);
+            if (cnt > 3) PSC_DMA(3);
+        }
+    }
+#endif
+}
+#undef PSC_DMA
+
+// The R+2 rows of this lane from LDS copy OFF / kLdsCopy (lo: LDS byte
+// addresses in copy 0; padding rows and columns point at a zeroed area that
+// both copies share).
+template <int DT, int R, int OFF>
+__device__ __forceinline__ void read_rows(const uint32_t (&lo)[R + 2], float (&xr)[R + 2]) {
+#pragma unroll
+    for (int r = 0; r < R + 2; ++r) {
+        if constexpr (DT == DT_F32)
+            xr[r] = *(const __attribute__((address_space(3))) float*)(uintptr_t)(lo[r] + OFF);
+        else
+            xr[r] = float(*(const __attribute__((address_space(3))) _Float16*)(uintptr_t)(lo[r] + OFF));
+    }
+}
+
+// One kernel whose rows sit (or are arriving) in copy B of the wave's LDS
+// area: wait for them, start the copy of kernel k+1 (also across the segment
+// end, for the next segment) into the other copy, read this lane's rows,
+// fetch the metadata of the kernels ahead, run the FMAs.
+template <int DT, int R, int B, class TapFn>
+__device__ __forceinline__ void lds_trip(const LdsCtx<DT>& c, const uint32_t (&lo)[R + 2], int k, int s1,
+                                         float (&w)[4], int& ci1, float (&acc)[R], TapFn taps) {
+    const int last = s1 - 1;
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);                // rows of kernel k are in LDS
+    asm volatile("" ::: "memory");
+    if (k + 1 < s1) dma_rows<DT>(c, ci1, B ^ 1);          // rows of kernel k+1
+    float xr[R + 2];
+    read_rows<DT, R, B * kLdsCopy>(lo, xr);
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);              // rows in registers
+    asm volatile("" ::: "memory");
+    float wn[4];
+    load_w4<DT>(c.vals, k + 1 <= last ? k + 1 : last, wn);
+    const int ci2 = __builtin_amdgcn_readfirstlane(c.cin_idx[k + 2 <= last ? k + 2 : last]);
+    taps(acc, xr, w);
+    w[0] = wn[0], w[1] = wn[1], w[2] = wn[2], w[3] = wn[3];
+    ci1 = ci2;
+}
+
+// Kernels [k, e) of one pattern segment, the first one's rows in copy B0.
+// Pairs of kernels per trip (one in each copy), an odd last one after the
+// loop: the single loop exit keeps the accumulators in place.  Returns the
+// copy that kernel e's rows go to.
+template <int DT, int R, int B0, class TapFn>
+__device__ __forceinline__ int run_pairs_lds(const LdsCtx<DT>& c, const uint32_t (&lo)[R + 2], int k, int e,
+                                             int s1, float (&acc)[R], TapFn taps) {
+    const int last = s1 - 1;
+    float w[4];
+    load_w4<DT>(c.vals, k, w);
+    int ci1 = __builtin_amdgcn_readfirstlane(c.cin_idx[k + 1 <= last ? k + 1 : last]);
+    while (k + 1 < e) {
+        lds_trip<DT, R, B0>(c, lo, k, s1, w, ci1, acc, taps);
+        lds_trip<DT, R, B0 ^ 1>(c, lo, k + 1, s1, w, ci1, acc, taps);
+        k += 2;
+    }
+    if (k < e) {
+        lds_trip<DT, R, B0>(c, lo, k, s1, w, ci1, acc, taps);
+        return B0 ^ 1;
+    }
+    return B0;
+}
+
+template <int DT, int R, class TapFn>
+__device__ __forceinline__ int run_kernels_lds(const LdsCtx<DT>& c, const uint32_t (&lo)[R + 2], int k, int e,
+                                               int s1, int par, float (&acc)[R], TapFn taps) {
+    return par == 0 ? run_pairs_lds<DT, R, 0>(c, lo, k, e, s1, acc, taps)
+                    : run_pairs_lds<DT, R, 1>(c, lo, k, e, s1, acc, taps);
+}
+
+template <int DT, int R, int MASK>
+__device__ __forceinline__ int run_shape_lds(const LdsCtx<DT>& c, const uint32_t (&lo)[R + 2], int k, int e,
+                                             int s1, int par, float (&acc)[R]) {
+    constexpr int Q0 = NthBit<MASK, 0>::value(), Q1 = NthBit<MASK, 1>::value();
+    constexpr int Q2 = NthBit<MASK, 2>::value(), Q3 = NthBit<MASK, 3>::value();
+    constexpr bool WS = DT == DT_F32;
+    return run_kernels_lds<DT, R>(c, lo, k, e, s1, par, acc,
+                                  [](float (&a)[R], const float (&x)[R + 2], const float (&w)[4]) {
+        tap_q<Q0, R, WS>(a, x, w[0]);
+        tap_q<Q1, R, WS>(a, x, w[1]);
+        tap_q<Q2, R, WS>(a, x, w[2]);
+        tap_q<Q3, R, WS>(a, x, w[3]);
+    });
+}
+
+template <int DT, int R>
+__device__ __forceinline__ int run_generic_lds(unsigned mask, const LdsCtx<DT>& c, const uint32_t (&lo)[R + 2],
+                                               int k, int e, int s1, int par, float (&acc)[R]) {
+    int q0 = 4, q1 = 4, q2 = 4, q3 = 4, seen = 0;
+#pragma unroll
+    for (int q = 0; q < 9; ++q) {
+        if ((mask >> q) & 1u) {
+            if (seen == 0) q0 = q;
+            else if (seen == 1) q1 = q;
+            else if (seen == 2) q2 = q;
+            else if (seen == 3) q3 = q;
+            ++seen;
+        }
+    }
+    constexpr bool WS = DT == DT_F32;
+    return run_kernels_lds<DT, R>(c, lo, k, e, s1, par, acc,
+                                  [=](float (&a)[R], const float (&x)[R + 2], const float (&w)[4]) {
+        tap_dyn<R, WS>(q0, a, x, w[0]);
+        tap_dyn<R, WS>(q1, a, x, w[1]);
+        tap_dyn<R, WS>(q2, a, x, w[2]);
+        tap_dyn<R, WS>(q3, a, x, w[3]);
+    });
+}
+
 #define PSC_SHAPE_CASE(I) \
     case I: run_shape<DT, R, kCentre3.code[I]>(c, vo, k, e, acc); return;
 #define PSC_SHAPE_CASE8(I)                                                                     \
@@ -308,8 +489,34 @@ __device__ __forceinline__ void run_pattern(int shape, unsigned mask, const RunC
 #undef PSC_SHAPE_CASE8
 #undef PSC_SHAPE_CASE
 
-// ------------------------------------------------------------------ kernel
+#define PSC_SHAPE_CASE(I) \
+    case I: return run_shape_lds<DT, R, kCentre3.code[I]>(c, lo, k, e, s1, par, acc);
+#define PSC_SHAPE_CASE8(I)                                                                     \
+    PSC_SHAPE_CASE(I) PSC_SHAPE_CASE(I + 1) PSC_SHAPE_CASE(I + 2) PSC_SHAPE_CASE(I + 3)        \
+    PSC_SHAPE_CASE(I + 4) PSC_SHAPE_CASE(I + 5) PSC_SHAPE_CASE(I + 6) PSC_SHAPE_CASE(I + 7)
+
 template <int DT, int R>
+__device__ __forceinline__ int run_pattern_lds(int shape, unsigned mask, const LdsCtx<DT>& c,
+                                               const uint32_t (&lo)[R + 2], int k, int e, int s1, int par,
+                                               float (&acc)[R]) {
+    switch (shape) {
+        PSC_SHAPE_CASE8(0)
+        PSC_SHAPE_CASE8(8)
+        PSC_SHAPE_CASE8(16)
+        PSC_SHAPE_CASE8(24)
+        PSC_SHAPE_CASE8(32)
+        PSC_SHAPE_CASE8(40)
+        PSC_SHAPE_CASE8(48)
+        default: return run_generic_lds<DT, R>(mask, c, lo, k, e, s1, par, acc);
+    }
+}
+#undef PSC_SHAPE_CASE8
+#undef PSC_SHAPE_CASE
+
+// ------------------------------------------------------------------ kernel
+// LDS = true stages the input rows through per-wave LDS (full-row segments
+// only); LDS = false loads them straight into registers.
+template <int DT, int R, bool LDS>
 __global__ __launch_bounds__(512) void k_conv_stream(const typename Elt<DT>::T* __restrict__ x,
                                                      const int32_t* __restrict__ perm,
                                                      const int32_t* __restrict__ seg_ptr,
@@ -319,7 +526,10 @@ __global__ __launch_bounds__(512) void k_conv_stream(const typename Elt<DT>::T* 
                                                      typename Elt<DT>::T* __restrict__ y, Geo g) {
     using E = Elt<DT>;
     constexpr int ROWS = R + 2;
-    __shared__ float red[kMaxSplit][R][64];     // partial sums of the shares of one filter
+    constexpr int ESZ = int(sizeof(typename E::T));
+    // dynamic LDS: the per-wave row areas (LDS form), then, after all
+    // kernels, the partial sums of the KS shares of a filter
+    extern __shared__ float psc_smem[];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
@@ -357,42 +567,115 @@ __global__ __launch_bounds__(512) void k_conv_stream(const typename Elt<DT>::T* 
         }
     }
     const int plane = g.H * g.W;
-    // byte offset of this lane's column in each of its R+2 input rows of
-    // channel 0; 2^31 (past the buffer range, reads zero) for padding
-    uint32_t vo[ROWS];
-#pragma unroll
-    for (int r = 0; r < ROWS; ++r) {
-        const int row = h0 - 1 + r;
-        vo[r] = (ld_col >= 0 && row >= 0 && row < g.H)
-                    ? uint32_t(nimg * g.cin * plane + row * g.W + ld_col) * uint32_t(sizeof(typename E::T))
-                    : 0x80000000u;
-    }
 
     float acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = 0.f;
 
+    const int* segp = seg_ptr + i * (g.m + 1);
+    int s0 = 0, s1 = 0;
     if (has_filter) {
-        const RunCtx<DT> ctx{cin_idx, vals,
-                             __builtin_amdgcn_make_buffer_rsrc(const_cast<typename E::T*>(x), int16_t(0),
-                                                               g.x_bytes, 0x00020000),
-                             __builtin_amdgcn_readfirstlane(plane * int(sizeof(typename E::T))), g.cin - 1};
-        const int* segp = seg_ptr + i * (g.m + 1);
         const int f0 = segp[0], f1 = segp[g.m];
         // share sp: the sp-th of KS equal contiguous ranges of the filter's
         // kernels, which crosses few pattern segments
         const int len = f1 - f0;
-        const int s0 = f0 + len * sp / g.KS, s1 = f0 + len * (sp + 1) / g.KS;
-        for (int p = 0; p < g.m; ++p) {
-            int k0 = segp[p], k1 = segp[p + 1];
-            k0 = k0 < s0 ? s0 : k0;
-            k1 = k1 > s1 ? s1 : k1;                         // malformed pointers stay in the share
-            if (k0 < k1) run_pattern<DT, R>(g.shape[p], g.mask[p], ctx, vo, k0, k1, acc);
+        s0 = f0 + len * sp / g.KS;
+        s1 = f0 + len * (sp + 1) / g.KS;
+    }
+    const auto xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<typename E::T*>(x), int16_t(0), g.x_bytes,
+                                                      0x00020000);
+
+    if constexpr (!LDS) {
+        // byte offset of this lane's column in each of its R+2 input rows of
+        // channel 0; 2^31 (past the buffer range, reads zero) for padding
+        uint32_t vo[ROWS];
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) {
+            const int row = h0 - 1 + r;
+            vo[r] = (ld_col >= 0 && row >= 0 && row < g.H)
+                        ? uint32_t(nimg * g.cin * plane + row * g.W + ld_col) * uint32_t(ESZ)
+                        : 0x80000000u;
         }
+        if (has_filter) {
+            const RunCtx<DT> ctx{cin_idx, vals, xr, __builtin_amdgcn_readfirstlane(plane * ESZ), g.cin - 1};
+            for (int p = 0; p < g.m; ++p) {
+                int k0 = segp[p], k1 = segp[p + 1];
+                k0 = k0 < s0 ? s0 : k0;
+                k1 = k1 > s1 ? s1 : k1;                     // malformed pointers stay in the share
+                if (k0 < k1) run_pattern<DT, R>(g.shape[p], g.mask[p], ctx, vo, k0, k1, acc);
+            }
+        }
+    } else {
+        // ---- this wave's LDS area: nruns regions of g.region bytes (run j's
+        // data starts 64 bytes in), then 64 zeroed bytes that padding reads
+        const uint32_t area = uint32_t(uintptr_t((const __attribute__((address_space(3))) void*)psc_smem)) +
+                              uint32_t(wave * g.wave_bytes);
+        // copy 0 of the runs, copy 1 kLdsCopy bytes later, then the zero
+        // area; padding reads of copy 1 land kLdsCopy past the zero area,
+        // which is zeroed too
+        const uint32_t zero_at = area + uint32_t(g.wave_bytes - 64 - kLdsCopy);
+        if (lane < 16) *(__attribute__((address_space(3))) float*)(uintptr_t)(zero_at + lane * 4) = 0.f;
+        if (lane < 16) *(__attribute__((address_space(3))) float*)(uintptr_t)(zero_at + kLdsCopy + lane * 4) = 0.f;
+        // runs: the wave's segments grouped by image; run j covers the rows
+        // of image n_first + j that its segments need
+        const int RBn = g.RB;
+        const int u_first = sgrp * g.S;
+        const int u_last = (u_first + g.S < g.U ? u_first + g.S : g.U) - 1;
+        const int n_first = u_first / RBn;
+        LdsCtx<DT> ctx;
+        ctx.xr = xr;
+        ctx.cin_idx = cin_idx;
+        ctx.vals = vals;
+        ctx.chan_bytes = __builtin_amdgcn_readfirstlane(plane * ESZ);
+        ctx.cmax = __builtin_amdgcn_readfirstlane(g.cin - 1);
+        ctx.nruns = __builtin_amdgcn_readfirstlane(u_first <= u_last ? u_last / RBn - n_first + 1 : 0);
+        ctx.vlane = uint32_t(lane) * 16u;
+#pragma unroll
+        for (int j = 0; j < kMaxRuns; ++j) {
+            const int n = n_first + j;
+            const int ua = u_first > n * RBn ? u_first : n * RBn;
+            const int ub = u_last < n * RBn + RBn - 1 ? u_last : n * RBn + RBn - 1;
+            int row_lo = (ua - n * RBn) * R - 1, row_hi = (ub - n * RBn + 1) * R + 1;
+            row_lo = row_lo < 0 ? 0 : row_lo;
+            row_hi = row_hi > g.H ? g.H : row_hi;
+            // wave-uniform values: SGPR operands of the copies
+            ctx.run_base[j] = __builtin_amdgcn_readfirstlane((n * g.cin * plane + row_lo * g.W) * ESZ);
+            ctx.run_lds[j] = __builtin_amdgcn_readfirstlane(int(area) + j * g.region + 64);
+            ctx.run_len[j] = __builtin_amdgcn_readfirstlane(j < ctx.nruns ? (row_hi - row_lo) * g.W * ESZ : 0);
+        }
+        // LDS byte address of each of this lane's rows (zero area for padding)
+        uint32_t lo[ROWS];
+        {
+            const int jn = nimg - n_first;
+            const int ua = u_first > nimg * RBn ? u_first : nimg * RBn;
+            int row_lo = (ua - nimg * RBn) * R - 1;
+            row_lo = row_lo < 0 ? 0 : row_lo;
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) {
+                const int row = h0 - 1 + r;
+                lo[r] = (ld_col >= 0 && row >= 0 && row < g.H)
+                            ? area + uint32_t(jn * g.region + 64 + ((row - row_lo) * g.W + ld_col) * ESZ)
+                            : zero_at;
+            }
+        }
+        if (has_filter && s0 < s1) {
+            dma_rows<DT>(ctx, __builtin_amdgcn_readfirstlane(cin_idx[s0]), 0);
+            int par = 0;
+            for (int p = 0; p < g.m; ++p) {
+                int k0 = segp[p], k1 = segp[p + 1];
+                k0 = k0 < s0 ? s0 : k0;
+                k1 = k1 > s1 ? s1 : k1;                     // malformed pointers stay in the share
+                if (k0 < k1) par = run_pattern_lds<DT, R>(g.shape[p], g.mask[p], ctx, lo, k0, k1, s1, par, acc);
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);            // no copy into LDS is left in flight
     }
 
     // ---- add the KS partial sums of each filter in share order
     if (g.KS > 1) {
+        float (*red)[R][64] = reinterpret_cast<float (*)[R][64]>(psc_smem);
+        // the partial sums reuse the row areas: wait until every wave is done
+        if constexpr (LDS) __syncthreads();
         // the KS waves of filter slot gf use red[0..KS) of their own barrier
         // phase: slots are processed one after another
         for (int slot = 0; slot < g.FW; ++slot) {
@@ -431,9 +714,20 @@ __global__ __launch_bounds__(512) void k_conv_stream(const typename Elt<DT>::T* 
 template <int DT, int R>
 hipError_t launch_r(const PackedView& pk, const ConvArgs& a, const Geo& g, hipStream_t stream) {
     using T = typename Elt<DT>::T;
-    hipLaunchKernelGGL((k_conv_stream<DT, R>), dim3(unsigned(g.nblocks)), dim3(unsigned(g.FW * g.KS * 64)), 0,
-                       stream, static_cast<const T*>(a.x), pk.filter_perm, pk.seg_ptr, pk.cin_idx,
-                       static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), static_cast<T*>(a.y), g);
+    const int waves = g.FW * g.KS;
+    const size_t red = g.KS > 1 ? size_t(g.KS) * R * 64 * sizeof(float) : 0;
+    const size_t rows = g.lds ? size_t(waves) * g.wave_bytes : 0;
+    const size_t smem = red > rows ? red : rows;
+    if (g.lds)
+        hipLaunchKernelGGL((k_conv_stream<DT, R, true>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)),
+                           smem, stream, static_cast<const T*>(a.x), pk.filter_perm, pk.seg_ptr, pk.cin_idx,
+                           static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), static_cast<T*>(a.y),
+                           g);
+    else
+        hipLaunchKernelGGL((k_conv_stream<DT, R, false>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)),
+                           smem, stream, static_cast<const T*>(a.x), pk.filter_perm, pk.seg_ptr, pk.cin_idx,
+                           static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), static_cast<T*>(a.y),
+                           g);
     return hipGetLastError();
 }
 
@@ -509,16 +803,56 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
     const int sgroups = (g.U + g.S - 1) / g.S;
     g.KS = 1;
     while (g.KS < kMaxSplit && int64_t(sgroups) * a.cout * g.KS < 4096 && a.cin >= 16 * g.KS) g.KS *= 2;
-    if (const char* t = getenv("PSC_CONV_TUNE")) {   // experiments: "KS=2"
+    int tune_flags = 0;
+    if (const char* t = getenv("PSC_CONV_TUNE")) {   // experiments: "KS=2", "DIRECT", "LDS"
         if (const char* q = strstr(t, "KS=")) g.KS = atoi(q + 3);
         if (g.KS < 1) g.KS = 1;
         if (g.KS > kMaxSplit) g.KS = kMaxSplit;
+        if (strstr(t, "DIRECT")) tune_flags |= 1;
+        if (strstr(t, "LDS")) tune_flags |= 2;
     }
     g.FW = g.KS >= 4 ? 1 : 4 / g.KS;
     if (g.FW > a.cout) g.FW = a.cout;
     const int fgroups = (a.cout + g.FW - 1) / g.FW;
     g.groups_x = fgroups;
     g.nblocks = fgroups * sgroups;
+    // LDS staging for full-row segments: runs per wave (images its segments
+    // touch) and the LDS bytes of the largest run
+    if (!g.cols_mode) {
+        const int esz = a.dtype == DT_F16 ? 2 : 4;
+        int nruns_max = 0, bytes_max = 0;
+        for (int sg = 0; sg < sgroups; ++sg) {
+            const int uf = sg * g.S, ul = (uf + g.S < g.U ? uf + g.S : g.U) - 1;
+            const int nf = uf / g.RB, nl = ul / g.RB;
+            nruns_max = nruns_max > nl - nf + 1 ? nruns_max : nl - nf + 1;
+            for (int n = nf; n <= nl; ++n) {
+                const int ua = uf > n * g.RB ? uf : n * g.RB;
+                const int ub = ul < n * g.RB + g.RB - 1 ? ul : n * g.RB + g.RB - 1;
+                int lo = (ua - n * g.RB) * R - 1, hi = (ub - n * g.RB + 1) * R + 1;
+                lo = lo < 0 ? 0 : lo;
+                hi = hi > a.h ? a.h : hi;
+                const int bytes = (hi - lo) * a.w * esz;
+                bytes_max = bytes_max > bytes ? bytes_max : bytes;
+            }
+        }
+        // a run's copy spans [data - 63, data + bytes + 1024) around its data
+        g.region = (64 + bytes_max + 1024 + 63) / 64 * 64;
+        // copy 0: the runs, then 64 zero bytes; copy 1 kLdsCopy bytes later
+        g.wave_bytes = kLdsCopy + nruns_max * g.region + 64;
+        // fp16 copies shift the LDS destination in 4-byte steps only: rows of
+        // even width keep every offset a multiple of 4 bytes
+        const bool fits = (bytes_max + 63 + 1023) / 1024 <= kMaxDma && nruns_max <= kMaxRuns &&
+                          nruns_max * g.region + 64 <= kLdsCopy &&
+                          int64_t(g.FW) * g.KS * g.wave_bytes <= 64 * 1024 &&
+                          (a.dtype != DT_F16 || a.w % 2 == 0);
+        // one full-row segment per wave and a grid of about one round of
+        // waves (batch 1 at W >= 32) is bound by the per-kernel latency,
+        // which the direct loads keep shorter
+        const int64_t waves = int64_t(g.nblocks) * g.FW * g.KS;
+        const bool throughput = g.S >= 2 || waves >= 2 * 6 * 1024;
+        g.lds = fits && throughput && !(tune_flags & 1) ? 1 : 0;
+        if (tune_flags & 2) g.lds = fits ? 1 : 0;
+    }
     switch (R) {
         case 8: return a.dtype == DT_F16 ? launch_r<DT_F16, 8>(pk, a, g, stream)
                                          : launch_r<DT_F32, 8>(pk, a, g, stream);
