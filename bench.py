@@ -4,7 +4,10 @@ A step is one forward pass of the whole workload through the HIP path: for
 the VGG-16 stack (default) the 13 pattern-sparse conv layers with fused ReLU
 and the four 2x2 max-pools on a 1x3x224x224 synthetic image; for the other
 workloads every listed layer on its own resident input.  Weights are pruned
-and packed on the GPU (projection, selection, packing) before timing.
+and packed on the GPU (projection, selection, packing) before timing.  The
+step's launches are captured once in a HIP graph and the timed steps are its
+replays (--no-graph times eager launches); per-layer times come from an eager
+pass with HIP events.
 
 Prints ONE JSON line: nonzero-MAC GFLOP/s of the step, ms/step, per-layer
 ms, the roofline of the conv kernel (measured with HIP events on the stream
@@ -38,6 +41,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--details", default=None, help="write per-layer comparisons to this JSON file")
     ap.add_argument("--list", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="time eager launches instead of replays of a captured HIP graph of the step")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 256 MiB device-to-device copy (reference for HBM counters)")
     return ap.parse_args()
@@ -91,6 +96,10 @@ class Net:
                 events[li][1].record()
             if L["pooled"] is not None:
                 B.maxpool2x2(L["y"], L["pooled"])
+
+    def output(self):
+        L = self.layers[-1]
+        return L["pooled"] if L["pooled"] is not None else L["y"]
 
     def nz_flops(self, li):
         lay = self.layers[li]["lay"]
@@ -209,6 +218,8 @@ def main():
         net.step()
     torch.cuda.synchronize()
     K = args.steps
+    # eager steps with HIP events around every conv launch (on the stream the
+    # launches use): per-layer times and the kernel's roofline
     ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
            for _ in net.layers] for _ in range(K)]
     torch.cuda.synchronize()
@@ -216,8 +227,31 @@ def main():
     for k in range(K):
         net.step(ev[k])
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_step = wall * 1e3 / K
+    ms_eager = (time.perf_counter() - t0) * 1e3 / K
+    ms_step, graph = ms_eager, False
+    if not args.no_graph:
+        # the step's 13 conv and 4 pool launches captured once in a HIP graph
+        # and replayed: the timed region is the replays alone
+        eager_out = net.output().clone()
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            net.step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            net.step()
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        if not torch.equal(net.output(), eager_out):
+            raise SystemExit("graph replay of the step differs from the eager step")
+        t0 = time.perf_counter()
+        for _ in range(K):
+            g.replay()
+        torch.cuda.synchronize()
+        ms_step, graph = (time.perf_counter() - t0) * 1e3 / K, True
     layer_ms = [float(np.median([ev[k][li][0].elapsed_time(ev[k][li][1]) for k in range(K)]))
                 for li in range(len(net.layers))]
     layer_mean_ms = [float(np.mean([ev[k][li][0].elapsed_time(ev[k][li][1]) for k in range(K)]))
@@ -242,6 +276,8 @@ def main():
         "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": wl.name, "batch": wl.batch, "layers": len(wl.layers), "m": wl.m,
                    "stack": "conv+relu, 2x2 max-pool after conv2/4/7/10" if wl.chained else "independent layers"},
+        "step_launch": "hip graph replay" if graph else "eager",
+        "ms_per_step_eager": round(ms_eager, 4),
         "ms_per_layer": {L["lay"].name: round(t, 4) for L, t in zip(net.layers, layer_ms)},
         "conv_ms_per_step": round(conv_ms, 4),
         "roofline": roof,
