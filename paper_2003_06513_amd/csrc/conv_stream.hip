@@ -43,6 +43,14 @@
 #include "common.h"
 #include "launch.h"
 
+// Scalar buffer loads (the LLVM intrinsic, declared by its name).
+typedef int32_t psc_i32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t psc_i32x2 __attribute__((ext_vector_type(2)));
+typedef float psc_f32x4 __attribute__((ext_vector_type(4)));
+__device__ int32_t psc_sbuf_i32(psc_i32x4, int32_t, int32_t) __asm("llvm.amdgcn.s.buffer.load.i32");
+__device__ psc_i32x2 psc_sbuf_i32x2(psc_i32x4, int32_t, int32_t) __asm("llvm.amdgcn.s.buffer.load.v2i32");
+__device__ psc_f32x4 psc_sbuf_f32x4(psc_i32x4, int32_t, int32_t) __asm("llvm.amdgcn.s.buffer.load.v4f32");
+
 namespace psc {
 namespace {
 
@@ -62,6 +70,8 @@ constexpr Centre3Table kCentre3{};
 
 constexpr int kMaxSplit = 8;
 
+typedef psc_i32x4 int32x4;
+
 struct Geo {
     int n, cin, H, W, cout, m;
     int S;          // segments per wave
@@ -74,6 +84,7 @@ struct Geo {
     int groups_x;   // filter groups (fastest varying logical block index)
     int nblocks;    // total workgroups
     int x_bytes;    // bytes of x (the buffer range), at most 2^31
+    int keep;       // kept kernels (entries of cin_idx)
     int relu;
     int lds;        // 1: input rows staged through per-wave LDS (full-row segments only)
     int region;     // LDS bytes reserved per run of rows
@@ -96,22 +107,24 @@ struct Geo {
 #define PSC_A(i) [a##i] "+v"(acc[i])
 #define PSC_X(i) [x##i] "v"(xr[DR + i])
 
-template <int R, int DR, int DS, bool WS> struct Tap;   // WS: weight may stay in an SGPR
+// WS: the weight may stay in an SGPR; NW: the asm starts with the two wait
+// states a DPP read needs after a VALU write of one of its operands.
+template <int R, int DR, int DS, bool WS, bool NW> struct Tap;
 
-#define PSC_TAPS(DSV, WSV, NOP, L, WC)                                                                \
-    template <int DR> struct Tap<2, DR, DSV, WSV> {                                                  \
+#define PSC_TAPS(DSV, WSV, NWV, NOP, L, WC)                                                           \
+    template <int DR> struct Tap<2, DR, DSV, WSV, NWV> {                                             \
         __device__ __forceinline__ static void run(float (&acc)[2], const float (&xr)[4], float w) {  \
             asm volatile(NOP L(0) L(1) : PSC_A(0), PSC_A(1) : PSC_X(0), PSC_X(1), [w] WC(w));         \
         }                                                                                             \
     };                                                                                                \
-    template <int DR> struct Tap<4, DR, DSV, WSV> {                                                  \
+    template <int DR> struct Tap<4, DR, DSV, WSV, NWV> {                                                  \
         __device__ __forceinline__ static void run(float (&acc)[4], const float (&xr)[6], float w) {  \
             asm volatile(NOP L(0) L(1) L(2) L(3)                                                      \
                          : PSC_A(0), PSC_A(1), PSC_A(2), PSC_A(3)                                     \
                          : PSC_X(0), PSC_X(1), PSC_X(2), PSC_X(3), [w] WC(w));                        \
         }                                                                                             \
     };                                                                                                \
-    template <int DR> struct Tap<7, DR, DSV, WSV> {                                                  \
+    template <int DR> struct Tap<7, DR, DSV, WSV, NWV> {                                                  \
         __device__ __forceinline__ static void run(float (&acc)[7], const float (&xr)[9], float w) {  \
             asm volatile(NOP L(0) L(1) L(2) L(3) L(4) L(5) L(6)                                       \
                          : PSC_A(0), PSC_A(1), PSC_A(2), PSC_A(3), PSC_A(4), PSC_A(5), PSC_A(6)       \
@@ -119,7 +132,7 @@ template <int R, int DR, int DS, bool WS> struct Tap;   // WS: weight may stay i
                            [w] WC(w));                                                                \
         }                                                                                             \
     };                                                                                                \
-    template <int DR> struct Tap<8, DR, DSV, WSV> {                                                  \
+    template <int DR> struct Tap<8, DR, DSV, WSV, NWV> {                                                  \
         __device__ __forceinline__ static void run(float (&acc)[8], const float (&xr)[10], float w) { \
             asm volatile(NOP L(0) L(1) L(2) L(3) L(4) L(5) L(6) L(7)                                  \
                          : PSC_A(0), PSC_A(1), PSC_A(2), PSC_A(3), PSC_A(4), PSC_A(5), PSC_A(6),      \
@@ -135,12 +148,12 @@ template <int R, int DR, int DS, bool WS> struct Tap;   // WS: weight may stay i
 #define PSC_WS(w) "s"(w)
 // kernel column 0 reads x at w - 1 (the lane to the left), column 2 at w + 1
 // (the lane to the right), column 1 the lane's own column
-PSC_TAPS(0, false, "s_nop 4\n", PSC_L_SHR, PSC_WV)
-PSC_TAPS(0, true, "s_nop 4\n", PSC_L_SHR, PSC_WV)
-PSC_TAPS(1, false, "", PSC_FC, PSC_WV)
-PSC_TAPS(1, true, "", PSC_FC, PSC_WS)
-PSC_TAPS(2, false, "s_nop 4\n", PSC_L_SHL, PSC_WV)
-PSC_TAPS(2, true, "s_nop 4\n", PSC_L_SHL, PSC_WV)
+PSC_TAPS(0, false, true, "s_nop 1\n", PSC_L_SHR, PSC_WV)
+PSC_TAPS(0, false, false, "", PSC_L_SHR, PSC_WV)
+PSC_TAPS(1, false, false, "", PSC_FC, PSC_WV)
+PSC_TAPS(1, true, false, "", PSC_FC, PSC_WS)
+PSC_TAPS(2, false, true, "s_nop 1\n", PSC_L_SHL, PSC_WV)
+PSC_TAPS(2, false, false, "", PSC_L_SHL, PSC_WV)
 #undef PSC_WS
 #undef PSC_WV
 #undef PSC_L_SHL
@@ -153,11 +166,15 @@ PSC_TAPS(2, true, "s_nop 4\n", PSC_L_SHL, PSC_WV)
 #undef PSC_SHL
 #undef PSC_SHR
 
-// fp32 weights arrive in SGPRs (scalar loads); fp16 ones are widened into
-// VGPRs.
-template <int Q, int R, bool WS>
+// Tap at position Q of the 3x3 kernel.  Same-column taps take the weight
+// from an SGPR when WS (fp32 scalar loads); the shifted (DPP) taps take it
+// from a VGPR and, unless NW is false, start with two wait states.
+template <int Q, int R, bool WS, bool NW = true>
 __device__ __forceinline__ void tap_q(float (&acc)[R], const float (&xr)[R + 2], float wv) {
-    Tap<R, Q / 3, Q % 3, WS>::run(acc, xr, wv);
+    if constexpr (Q % 3 == 1)
+        Tap<R, Q / 3, 1, WS, false>::run(acc, xr, wv);
+    else
+        Tap<R, Q / 3, Q % 3, false, NW>::run(acc, xr, wv);
 }
 
 template <int R, bool WS>
@@ -172,6 +189,52 @@ __device__ __forceinline__ void tap_dyn(int q, float (&acc)[R], const float (&xr
         case 6: tap_q<6, R, WS>(acc, xr, wv); break;
         case 7: tap_q<7, R, WS>(acc, xr, wv); break;
         default: tap_q<8, R, WS>(acc, xr, wv); break;
+    }
+}
+
+// Copy of a weight into a VGPR, as an asm statement so that it stays ahead
+// of the taps that follow it.
+__device__ __forceinline__ float to_vgpr(float w) {
+    float v;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(v) : "s"(w));
+    return v;
+}
+
+// The 4 taps of one kernel of a centre+3 shape.  fp32 with R >= 3: the
+// weights of the shifted taps are copied to VGPRs first, the same-column
+// taps (the centre at least) run next and the shifted taps last, so at least
+// R FMAs separate any VALU write from a DPP read and the shifted taps need no
+// wait states.  Otherwise the taps run in position order with wait states.
+template <int J, int Q, int R>
+__device__ __forceinline__ void tap_same(float (&a)[R], const float (&x)[R + 2], const float (&w)[4]) {
+    if constexpr (Q % 3 == 1) tap_q<Q, R, true>(a, x, w[J]);
+}
+template <int J, int Q, int R>
+__device__ __forceinline__ void tap_shift(float (&a)[R], const float (&x)[R + 2], const float (&wv)[4]) {
+    if constexpr (Q % 3 != 1) tap_q<Q, R, false, false>(a, x, wv[J]);
+}
+template <int DT, int R, int Q0, int Q1, int Q2, int Q3>
+__device__ __forceinline__ void kernel_taps(float (&a)[R], const float (&x)[R + 2], const float (&w)[4]) {
+    if constexpr (DT == DT_F32 && R >= 3) {
+        float wv[4] = {w[0], w[1], w[2], w[3]};
+        if constexpr (Q0 % 3 != 1) wv[0] = to_vgpr(w[0]);
+        if constexpr (Q1 % 3 != 1) wv[1] = to_vgpr(w[1]);
+        if constexpr (Q2 % 3 != 1) wv[2] = to_vgpr(w[2]);
+        if constexpr (Q3 % 3 != 1) wv[3] = to_vgpr(w[3]);
+        tap_same<0, Q0, R>(a, x, w);
+        tap_same<1, Q1, R>(a, x, w);
+        tap_same<2, Q2, R>(a, x, w);
+        tap_same<3, Q3, R>(a, x, w);
+        tap_shift<0, Q0, R>(a, x, wv);
+        tap_shift<1, Q1, R>(a, x, wv);
+        tap_shift<2, Q2, R>(a, x, wv);
+        tap_shift<3, Q3, R>(a, x, wv);
+    } else {
+        constexpr bool WS = DT == DT_F32;
+        tap_q<Q0, R, WS>(a, x, w[0]);
+        tap_q<Q1, R, WS>(a, x, w[1]);
+        tap_q<Q2, R, WS>(a, x, w[2]);
+        tap_q<Q3, R, WS>(a, x, w[3]);
     }
 }
 
@@ -190,27 +253,53 @@ struct NthBit {
 };
 
 // ------------------------------------------------------------------ runs
-template <int DT>
-struct RunCtx {
-    const int32_t* __restrict__ cin_idx;
-    const typename Elt<DT>::T* __restrict__ vals;
-    __amdgpu_buffer_rsrc_t xr;   // x, bounded to its size
-    int chan_bytes;              // bytes of one input channel plane
-    int cmax;                    // last input channel
+struct RunCtx;
+
+// Scalar buffer loads (wave-uniform, into SGPRs) of the packed kernels'
+// channel indices and weights: 32-bit offsets from a descriptor, no 64-bit
+// address arithmetic per kernel.
+
+__device__ __forceinline__ int32x4 scalar_rsrc(const void* p, int bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(p);
+    return int32x4{int32_t(uint32_t(a)), int32_t(uint32_t(a >> 32) & 0xffffu), bytes, 0x00020000};
+}
+
+struct Meta {
+    int32x4 ci;   // cin_idx, keep entries
+    int32x4 w;    // values, keep * 4 weights
 };
 
+// Channel index of kernel k (callers keep k inside the filter's kernels).
+__device__ __forceinline__ int meta_ci(const Meta& m, int k) { return psc_sbuf_i32(m.ci, k * 4, 0); }
+
+// The 4 weights of kernel k as floats (fp32: SGPRs; fp16: widened).
 template <int DT>
-__device__ __forceinline__ void load_w4(const typename Elt<DT>::T* __restrict__ vals, int k, float (&wv)[4]) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) wv[j] = Elt<DT>::load(vals, int64_t(k) * 4 + j);
+__device__ __forceinline__ void meta_w(const Meta& m, int k, float (&w)[4]) {
+    if constexpr (DT == DT_F32) {
+        const psc_f32x4 v = psc_sbuf_f32x4(m.w, k * 16, 0);
+        w[0] = v.x, w[1] = v.y, w[2] = v.z, w[3] = v.w;
+    } else {
+        const psc_i32x2 v = psc_sbuf_i32x2(m.w, k * 8, 0);
+        w[0] = float(__builtin_bit_cast(_Float16, uint16_t(uint32_t(v.x))));
+        w[1] = float(__builtin_bit_cast(_Float16, uint16_t(uint32_t(v.x) >> 16)));
+        w[2] = float(__builtin_bit_cast(_Float16, uint16_t(uint32_t(v.y))));
+        w[3] = float(__builtin_bit_cast(_Float16, uint16_t(uint32_t(v.y) >> 16)));
+    }
 }
+
+struct RunCtx {
+    Meta m;
+    __amdgpu_buffer_rsrc_t xr;   // x, bounded to its size
+    int chan_bytes;              // bytes of one input channel plane
+};
 
 // The R+2 input rows of channel ci in this lane's column (zero outside the
 // image: those offsets lie past the buffer range).
 template <int DT, int R>
-__device__ __forceinline__ void load_rows(const RunCtx<DT>& c, const uint32_t (&vo)[R + 2], int ci,
+__device__ __forceinline__ void load_rows(const RunCtx& c, const uint32_t (&vo)[R + 2], int ci,
                                           float (&xr)[R + 2]) {
-    ci = ci < 0 ? 0 : (ci > c.cmax ? c.cmax : ci);    // a malformed index stays inside x
+    // every offset of a buffer load is range-checked: a malformed channel
+    // index reads zeros or other data of x, never memory outside it
     const int soff = __builtin_amdgcn_readfirstlane(ci * c.chan_bytes);   // wave-uniform: an SGPR operand
 #pragma unroll
     for (int r = 0; r < R + 2; ++r) {
@@ -225,26 +314,26 @@ __device__ __forceinline__ void load_rows(const RunCtx<DT>& c, const uint32_t (&
 // trip: the rows of one load while the other's FMAs run; metadata is read two
 // kernels ahead; the single loop exit keeps the accumulators in place.
 template <int DT, int R, class TapFn>
-__device__ __forceinline__ void run_kernels(const RunCtx<DT>& c, const uint32_t (&vo)[R + 2], int k, int e,
+__device__ __forceinline__ void run_kernels(const RunCtx& c, const uint32_t (&vo)[R + 2], int k, int e,
                                             float (&acc)[R], TapFn taps) {
     const int last = e - 1;
     float wA[4], wB[4];
-    load_w4<DT>(c.vals, k, wA);
+    meta_w<DT>(c.m, k, wA);
     int kk = k + 1 <= last ? k + 1 : last;
-    int ciB = __builtin_amdgcn_readfirstlane(c.cin_idx[kk]);
-    load_w4<DT>(c.vals, kk, wB);
+    int ciB = meta_ci(c.m, kk);
+    meta_w<DT>(c.m, kk, wB);
     float xA[R + 2], xB[R + 2];
-    load_rows<DT, R>(c, vo, __builtin_amdgcn_readfirstlane(c.cin_idx[k]), xA);
+    load_rows<DT, R>(c, vo, meta_ci(c.m, k), xA);
     while (k + 1 < e) {
         load_rows<DT, R>(c, vo, ciB, xB);                      // rows of kernel k+1
         kk = k + 2 <= last ? k + 2 : last;
-        const int ciA2 = __builtin_amdgcn_readfirstlane(c.cin_idx[kk]);
+        const int ciA2 = meta_ci(c.m, kk);
         float wA2[4];
-        load_w4<DT>(c.vals, kk, wA2);
+        meta_w<DT>(c.m, kk, wA2);
         kk = k + 3 <= last ? k + 3 : last;
-        const int ciB2 = __builtin_amdgcn_readfirstlane(c.cin_idx[kk]);
+        const int ciB2 = meta_ci(c.m, kk);
         float wB2[4];
-        load_w4<DT>(c.vals, kk, wB2);
+        meta_w<DT>(c.m, kk, wB2);
         taps(acc, xA, wA);                                     // kernel k
         load_rows<DT, R>(c, vo, ciA2, xA);                     // rows of kernel k+2
         taps(acc, xB, wB);                                     // kernel k+1
@@ -257,22 +346,18 @@ __device__ __forceinline__ void run_kernels(const RunCtx<DT>& c, const uint32_t 
 }
 
 template <int DT, int R, int MASK>
-__device__ __forceinline__ void run_shape(const RunCtx<DT>& c, const uint32_t (&vo)[R + 2], int k, int e,
+__device__ __forceinline__ void run_shape(const RunCtx& c, const uint32_t (&vo)[R + 2], int k, int e,
                                           float (&acc)[R]) {
     constexpr int Q0 = NthBit<MASK, 0>::value(), Q1 = NthBit<MASK, 1>::value();
     constexpr int Q2 = NthBit<MASK, 2>::value(), Q3 = NthBit<MASK, 3>::value();
-    constexpr bool WS = DT == DT_F32;
     run_kernels<DT, R>(c, vo, k, e, acc, [](float (&a)[R], const float (&x)[R + 2], const float (&w)[4]) {
-        tap_q<Q0, R, WS>(a, x, w[0]);
-        tap_q<Q1, R, WS>(a, x, w[1]);
-        tap_q<Q2, R, WS>(a, x, w[2]);
-        tap_q<Q3, R, WS>(a, x, w[3]);
+        kernel_taps<DT, R, Q0, Q1, Q2, Q3>(a, x, w);
     });
 }
 
 // Any 4-of-9 mask: the taps are chosen per kernel by uniform branches.
 template <int DT, int R>
-__device__ __forceinline__ void run_generic(unsigned mask, const RunCtx<DT>& c, const uint32_t (&vo)[R + 2],
+__device__ __forceinline__ void run_generic(unsigned mask, const RunCtx& c, const uint32_t (&vo)[R + 2],
                                             int k, int e, float (&acc)[R]) {
     int q0 = 4, q1 = 4, q2 = 4, q3 = 4, seen = 0;
 #pragma unroll
@@ -311,17 +396,16 @@ constexpr int kLdsCopy = 4096; // bytes between the two copies of a wave's runs
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-template <int DT>
+// NR: runs per wave the code is compiled for (1, or up to kMaxRuns).
+template <int NR>
 struct LdsCtx {
+    Meta m;
     __amdgpu_buffer_rsrc_t xr;            // x, bounded to its size
-    const int32_t* __restrict__ cin_idx;
-    const typename Elt<DT>::T* __restrict__ vals;
     int chan_bytes;                       // bytes of one input channel plane
-    int cmax;                             // last input channel
     int nruns;
-    int run_base[kMaxRuns];               // byte offset in x of run j, channel 0
-    int run_lds[kMaxRuns];                // LDS address of run j's first byte
-    int run_len[kMaxRuns];                // bytes of run j
+    int run_base[NR];                     // byte offset in x of run j, channel 0
+    int run_lds[NR];                      // LDS address of run j's first byte
+    int run_len[NR];                      // bytes of run j
     uint32_t vlane;                       // lane * 16
 };
 
@@ -337,14 +421,15 @@ constexpr int kWaitLgkm0 = 0xC07F;        // lgkmcnt(0)
 // shifted back by the same misalignment, so byte t of run j always lands at
 // run_lds[j] + t.  Bytes past the end of x read as zero (every offset of a
 // buffer load is range-checked).
-template <int DT>
-__device__ __forceinline__ void dma_rows(const LdsCtx<DT>& c, int ci, int buf) {
+template <int NR>
+__device__ __forceinline__ void dma_rows(const LdsCtx<NR>& c, int ci, int buf) {
 #if defined(__HIP_DEVICE_COMPILE__)   // the 16-byte form exists only for the gfx950 device pass
-    ci = ci < 0 ? 0 : (ci > c.cmax ? c.cmax : ci);        // a malformed index stays inside x
+    // a malformed channel index reads zeros or other data of x (every offset
+    // of a buffer load is range-checked)
     const int coff = ci * c.chan_bytes;
 #pragma unroll
-    for (int j = 0; j < kMaxRuns; ++j) {
-        if (j < c.nruns) {
+    for (int j = 0; j < NR; ++j) {
+        if (NR == 1 || j < c.nruns) {
             const int start = c.run_base[j] + coff;
             const int mis = start & 63;
             const int soff = start - mis;
@@ -375,75 +460,74 @@ __device__ __forceinline__ void read_rows(const uint32_t (&lo)[R + 2], float (&x
 }
 
 // One kernel whose rows sit (or are arriving) in copy B of the wave's LDS
-// area: wait for them, start the copy of kernel k+1 (also across the segment
-// end, for the next segment) into the other copy, read this lane's rows,
-// fetch the metadata of the kernels ahead, run the FMAs.
-template <int DT, int R, int B, class TapFn>
-__device__ __forceinline__ void lds_trip(const LdsCtx<DT>& c, const uint32_t (&lo)[R + 2], int k, int s1,
-                                         float (&w)[4], int& ci1, float (&acc)[R], TapFn taps) {
+// area: wait for them, start the copy of kernel k+1 (channel ci; also across
+// the segment end, for the next segment) into the other copy, read this
+// lane's rows and run the FMAs with the weights w of kernel k; then refill w
+// and ci with the weights of kernel k+2 and the channel of kernel k+3, for
+// the next trip of the same copy.
+template <int DT, int R, int NR, int B, class TapFn>
+__device__ __forceinline__ void lds_trip(const LdsCtx<NR>& c, const uint32_t (&lo)[R + 2], int k, int s1,
+                                         float (&w)[4], int& ci, float (&acc)[R], TapFn taps) {
     const int last = s1 - 1;
     __builtin_amdgcn_s_waitcnt(kWaitVm0);                // rows of kernel k are in LDS
     asm volatile("" ::: "memory");
-    if (k + 1 < s1) dma_rows<DT>(c, ci1, B ^ 1);          // rows of kernel k+1
+    if (k + 1 < s1) dma_rows<NR>(c, ci, B ^ 1);           // rows of kernel k+1
     float xr[R + 2];
     read_rows<DT, R, B * kLdsCopy>(lo, xr);
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);              // rows in registers
     asm volatile("" ::: "memory");
-    float wn[4];
-    load_w4<DT>(c.vals, k + 1 <= last ? k + 1 : last, wn);
-    const int ci2 = __builtin_amdgcn_readfirstlane(c.cin_idx[k + 2 <= last ? k + 2 : last]);
     taps(acc, xr, w);
-    w[0] = wn[0], w[1] = wn[1], w[2] = wn[2], w[3] = wn[3];
-    ci1 = ci2;
+    meta_w<DT>(c.m, k + 2 <= last ? k + 2 : last, w);
+    ci = meta_ci(c.m, k + 3 <= last ? k + 3 : last);
 }
 
 // Kernels [k, e) of one pattern segment, the first one's rows in copy B0.
-// Pairs of kernels per trip (one in each copy), an odd last one after the
-// loop: the single loop exit keeps the accumulators in place.  Returns the
-// copy that kernel e's rows go to.
-template <int DT, int R, int B0, class TapFn>
-__device__ __forceinline__ int run_pairs_lds(const LdsCtx<DT>& c, const uint32_t (&lo)[R + 2], int k, int e,
+// Pairs of kernels per trip, one in each copy.  Each copy has its own set of
+// weight and channel registers, refilled two kernels ahead, so every
+// prefetch is consumed only after the loop's back edge.  An odd last kernel
+// runs after the loop: the single loop exit keeps the accumulators in place.
+// Returns the copy that kernel e's rows go to.
+template <int DT, int R, int NR, int B0, class TapFn>
+__device__ __forceinline__ int run_pairs_lds(const LdsCtx<NR>& c, const uint32_t (&lo)[R + 2], int k, int e,
                                              int s1, float (&acc)[R], TapFn taps) {
     const int last = s1 - 1;
-    float w[4];
-    load_w4<DT>(c.vals, k, w);
-    int ci1 = __builtin_amdgcn_readfirstlane(c.cin_idx[k + 1 <= last ? k + 1 : last]);
+    float wA[4], wB[4];
+    meta_w<DT>(c.m, k, wA);
+    meta_w<DT>(c.m, k + 1 <= last ? k + 1 : last, wB);
+    int ciA = meta_ci(c.m, k + 1 <= last ? k + 1 : last);
+    int ciB = meta_ci(c.m, k + 2 <= last ? k + 2 : last);
     while (k + 1 < e) {
-        lds_trip<DT, R, B0>(c, lo, k, s1, w, ci1, acc, taps);
-        lds_trip<DT, R, B0 ^ 1>(c, lo, k + 1, s1, w, ci1, acc, taps);
+        lds_trip<DT, R, NR, B0>(c, lo, k, s1, wA, ciA, acc, taps);
+        lds_trip<DT, R, NR, B0 ^ 1>(c, lo, k + 1, s1, wB, ciB, acc, taps);
         k += 2;
     }
     if (k < e) {
-        lds_trip<DT, R, B0>(c, lo, k, s1, w, ci1, acc, taps);
+        lds_trip<DT, R, NR, B0>(c, lo, k, s1, wA, ciA, acc, taps);
         return B0 ^ 1;
     }
     return B0;
 }
 
-template <int DT, int R, class TapFn>
-__device__ __forceinline__ int run_kernels_lds(const LdsCtx<DT>& c, const uint32_t (&lo)[R + 2], int k, int e,
+template <int DT, int R, int NR, class TapFn>
+__device__ __forceinline__ int run_kernels_lds(const LdsCtx<NR>& c, const uint32_t (&lo)[R + 2], int k, int e,
                                                int s1, int par, float (&acc)[R], TapFn taps) {
-    return par == 0 ? run_pairs_lds<DT, R, 0>(c, lo, k, e, s1, acc, taps)
-                    : run_pairs_lds<DT, R, 1>(c, lo, k, e, s1, acc, taps);
+    return par == 0 ? run_pairs_lds<DT, R, NR, 0>(c, lo, k, e, s1, acc, taps)
+                    : run_pairs_lds<DT, R, NR, 1>(c, lo, k, e, s1, acc, taps);
 }
 
-template <int DT, int R, int MASK>
-__device__ __forceinline__ int run_shape_lds(const LdsCtx<DT>& c, const uint32_t (&lo)[R + 2], int k, int e,
+template <int DT, int R, int NR, int MASK>
+__device__ __forceinline__ int run_shape_lds(const LdsCtx<NR>& c, const uint32_t (&lo)[R + 2], int k, int e,
                                              int s1, int par, float (&acc)[R]) {
     constexpr int Q0 = NthBit<MASK, 0>::value(), Q1 = NthBit<MASK, 1>::value();
     constexpr int Q2 = NthBit<MASK, 2>::value(), Q3 = NthBit<MASK, 3>::value();
-    constexpr bool WS = DT == DT_F32;
-    return run_kernels_lds<DT, R>(c, lo, k, e, s1, par, acc,
-                                  [](float (&a)[R], const float (&x)[R + 2], const float (&w)[4]) {
-        tap_q<Q0, R, WS>(a, x, w[0]);
-        tap_q<Q1, R, WS>(a, x, w[1]);
-        tap_q<Q2, R, WS>(a, x, w[2]);
-        tap_q<Q3, R, WS>(a, x, w[3]);
+    return run_kernels_lds<DT, R, NR>(c, lo, k, e, s1, par, acc,
+                                      [](float (&a)[R], const float (&x)[R + 2], const float (&w)[4]) {
+        kernel_taps<DT, R, Q0, Q1, Q2, Q3>(a, x, w);
     });
 }
 
-template <int DT, int R>
-__device__ __forceinline__ int run_generic_lds(unsigned mask, const LdsCtx<DT>& c, const uint32_t (&lo)[R + 2],
+template <int DT, int R, int NR>
+__device__ __forceinline__ int run_generic_lds(unsigned mask, const LdsCtx<NR>& c, const uint32_t (&lo)[R + 2],
                                                int k, int e, int s1, int par, float (&acc)[R]) {
     int q0 = 4, q1 = 4, q2 = 4, q3 = 4, seen = 0;
 #pragma unroll
@@ -457,8 +541,8 @@ __device__ __forceinline__ int run_generic_lds(unsigned mask, const LdsCtx<DT>& 
         }
     }
     constexpr bool WS = DT == DT_F32;
-    return run_kernels_lds<DT, R>(c, lo, k, e, s1, par, acc,
-                                  [=](float (&a)[R], const float (&x)[R + 2], const float (&w)[4]) {
+    return run_kernels_lds<DT, R, NR>(c, lo, k, e, s1, par, acc,
+                                      [=](float (&a)[R], const float (&x)[R + 2], const float (&w)[4]) {
         tap_dyn<R, WS>(q0, a, x, w[0]);
         tap_dyn<R, WS>(q1, a, x, w[1]);
         tap_dyn<R, WS>(q2, a, x, w[2]);
@@ -473,7 +557,7 @@ __device__ __forceinline__ int run_generic_lds(unsigned mask, const LdsCtx<DT>& 
     PSC_SHAPE_CASE(I + 4) PSC_SHAPE_CASE(I + 5) PSC_SHAPE_CASE(I + 6) PSC_SHAPE_CASE(I + 7)
 
 template <int DT, int R>
-__device__ __forceinline__ void run_pattern(int shape, unsigned mask, const RunCtx<DT>& c,
+__device__ __forceinline__ void run_pattern(int shape, unsigned mask, const RunCtx& c,
                                             const uint32_t (&vo)[R + 2], int k, int e, float (&acc)[R]) {
     switch (shape) {
         PSC_SHAPE_CASE8(0)
@@ -490,13 +574,13 @@ __device__ __forceinline__ void run_pattern(int shape, unsigned mask, const RunC
 #undef PSC_SHAPE_CASE
 
 #define PSC_SHAPE_CASE(I) \
-    case I: return run_shape_lds<DT, R, kCentre3.code[I]>(c, lo, k, e, s1, par, acc);
+    case I: return run_shape_lds<DT, R, NR, kCentre3.code[I]>(c, lo, k, e, s1, par, acc);
 #define PSC_SHAPE_CASE8(I)                                                                     \
     PSC_SHAPE_CASE(I) PSC_SHAPE_CASE(I + 1) PSC_SHAPE_CASE(I + 2) PSC_SHAPE_CASE(I + 3)        \
     PSC_SHAPE_CASE(I + 4) PSC_SHAPE_CASE(I + 5) PSC_SHAPE_CASE(I + 6) PSC_SHAPE_CASE(I + 7)
 
-template <int DT, int R>
-__device__ __forceinline__ int run_pattern_lds(int shape, unsigned mask, const LdsCtx<DT>& c,
+template <int DT, int R, int NR>
+__device__ __forceinline__ int run_pattern_lds(int shape, unsigned mask, const LdsCtx<NR>& c,
                                                const uint32_t (&lo)[R + 2], int k, int e, int s1, int par,
                                                float (&acc)[R]) {
     switch (shape) {
@@ -507,7 +591,7 @@ __device__ __forceinline__ int run_pattern_lds(int shape, unsigned mask, const L
         PSC_SHAPE_CASE8(32)
         PSC_SHAPE_CASE8(40)
         PSC_SHAPE_CASE8(48)
-        default: return run_generic_lds<DT, R>(mask, c, lo, k, e, s1, par, acc);
+        default: return run_generic_lds<DT, R, NR>(mask, c, lo, k, e, s1, par, acc);
     }
 }
 #undef PSC_SHAPE_CASE8
@@ -515,8 +599,9 @@ __device__ __forceinline__ int run_pattern_lds(int shape, unsigned mask, const L
 
 // ------------------------------------------------------------------ kernel
 // LDS = true stages the input rows through per-wave LDS (full-row segments
-// only); LDS = false loads them straight into registers.
-template <int DT, int R, bool LDS>
+// only; NR: runs per wave compiled for); LDS = false loads them straight
+// into registers.
+template <int DT, int R, bool LDS, int NR>
 __global__ __launch_bounds__(512) void k_conv_stream(const typename Elt<DT>::T* __restrict__ x,
                                                      const int32_t* __restrict__ perm,
                                                      const int32_t* __restrict__ seg_ptr,
@@ -584,6 +669,7 @@ __global__ __launch_bounds__(512) void k_conv_stream(const typename Elt<DT>::T* 
     }
     const auto xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<typename E::T*>(x), int16_t(0), g.x_bytes,
                                                       0x00020000);
+    const Meta meta{scalar_rsrc(cin_idx, g.keep * 4), scalar_rsrc(vals, g.keep * 4 * ESZ)};
 
     if constexpr (!LDS) {
         // byte offset of this lane's column in each of its R+2 input rows of
@@ -597,7 +683,7 @@ __global__ __launch_bounds__(512) void k_conv_stream(const typename Elt<DT>::T* 
                         : 0x80000000u;
         }
         if (has_filter) {
-            const RunCtx<DT> ctx{cin_idx, vals, xr, __builtin_amdgcn_readfirstlane(plane * ESZ), g.cin - 1};
+            const RunCtx ctx{meta, xr, __builtin_amdgcn_readfirstlane(plane * ESZ)};
             for (int p = 0; p < g.m; ++p) {
                 int k0 = segp[p], k1 = segp[p + 1];
                 k0 = k0 < s0 ? s0 : k0;
@@ -622,16 +708,14 @@ __global__ __launch_bounds__(512) void k_conv_stream(const typename Elt<DT>::T* 
         const int u_first = sgrp * g.S;
         const int u_last = (u_first + g.S < g.U ? u_first + g.S : g.U) - 1;
         const int n_first = u_first / RBn;
-        LdsCtx<DT> ctx;
+        LdsCtx<NR> ctx;
+        ctx.m = meta;
         ctx.xr = xr;
-        ctx.cin_idx = cin_idx;
-        ctx.vals = vals;
         ctx.chan_bytes = __builtin_amdgcn_readfirstlane(plane * ESZ);
-        ctx.cmax = __builtin_amdgcn_readfirstlane(g.cin - 1);
         ctx.nruns = __builtin_amdgcn_readfirstlane(u_first <= u_last ? u_last / RBn - n_first + 1 : 0);
         ctx.vlane = uint32_t(lane) * 16u;
 #pragma unroll
-        for (int j = 0; j < kMaxRuns; ++j) {
+        for (int j = 0; j < NR; ++j) {
             const int n = n_first + j;
             const int ua = u_first > n * RBn ? u_first : n * RBn;
             const int ub = u_last < n * RBn + RBn - 1 ? u_last : n * RBn + RBn - 1;
@@ -659,13 +743,13 @@ __global__ __launch_bounds__(512) void k_conv_stream(const typename Elt<DT>::T* 
             }
         }
         if (has_filter && s0 < s1) {
-            dma_rows<DT>(ctx, __builtin_amdgcn_readfirstlane(cin_idx[s0]), 0);
+            dma_rows<NR>(ctx, meta_ci(meta, s0), 0);
             int par = 0;
             for (int p = 0; p < g.m; ++p) {
                 int k0 = segp[p], k1 = segp[p + 1];
                 k0 = k0 < s0 ? s0 : k0;
                 k1 = k1 > s1 ? s1 : k1;                     // malformed pointers stay in the share
-                if (k0 < k1) par = run_pattern_lds<DT, R>(g.shape[p], g.mask[p], ctx, lo, k0, k1, s1, par, acc);
+                if (k0 < k1) par = run_pattern_lds<DT, R, NR>(g.shape[p], g.mask[p], ctx, lo, k0, k1, s1, par, acc);
             }
         }
         __builtin_amdgcn_s_waitcnt(kWaitVm0);            // no copy into LDS is left in flight
@@ -718,13 +802,18 @@ hipError_t launch_r(const PackedView& pk, const ConvArgs& a, const Geo& g, hipSt
     const size_t red = g.KS > 1 ? size_t(g.KS) * R * 64 * sizeof(float) : 0;
     const size_t rows = g.lds ? size_t(waves) * g.wave_bytes : 0;
     const size_t smem = red > rows ? red : rows;
-    if (g.lds)
-        hipLaunchKernelGGL((k_conv_stream<DT, R, true>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)),
+    if (g.lds == 1)
+        hipLaunchKernelGGL((k_conv_stream<DT, R, true, 1>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)),
                            smem, stream, static_cast<const T*>(a.x), pk.filter_perm, pk.seg_ptr, pk.cin_idx,
                            static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), static_cast<T*>(a.y),
                            g);
+    else if (g.lds > 1)
+        hipLaunchKernelGGL((k_conv_stream<DT, R, true, kMaxRuns>), dim3(unsigned(g.nblocks)),
+                           dim3(unsigned(waves * 64)), smem, stream, static_cast<const T*>(a.x), pk.filter_perm,
+                           pk.seg_ptr, pk.cin_idx, static_cast<const T*>(pk.values), static_cast<const T*>(a.bias),
+                           static_cast<T*>(a.y), g);
     else
-        hipLaunchKernelGGL((k_conv_stream<DT, R, false>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)),
+        hipLaunchKernelGGL((k_conv_stream<DT, R, false, 1>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)),
                            smem, stream, static_cast<const T*>(a.x), pk.filter_perm, pk.seg_ptr, pk.cin_idx,
                            static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), static_cast<T*>(a.y),
                            g);
@@ -741,7 +830,9 @@ hipError_t launch_r(const PackedView& pk, const ConvArgs& a, const Geo& g, hipSt
 hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const ConvArgs& a,
                               hipStream_t stream) {
     const int64_t x_bytes = int64_t(a.n) * a.cin * a.h * a.w * (a.dtype == DT_F16 ? 2 : 4);
-    if (x_bytes > (int64_t(1) << 31)) return hipErrorNotSupported;
+    // buffer descriptors address at most 2 GiB (x) and the packed weights
+    if (x_bytes > (int64_t(1) << 31) || a.keep * 4 * (a.dtype == DT_F16 ? 2 : 4) > 0x7fffffff)
+        return hipErrorNotSupported;
     Geo g;
     std::memset(&g, 0, sizeof g);
     g.n = a.n;
@@ -752,6 +843,7 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
     g.m = tab.m;
     g.relu = a.relu;
     g.x_bytes = int(x_bytes > 0x7fffffff ? 0x7fffffff : x_bytes);
+    g.keep = int(a.keep);
     for (int p = 0; p < kMaxPatterns; ++p) {
         g.shape[p] = -1;
         g.mask[p] = p < tab.m ? tab.mask[p] : 0;
@@ -852,6 +944,7 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
         const bool throughput = g.S >= 2 || waves >= 2 * 6 * 1024;
         g.lds = fits && throughput && !(tune_flags & 1) ? 1 : 0;
         if (tune_flags & 2) g.lds = fits ? 1 : 0;
+        if (g.lds && nruns_max > 1) g.lds = 2;             // several runs per wave: the general form
     }
     switch (R) {
         case 8: return a.dtype == DT_F16 ? launch_r<DT_F16, 8>(pk, a, g, stream)
