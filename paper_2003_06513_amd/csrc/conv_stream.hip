@@ -597,6 +597,308 @@ __device__ __forceinline__ int run_pattern_lds(int shape, unsigned mask, const L
 #undef PSC_SHAPE_CASE8
 #undef PSC_SHAPE_CASE
 
+// ------------------------------------------------------------------ wide rows
+// Images 64..252 columns wide whose rows start on 64-byte boundaries (fp32,
+// width a multiple of 16): a lane owns 4 adjacent output columns and R rows
+// of a full-row band, and each input row arrives as one aligned 16-byte load
+// per lane, which the vector memory path serves at full rate.  The
+// neighbour columns left of the lane's first and right of its last column
+// come from the adjacent lanes through DPP; the other taps read the lane's
+// own values.  Segments are padded to a multiple of 4 lanes so that every
+// 4-lane group of a load stays in one 64-byte block.
+
+// One output row of a tap: a[c] += w * x[c + DS - 1] over the lane's 4
+// columns, with x[-1] / x[4] taken from the lane to the left / right.
+template <int DS> struct TapRow4;
+#define PSC_A4 [a0] "+v"(a[0]), [a1] "+v"(a[1]), [a2] "+v"(a[2]), [a3] "+v"(a[3])
+#define PSC_X4 [x0] "v"(x[0]), [x1] "v"(x[1]), [x2] "v"(x[2]), [x3] "v"(x[3])
+template <> struct TapRow4<1> {
+    __device__ __forceinline__ static void run(float* a, const float* x, float ws, float) {
+        asm volatile("v_fmac_f32_e32 %[a0], %[ws], %[x0]\n"
+                     "v_fmac_f32_e32 %[a1], %[ws], %[x1]\n"
+                     "v_fmac_f32_e32 %[a2], %[ws], %[x2]\n"
+                     "v_fmac_f32_e32 %[a3], %[ws], %[x3]\n"
+                     : PSC_A4 : PSC_X4, [ws] "s"(ws));
+    }
+};
+template <> struct TapRow4<0> {
+    __device__ __forceinline__ static void run(float* a, const float* x, float ws, float wv) {
+        asm volatile("v_fmac_f32_dpp %[a0], %[x3], %[wv] wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+                     "v_fmac_f32_e32 %[a1], %[ws], %[x0]\n"
+                     "v_fmac_f32_e32 %[a2], %[ws], %[x1]\n"
+                     "v_fmac_f32_e32 %[a3], %[ws], %[x2]\n"
+                     : PSC_A4 : PSC_X4, [ws] "s"(ws), [wv] "v"(wv));
+    }
+};
+template <> struct TapRow4<2> {
+    __device__ __forceinline__ static void run(float* a, const float* x, float ws, float wv) {
+        asm volatile("v_fmac_f32_e32 %[a0], %[ws], %[x1]\n"
+                     "v_fmac_f32_e32 %[a1], %[ws], %[x2]\n"
+                     "v_fmac_f32_e32 %[a2], %[ws], %[x3]\n"
+                     "v_fmac_f32_dpp %[a3], %[x0], %[wv] wave_shl:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+                     : PSC_A4 : PSC_X4, [ws] "s"(ws), [wv] "v"(wv));
+    }
+};
+#undef PSC_X4
+#undef PSC_A4
+
+// Tap at kernel position Q over the lane's R rows; x[r] holds the 4 columns
+// of input row r (r = 0 is the row above the lane's first output row).
+template <int Q, int R>
+__device__ __forceinline__ void tap4(float (&acc)[4 * R], const float (&x)[R + 2][4], float ws, float wv) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) TapRow4<Q % 3>::run(&acc[4 * r], x[r + Q / 3], ws, wv);
+}
+
+template <int J, int Q, int R>
+__device__ __forceinline__ void tap4_same(float (&a)[4 * R], const float (&x)[R + 2][4], const float (&w)[4]) {
+    if constexpr (Q % 3 == 1) tap4<Q, R>(a, x, w[J], 0.f);
+}
+template <int J, int Q, int R>
+__device__ __forceinline__ void tap4_shift(float (&a)[4 * R], const float (&x)[R + 2][4], const float (&w)[4],
+                                           const float (&wv)[4]) {
+    if constexpr (Q % 3 != 1) tap4<Q, R>(a, x, w[J], wv[J]);
+}
+
+// The 4 taps of one kernel: the shifted taps' weights are copied to VGPRs
+// first and the same-column taps (the centre at least: 4R FMAs) run before
+// the shifted ones, so no DPP read follows a VALU write of its operands
+// within two wait states.
+template <int R, int Q0, int Q1, int Q2, int Q3>
+__device__ __forceinline__ void kernel_taps4(float (&a)[4 * R], const float (&x)[R + 2][4], const float (&w)[4]) {
+    float wv[4] = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (Q0 % 3 != 1) wv[0] = to_vgpr(w[0]);
+    if constexpr (Q1 % 3 != 1) wv[1] = to_vgpr(w[1]);
+    if constexpr (Q2 % 3 != 1) wv[2] = to_vgpr(w[2]);
+    if constexpr (Q3 % 3 != 1) wv[3] = to_vgpr(w[3]);
+    tap4_same<0, Q0, R>(a, x, w);
+    tap4_same<1, Q1, R>(a, x, w);
+    tap4_same<2, Q2, R>(a, x, w);
+    tap4_same<3, Q3, R>(a, x, w);
+    tap4_shift<0, Q0, R>(a, x, w, wv);
+    tap4_shift<1, Q1, R>(a, x, w, wv);
+    tap4_shift<2, Q2, R>(a, x, w, wv);
+    tap4_shift<3, Q3, R>(a, x, w, wv);
+}
+
+template <int R>
+__device__ __forceinline__ void kernel_taps4_dyn(const int (&q)[4], float (&a)[4 * R], const float (&x)[R + 2][4],
+                                                 const float (&w)[4]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const float wv = to_vgpr(w[j]);
+        asm volatile("s_nop 1" ::: "memory");   // wait states before the DPP read of wv
+        switch (q[j]) {
+            case 0: tap4<0, R>(a, x, w[j], wv); break;
+            case 1: tap4<1, R>(a, x, w[j], wv); break;
+            case 2: tap4<2, R>(a, x, w[j], wv); break;
+            case 3: tap4<3, R>(a, x, w[j], wv); break;
+            case 4: tap4<4, R>(a, x, w[j], wv); break;
+            case 5: tap4<5, R>(a, x, w[j], wv); break;
+            case 6: tap4<6, R>(a, x, w[j], wv); break;
+            case 7: tap4<7, R>(a, x, w[j], wv); break;
+            default: tap4<8, R>(a, x, w[j], wv); break;
+        }
+    }
+}
+
+// The R+2 input rows (4 columns each) of channel ci for this lane.
+template <int R>
+__device__ __forceinline__ void load_rows4(const RunCtx& c, const uint32_t (&vo)[R + 2], int ci,
+                                           float (&x)[R + 2][4]) {
+    const int soff = __builtin_amdgcn_readfirstlane(ci * c.chan_bytes);
+#pragma unroll
+    for (int r = 0; r < R + 2; ++r) {
+        const psc_f32x4 v = __builtin_bit_cast(psc_f32x4, __builtin_amdgcn_raw_buffer_load_b128(c.xr, vo[r], soff, 0));
+        x[r][0] = v.x, x[r][1] = v.y, x[r][2] = v.z, x[r][3] = v.w;
+    }
+}
+
+// Kernels [k, e) of one pattern segment share; two per trip as in the
+// one-column form.
+template <int R, class TapFn>
+__device__ __forceinline__ void run_kernels4(const RunCtx& c, const uint32_t (&vo)[R + 2], int k, int e,
+                                             float (&acc)[4 * R], TapFn taps) {
+    const int last = e - 1;
+    float wA[4], wB[4];
+    meta_w<DT_F32>(c.m, k, wA);
+    int kk = k + 1 <= last ? k + 1 : last;
+    int ciB = meta_ci(c.m, kk);
+    meta_w<DT_F32>(c.m, kk, wB);
+    float xA[R + 2][4], xB[R + 2][4];
+    load_rows4<R>(c, vo, meta_ci(c.m, k), xA);
+    while (k + 1 < e) {
+        load_rows4<R>(c, vo, ciB, xB);                         // rows of kernel k+1
+        kk = k + 2 <= last ? k + 2 : last;
+        const int ciA2 = meta_ci(c.m, kk);
+        float wA2[4];
+        meta_w<DT_F32>(c.m, kk, wA2);
+        kk = k + 3 <= last ? k + 3 : last;
+        const int ciB2 = meta_ci(c.m, kk);
+        float wB2[4];
+        meta_w<DT_F32>(c.m, kk, wB2);
+        taps(acc, xA, wA);                                     // kernel k
+        load_rows4<R>(c, vo, ciA2, xA);                        // rows of kernel k+2
+        taps(acc, xB, wB);                                     // kernel k+1
+        k += 2;
+        wA[0] = wA2[0], wA[1] = wA2[1], wA[2] = wA2[2], wA[3] = wA2[3];
+        wB[0] = wB2[0], wB[1] = wB2[1], wB[2] = wB2[2], wB[3] = wB2[3];
+        ciB = ciB2;
+    }
+    if (k < e) taps(acc, xA, wA);
+}
+
+template <int R, int MASK>
+__device__ __forceinline__ void run_shape4(const RunCtx& c, const uint32_t (&vo)[R + 2], int k, int e,
+                                           float (&acc)[4 * R]) {
+    constexpr int Q0 = NthBit<MASK, 0>::value(), Q1 = NthBit<MASK, 1>::value();
+    constexpr int Q2 = NthBit<MASK, 2>::value(), Q3 = NthBit<MASK, 3>::value();
+    run_kernels4<R>(c, vo, k, e, acc, [](float (&a)[4 * R], const float (&x)[R + 2][4], const float (&w)[4]) {
+        kernel_taps4<R, Q0, Q1, Q2, Q3>(a, x, w);
+    });
+}
+
+template <int R>
+__device__ __forceinline__ void run_generic4(unsigned mask, const RunCtx& c, const uint32_t (&vo)[R + 2], int k,
+                                             int e, float (&acc)[4 * R]) {
+    int q[4] = {4, 4, 4, 4}, seen = 0;
+#pragma unroll
+    for (int p = 0; p < 9; ++p) {
+        if ((mask >> p) & 1u) {
+            if (seen == 0) q[0] = p;
+            else if (seen == 1) q[1] = p;
+            else if (seen == 2) q[2] = p;
+            else if (seen == 3) q[3] = p;
+            ++seen;
+        }
+    }
+    run_kernels4<R>(c, vo, k, e, acc, [=](float (&a)[4 * R], const float (&x)[R + 2][4], const float (&w)[4]) {
+        kernel_taps4_dyn<R>(q, a, x, w);
+    });
+}
+
+#define PSC_SHAPE_CASE(I) \
+    case I: run_shape4<R, kCentre3.code[I]>(c, vo, k, e, acc); return;
+#define PSC_SHAPE_CASE8(I)                                                                     \
+    PSC_SHAPE_CASE(I) PSC_SHAPE_CASE(I + 1) PSC_SHAPE_CASE(I + 2) PSC_SHAPE_CASE(I + 3)        \
+    PSC_SHAPE_CASE(I + 4) PSC_SHAPE_CASE(I + 5) PSC_SHAPE_CASE(I + 6) PSC_SHAPE_CASE(I + 7)
+template <int R>
+__device__ __forceinline__ void run_pattern4(int shape, unsigned mask, const RunCtx& c, const uint32_t (&vo)[R + 2],
+                                             int k, int e, float (&acc)[4 * R]) {
+    switch (shape) {
+        PSC_SHAPE_CASE8(0)
+        PSC_SHAPE_CASE8(8)
+        PSC_SHAPE_CASE8(16)
+        PSC_SHAPE_CASE8(24)
+        PSC_SHAPE_CASE8(32)
+        PSC_SHAPE_CASE8(40)
+        PSC_SHAPE_CASE8(48)
+        default: run_generic4<R>(mask, c, vo, k, e, acc); return;
+    }
+}
+#undef PSC_SHAPE_CASE8
+#undef PSC_SHAPE_CASE
+
+// Wide form of the kernel (fp32): same blocks, shares, reduction and
+// epilogue as the one-column form, 4 columns per lane.
+template <int R>
+__global__ __launch_bounds__(512) void k_conv_wide(const float* __restrict__ x, const int32_t* __restrict__ perm,
+                                                   const int32_t* __restrict__ seg_ptr,
+                                                   const int32_t* __restrict__ cin_idx,
+                                                   const float* __restrict__ vals, const float* __restrict__ bias,
+                                                   float* __restrict__ y, Geo g) {
+    constexpr int ROWS = R + 2;
+    extern __shared__ float psc_smem4[];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+    const int gf = wave / g.KS, sp = wave - gf * g.KS;
+    const int b = blockIdx.x;
+    int lb = b;
+    if (g.nblocks >= 8) {
+        const int per = g.nblocks / 8, rem = g.nblocks % 8;
+        const int xcd = b % 8, slot = b / 8;
+        lb = (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + slot;
+    }
+    const int fg = lb % g.groups_x, sgrp = lb / g.groups_x;
+    const int i = fg * g.FW + gf;
+    const bool has_filter = i < g.cout;
+
+    // ---- lane geometry: lane cidx of segment s holds columns 4*cidx .. +3
+    const int s = lane / g.seg_len, cidx = lane - s * g.seg_len;
+    const int u = sgrp * g.S + s;
+    int col0 = -1, nimg = 0, h0 = 0;
+    if (s < g.S && u < g.U) {
+        nimg = u / g.RB;
+        h0 = (u % g.RB) * R;
+        if (4 * cidx < g.W) col0 = 4 * cidx;
+    }
+    const int plane = g.H * g.W;
+    uint32_t vo[ROWS];
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) {
+        const int row = h0 - 1 + r;
+        vo[r] = (col0 >= 0 && row >= 0 && row < g.H) ? uint32_t(nimg * g.cin * plane + row * g.W + col0) * 4u
+                                                     : 0x80000000u;
+    }
+    float acc[4 * R];
+#pragma unroll
+    for (int r = 0; r < 4 * R; ++r) acc[r] = 0.f;
+
+    const int* segp = seg_ptr + i * (g.m + 1);
+    if (has_filter) {
+        const int f0 = segp[0], f1 = segp[g.m];
+        const int len = f1 - f0;
+        const int s0 = f0 + len * sp / g.KS, s1 = f0 + len * (sp + 1) / g.KS;
+        const RunCtx ctx{Meta{scalar_rsrc(cin_idx, g.keep * 4), scalar_rsrc(vals, g.keep * 16)},
+                         __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(x), int16_t(0), g.x_bytes, 0x00020000),
+                         __builtin_amdgcn_readfirstlane(plane * 4)};
+        for (int p = 0; p < g.m; ++p) {
+            int k0 = segp[p], k1 = segp[p + 1];
+            k0 = k0 < s0 ? s0 : k0;
+            k1 = k1 > s1 ? s1 : k1;
+            if (k0 < k1) run_pattern4<R>(g.shape[p], g.mask[p], ctx, vo, k0, k1, acc);
+        }
+    }
+
+    if (g.KS > 1) {
+        float (*red)[4 * R][64] = reinterpret_cast<float (*)[4 * R][64]>(psc_smem4);
+        for (int slot = 0; slot < g.FW; ++slot) {
+            if (slot == gf) {
+#pragma unroll
+                for (int r = 0; r < 4 * R; ++r) red[sp][r][lane] = acc[r];
+            }
+            __syncthreads();
+            if (slot == gf) {
+#pragma unroll
+                for (int r = 0; r < 4 * R; ++r) {
+                    float v = 0.f;
+                    for (int t = 0; t < g.KS; ++t) v += red[t][r][lane];
+                    acc[r] = v;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    if (!has_filter || col0 < 0) return;
+    const int f = perm[i];
+    const float bv = bias ? bias[f] : 0.f;
+    float* yp = y + (nimg * g.cout + f) * plane + col0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int row = h0 + r;
+        if (row < g.H && (r % g.KS) == sp) {
+            psc_f32x4 v{acc[4 * r] + bv, acc[4 * r + 1] + bv, acc[4 * r + 2] + bv, acc[4 * r + 3] + bv};
+            if (g.relu) {
+                v.x = v.x > 0.f ? v.x : 0.f;
+                v.y = v.y > 0.f ? v.y : 0.f;
+                v.z = v.z > 0.f ? v.z : 0.f;
+                v.w = v.w > 0.f ? v.w : 0.f;
+            }
+            *reinterpret_cast<psc_f32x4*>(yp + row * g.W) = v;
+        }
+    }
+}
+
 // ------------------------------------------------------------------ kernel
 // LDS = true stages the input rows through per-wave LDS (full-row segments
 // only; NR: runs per wave compiled for); LDS = false loads them straight
@@ -795,6 +1097,17 @@ __global__ __launch_bounds__(512) void k_conv_stream(const typename Elt<DT>::T* 
     }
 }
 
+template <int R>
+hipError_t launch_wide(const PackedView& pk, const ConvArgs& a, const Geo& g, hipStream_t stream) {
+    const int waves = g.FW * g.KS;
+    const size_t smem = g.KS > 1 ? size_t(g.KS) * 4 * R * 64 * sizeof(float) : 0;
+    hipLaunchKernelGGL((k_conv_wide<R>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)), smem, stream,
+                       static_cast<const float*>(a.x), pk.filter_perm, pk.seg_ptr, pk.cin_idx,
+                       static_cast<const float*>(pk.values), static_cast<const float*>(a.bias),
+                       static_cast<float*>(a.y), g);
+    return hipGetLastError();
+}
+
 template <int DT, int R>
 hipError_t launch_r(const PackedView& pk, const ConvArgs& a, const Geo& g, hipStream_t stream) {
     using T = typename Elt<DT>::T;
@@ -851,6 +1164,38 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
             for (int t = 0; t < 56; ++t)
                 if (kCentre3.code[t] == tab.mask[p]) g.shape[p] = int8_t(t);
     }
+    int tune_flags = 0;
+    int tune_ks = 0;
+    if (const char* t = getenv("PSC_CONV_TUNE")) {   // experiments: "KS=2", "DIRECT", "LDS", "NOWIDE"
+        if (const char* q = strstr(t, "KS=")) tune_ks = atoi(q + 3);
+        if (strstr(t, "DIRECT")) tune_flags |= 1;
+        if (strstr(t, "LDS")) tune_flags |= 2;
+        if (strstr(t, "NOWIDE")) tune_flags |= 4;
+    }
+    // wide form: fp32 rows of 64..252 columns starting on 64-byte boundaries
+    // (width a multiple of 16): 4 columns per lane, full-row segments padded
+    // to a multiple of 4 lanes
+    if (a.dtype == DT_F32 && a.w % 16 == 0 && a.w >= 64 && a.w / 4 + 1 <= 64 && !(tune_flags & 4)) {
+        g.cols_mode = 0;
+        g.seg_len = (a.w / 4 + 1 + 3) / 4 * 4;
+        g.S = 64 / g.seg_len;
+        g.Wt = a.w;
+        g.CT = 1;
+        // two rows per lane: 4(R+2) row values a kernel, twice for the
+        // prefetch, keep the wave near 80 VGPRs (6 waves per SIMD)
+        constexpr int R = 2;
+        g.RB = (a.h + R - 1) / R;
+        g.U = a.n * g.RB;
+        const int sgroups = (g.U + g.S - 1) / g.S;
+        g.KS = 1;
+        while (g.KS < kMaxSplit && int64_t(sgroups) * a.cout * g.KS < 4096 && a.cin >= 16 * g.KS) g.KS *= 2;
+        if (tune_ks > 0) g.KS = tune_ks > kMaxSplit ? kMaxSplit : tune_ks;
+        g.FW = g.KS >= 4 ? 1 : 4 / g.KS;
+        if (g.FW > a.cout) g.FW = a.cout;
+        g.groups_x = (a.cout + g.FW - 1) / g.FW;
+        g.nblocks = g.groups_x * sgroups;
+        return launch_wide<R>(pk, a, g, stream);
+    }
     // lane layout: full-row segments if they use the lanes at least as well
     // as haloed column tiles
     const int S_rows = a.w <= 63 ? 65 / (a.w + 1) : 0;
@@ -895,14 +1240,7 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
     const int sgroups = (g.U + g.S - 1) / g.S;
     g.KS = 1;
     while (g.KS < kMaxSplit && int64_t(sgroups) * a.cout * g.KS < 4096 && a.cin >= 16 * g.KS) g.KS *= 2;
-    int tune_flags = 0;
-    if (const char* t = getenv("PSC_CONV_TUNE")) {   // experiments: "KS=2", "DIRECT", "LDS"
-        if (const char* q = strstr(t, "KS=")) g.KS = atoi(q + 3);
-        if (g.KS < 1) g.KS = 1;
-        if (g.KS > kMaxSplit) g.KS = kMaxSplit;
-        if (strstr(t, "DIRECT")) tune_flags |= 1;
-        if (strstr(t, "LDS")) tune_flags |= 2;
-    }
+    if (tune_ks > 0) g.KS = tune_ks > kMaxSplit ? kMaxSplit : tune_ks;
     g.FW = g.KS >= 4 ? 1 : 4 / g.KS;
     if (g.FW > a.cout) g.FW = a.cout;
     const int fgroups = (a.cout + g.FW - 1) / g.FW;

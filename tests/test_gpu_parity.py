@@ -110,7 +110,7 @@ CONV_SHAPES = [
     (1, 3, 8, 5, 5), (2, 5, 7, 9, 11), (1, 16, 16, 1, 1), (1, 8, 8, 2, 3), (3, 4, 5, 3, 4),
     (1, 8, 16, 4, 4), (2, 6, 9, 7, 7), (1, 5, 4, 13, 13), (1, 4, 8, 6, 130), (1, 8, 8, 10, 32),
     (1, 4, 4, 3, 63), (1, 4, 4, 3, 64), (2, 3, 6, 8, 62), (1, 6, 10, 17, 16), (5, 7, 3, 4, 8),
-    (1, 3, 8, 9, 224),
+    (1, 3, 8, 9, 224), (2, 5, 6, 7, 112), (1, 20, 9, 5, 240), (3, 17, 5, 3, 64),
 ]
 
 
