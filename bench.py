@@ -265,7 +265,7 @@ def main():
         traffic = profiled_traffic(os.path.join(ROOT, "paper_2003_06513_amd", "csrc", "conv_stream.hip"))
     roof = {"bound": "alu", "achieved": round(achieved_tf, 3), "peak": PEAK_VALU_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved_tf / PEAK_VALU_TFLOPS, 4), "traffic": traffic,
-            "kernel": "k_conv_stream",
+            "kernel": "k_conv_wide (224- and 112-wide layers) + k_conv_stream (the others)",
             "per_launch": "8*N*H*W*keep nonzero-MAC flops averaged over the %d conv launches of a step, "
                           "/ their mean duration (HIP events on the launch stream)" % len(net.layers),
             "avg_launch_us": round(conv_ms * 1e3 / len(net.layers), 3)}
