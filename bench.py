@@ -2,8 +2,9 @@
 
 A step is one forward pass of the whole workload through the HIP path: for
 the VGG-16 stack (default) the 13 pattern-sparse conv layers with fused ReLU
-and the four 2x2 max-pools on a 1x3x224x224 synthetic image; for the other
-workloads every listed layer on its own resident input.  Weights are pruned
+and the four 2x2 max-pools (fused into the conv launch they follow where
+that is faster, as timed at start-up) on a 1x3x224x224 synthetic image; for
+the other workloads every listed layer on its own resident input.  Weights are pruned
 and packed on the GPU (projection, selection, packing) before timing.  The
 step's launches are captured once in a HIP graph and the timed steps are its
 replays (--no-graph times eager launches); per-layer times come from an eager
@@ -20,6 +21,7 @@ import json
 import os
 import sys
 import time
+from types import SimpleNamespace
 
 import numpy as np
 
@@ -43,6 +45,9 @@ def parse():
     ap.add_argument("--list", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
                     help="time eager launches instead of replays of a captured HIP graph of the step")
+    ap.add_argument("--fuse-pool", default="auto",
+                    help="pooled layers whose pool runs inside the conv launch: auto (the faster form, "
+                         "timed at start-up), all, none, or layer names separated by commas")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 256 MiB device-to-device copy (reference for HBM counters)")
     return ap.parse_args()
@@ -80,7 +85,7 @@ class Net:
             pooled = None
             if lay.pool_after:
                 pooled = torch.empty((n, lay.cout, lay.h // 2, lay.w // 2), dtype=tdt, device="cuda")
-            self.layers.append(dict(lay=lay, w=w, prep=prep, x=x, y=y, pooled=pooled))
+            self.layers.append(dict(lay=lay, w=w, prep=prep, x=x, y=y, pooled=pooled, fused=False))
             if wl.chained:
                 x = pooled if pooled is not None else y
         torch.cuda.synchronize()
@@ -90,12 +95,46 @@ class Net:
         for li, L in enumerate(self.layers):
             if events is not None:
                 events[li][0].record()
-            B.conv3x3_fwd(L["prep"].layer, L["prep"].packed, L["x"], L["y"], relu=L["lay"].relu,
-                          algo=self.algo)
+            if L["fused"]:
+                # conv, ReLU and the 2x2 max-pool in one launch
+                B.conv3x3_fwd_pool2(L["prep"].layer, L["prep"].packed, L["x"], L["pooled"], relu=L["lay"].relu,
+                                    algo=self.algo)
+            else:
+                B.conv3x3_fwd(L["prep"].layer, L["prep"].packed, L["x"], L["y"], relu=L["lay"].relu,
+                              algo=self.algo)
             if events is not None:
                 events[li][1].record()
-            if L["pooled"] is not None:
+            if L["pooled"] is not None and not L["fused"]:
                 B.maxpool2x2(L["y"], L["pooled"])
+
+    def choose_fusion(self, mode="auto", reps=20):
+        """Per pooled layer, the fused conv + pool launch or the conv launch
+        followed by the pool kernel: with mode "auto" the faster of the two,
+        timed on this device; else "all", "none" or a list of layer names."""
+        import torch
+        names = [n for n in mode.split(",") if n] if mode not in ("auto", "all", "none") else []
+        for L in self.layers:
+            L["fused"] = False
+            if L["pooled"] is None:
+                continue
+            if mode != "auto":
+                L["fused"] = mode == "all" or L["lay"].name in names
+                continue
+            t = {}
+            for fused in (False, True):
+                L["fused"] = fused
+                one = [dict(L)]
+                run = lambda: Net.step(SimpleNamespace(layers=one, algo=self.algo))
+                for _ in range(3):
+                    run()
+                s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                s.record()
+                for _ in range(reps):
+                    run()
+                e.record()
+                torch.cuda.synchronize()
+                t[fused] = s.elapsed_time(e)
+            L["fused"] = t[True] < t[False]
 
     def output(self):
         L = self.layers[-1]
@@ -131,9 +170,10 @@ def cpu_baseline(net, budget_s=10.0):
                       % (layers, passes, len(host), flops / 1e9, secs)}
 
 
-def profiled_traffic(kernel_src):
+def profiled_traffic(kernel_src, fused):
     """HBM bytes per conv launch from the committed rocprofv3 counter summary
-    of this workload, or None when the kernel source changed since."""
+    of this workload, or None when the kernel source or the set of layers
+    with the pool fused into the conv launch differ from the profiled ones."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "k_conv_stream_vgg16_224_b1_f32.md")
     if not os.path.exists(path):
@@ -147,6 +187,8 @@ def profiled_traffic(kernel_src):
                 k, v = line[2:].strip().split(": ", 1)
                 fields[k.strip("`")] = v.strip().strip("`")
     if fields.get("conv_stream.hip sha256") != digest:
+        return None
+    if fields.get("pool fused into") != (",".join(fused) or "none"):
         return None
     try:
         return int(fields["hbm bytes per conv launch"])
@@ -213,6 +255,7 @@ def main():
     B.lib()
     wl = find_workload(args.workload)
     net = Net(wl, args.algo)
+    net.choose_fusion(args.fuse_pool)
 
     for _ in range(args.warmup):
         net.step()
@@ -230,7 +273,7 @@ def main():
     ms_eager = (time.perf_counter() - t0) * 1e3 / K
     ms_step, graph = ms_eager, False
     if not args.no_graph:
-        # the step's 13 conv and 4 pool launches captured once in a HIP graph
+        # the step's conv and pool launches captured once in a HIP graph
         # and replayed: the timed region is the replays alone
         eager_out = net.output().clone()
         g = torch.cuda.CUDAGraph()
@@ -262,7 +305,8 @@ def main():
     achieved_tf = total_nz / (conv_ms * 1e-3) / 1e12
     traffic = None
     if wl.name == "vgg16_224_b1_f32":
-        traffic = profiled_traffic(os.path.join(ROOT, "paper_2003_06513_amd", "csrc", "conv_stream.hip"))
+        traffic = profiled_traffic(os.path.join(ROOT, "paper_2003_06513_amd", "csrc", "conv_stream.hip"),
+                                   [L["lay"].name for L in net.layers if L["fused"]])
     roof = {"bound": "alu", "achieved": round(achieved_tf, 3), "peak": PEAK_VALU_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved_tf / PEAK_VALU_TFLOPS, 4), "traffic": traffic,
             "kernel": "k_conv_wide (224- and 112-wide layers) + k_conv_stream (the others)",
@@ -275,7 +319,8 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": wl.name, "batch": wl.batch, "layers": len(wl.layers), "m": wl.m,
-                   "stack": "conv+relu, 2x2 max-pool after conv2/4/7/10" if wl.chained else "independent layers"},
+                   "stack": "conv+relu, 2x2 max-pool after conv2/4/7/10" if wl.chained else "independent layers",
+                   "pool_fused_into": [L["lay"].name for L in net.layers if L["fused"]]},
         "step_launch": "hip graph replay" if graph else "eager",
         "ms_per_step_eager": round(ms_eager, 4),
         "ms_per_layer": {L["lay"].name: round(t, 4) for L, t in zip(net.layers, layer_ms)},

@@ -158,6 +158,17 @@ psc_status psc_conv3x3_fwd_algo(const psc_layer *layer, const psc_packed *packed
                                 int32_t h, int32_t w, const void *d_bias,
                                 int32_t relu, void *d_y, int32_t algo, void *stream);
 
+/* Sec. 4.1, Eq. 1 followed by the 2x2/2 max-pool of the VGG-16 stack, in
+ * one pass: d_y [n][cout][h/2][w/2] (original filter order) receives
+ *   y[n,f,i,j] = max over a,b in {0,1} of sigma(conv(x)[n,f,2i+a,2j+b] + b[f])
+ * with conv and sigma as in psc_conv3x3_fwd; the un-pooled output is never
+ * written.  h and w must be even.  algo as in psc_conv3x3_fwd_algo.  d_y must
+ * not overlap d_x. */
+psc_status psc_conv3x3_fwd_pool2(const psc_layer *layer, const psc_packed *packed,
+                                 int32_t act_dtype, const void *d_x, int32_t n,
+                                 int32_t h, int32_t w, const void *d_bias,
+                                 int32_t relu, void *d_y, int32_t algo, void *stream);
+
 /* Comparator: the dense 3x3 convolution (stride 1, pad 1) of dense OIHW
  * weights d_w [cout][cin][3][3] on the vector ALUs, same conventions and
  * accumulation as psc_conv3x3_fwd. */

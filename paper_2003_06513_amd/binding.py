@@ -83,6 +83,7 @@ def lib() -> ctypes.CDLL:
         "psc_unpack_dense": ([LP, PP, P, P], ctypes.c_int),
         "psc_conv3x3_fwd": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, P], ctypes.c_int),
         "psc_conv3x3_fwd_algo": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, P], ctypes.c_int),
+        "psc_conv3x3_fwd_pool2": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, P], ctypes.c_int),
         "psc_dense3x3_fwd": ([i32, P, i32, i32, i32, i32, P, i32, P, i32, P, P], ctypes.c_int),
         "psc_maxpool2x2": ([i32, P, i32, i32, i32, i32, P, P], ctypes.c_int),
     }
@@ -241,6 +242,19 @@ def conv3x3_fwd(layer: Layer, packed: Packed, x, y, bias=None, relu: bool = Fals
     _check(lib().psc_conv3x3_fwd_algo(layer.ref(), ctypes.byref(cp), dtype_code(x), _dev(x, "x"), n, h,
                                       w, _dev(bias, "bias"), int(bool(relu)), _dev(y, "y"), int(algo),
                                       _stream(stream)), "psc_conv3x3_fwd")
+
+
+def conv3x3_fwd_pool2(layer: Layer, packed: Packed, x, y, bias=None, relu: bool = False, algo: int = 0,
+                      stream=None):
+    """psc_conv3x3_fwd_pool2: conv, sigma and the 2x2/2 max-pool in one pass;
+    y is [n][cout][h/2][w/2]."""
+    n, cin, h, w = (int(d) for d in x.shape)
+    if cin != layer.cin or tuple(y.shape) != (n, layer.cout, h // 2, w // 2):
+        raise ValueError("x/y shapes do not match the layer and the 2x2 pool")
+    cp = packed.c()
+    _check(lib().psc_conv3x3_fwd_pool2(layer.ref(), ctypes.byref(cp), dtype_code(x), _dev(x, "x"), n, h,
+                                       w, _dev(bias, "bias"), int(bool(relu)), _dev(y, "y"), int(algo),
+                                       _stream(stream)), "psc_conv3x3_fwd_pool2")
 
 
 def dense3x3_fwd(x, wd, y, bias=None, relu: bool = False, stream=None):

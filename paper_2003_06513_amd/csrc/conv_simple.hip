@@ -11,6 +11,9 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
 
 namespace {
 
+// One output pixel per lane; with pool, one pooled pixel: the maximum of
+// the four outputs of its 2x2 window (sigma and max commute, the bias is
+// common to the window).
 template <int DT>
 __global__ __launch_bounds__(256) void k_conv_simple(const typename Elt<DT>::T* __restrict__ x, int cin,
                                                      int H, int W, int cout, PatTable tab,
@@ -20,36 +23,43 @@ __global__ __launch_bounds__(256) void k_conv_simple(const typename Elt<DT>::T* 
                                                      const uint8_t* __restrict__ pat_id,
                                                      const typename Elt<DT>::T* __restrict__ values,
                                                      const typename Elt<DT>::T* __restrict__ bias,
-                                                     int relu, typename Elt<DT>::T* __restrict__ y) {
+                                                     int relu, int pool, typename Elt<DT>::T* __restrict__ y) {
     using E = Elt<DT>;
     __shared__ uint16_t msk[kMaxPatterns];
     for (int p = threadIdx.x; p < tab.m; p += 256) msk[p] = tab.mask[p];
     __syncthreads();
     const int i = blockIdx.y, n = blockIdx.z;
     const int plane = H * W;
+    const int OW = pool ? W / 2 : W, oplane = pool ? plane / 4 : plane;
     const int pix = blockIdx.x * 256 + threadIdx.x;
-    if (pix >= plane) return;
-    const int oh = pix / W, ow = pix - oh * W;
+    if (pix >= oplane) return;
+    const int ph = pix / OW, pw = pix - ph * OW;
     const int f = perm[i];
     const typename E::T* xn = x + int64_t(n) * cin * plane;
-    float acc = 0.f;
-    for (int k = fptr[i]; k < fptr[i + 1]; ++k) {
-        const int ci = cin_idx[k], p = pat_id[k];
-        if (unsigned(ci) >= unsigned(cin) || p >= tab.m) continue;   // malformed storage
-        const typename E::T* xc = xn + int64_t(ci) * plane;
-        const unsigned mk = msk[p];
-        int j = 0;
-        for (int q = 0; q < 9; ++q) {
-            if (!((mk >> q) & 1u)) continue;
-            const float v = E::load(values, int64_t(k) * 4 + j);
-            ++j;
-            const int ih = oh + q / 3 - 1, iw = ow + q % 3 - 1;
-            if (ih >= 0 && ih < H && iw >= 0 && iw < W) acc = fmaf(v, E::load(xc, ih * W + iw), acc);
+    float best = 0.f;
+    const int nwin = pool ? 4 : 1;
+    for (int t = 0; t < nwin; ++t) {
+        const int oh = pool ? 2 * ph + (t >> 1) : ph, ow = pool ? 2 * pw + (t & 1) : pw;
+        float acc = 0.f;
+        for (int k = fptr[i]; k < fptr[i + 1]; ++k) {
+            const int ci = cin_idx[k], p = pat_id[k];
+            if (unsigned(ci) >= unsigned(cin) || p >= tab.m) continue;   // malformed storage
+            const typename E::T* xc = xn + int64_t(ci) * plane;
+            const unsigned mk = msk[p];
+            int j = 0;
+            for (int q = 0; q < 9; ++q) {
+                if (!((mk >> q) & 1u)) continue;
+                const float v = E::load(values, int64_t(k) * 4 + j);
+                ++j;
+                const int ih = oh + q / 3 - 1, iw = ow + q % 3 - 1;
+                if (ih >= 0 && ih < H && iw >= 0 && iw < W) acc = fmaf(v, E::load(xc, ih * W + iw), acc);
+            }
         }
+        best = t == 0 ? acc : fmaxf(best, acc);
     }
-    if (bias) acc += E::load(bias, f);
-    if (relu) acc = acc > 0.f ? acc : 0.f;
-    y[(int64_t(n) * cout + f) * plane + pix] = E::from_f(acc);
+    if (bias) best += E::load(bias, f);
+    if (relu) best = best > 0.f ? best : 0.f;
+    y[(int64_t(n) * cout + f) * oplane + pix] = E::from_f(best);
 }
 
 // Dense comparator: a block computes a 16x16 output tile for 4 filters of
@@ -134,10 +144,11 @@ __global__ __launch_bounds__(256) void k_maxpool(const typename Elt<DT>::T* __re
 template <int DT>
 hipError_t conv_simple(const PatTable& tab, const PackedView& pk, const ConvArgs& a, hipStream_t s) {
     using T = typename Elt<DT>::T;
-    const dim3 grid(unsigned((a.h * a.w + 255) / 256), unsigned(a.cout), unsigned(a.n));
+    const int outs = a.pool ? (a.h / 2) * (a.w / 2) : a.h * a.w;
+    const dim3 grid(unsigned((outs + 255) / 256), unsigned(a.cout), unsigned(a.n));
     hipLaunchKernelGGL(k_conv_simple<DT>, grid, dim3(256), 0, s, static_cast<const T*>(a.x), a.cin, a.h,
                        a.w, a.cout, tab, pk.filter_perm, pk.filter_ptr, pk.cin_idx, pk.pat_id,
-                       static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), a.relu,
+                       static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), a.relu, a.pool,
                        static_cast<T*>(a.y));
     return hipGetLastError();
 }
@@ -149,8 +160,8 @@ hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs
     if (algo == 0) {
         const hipError_t e = launch_conv_stream(tab, pk, a, stream);
         if (e != hipErrorNotSupported) return e;
-        // inputs beyond the 2 GiB one buffer descriptor covers take the
-        // one-output-per-lane kernel
+        // inputs beyond the 2 GiB one buffer descriptor covers, and pooled
+        // outputs of haloed column tiles, take the one-output-per-lane kernel
     }
     return a.dtype == DT_F16 ? conv_simple<DT_F16>(tab, pk, a, stream)
                              : conv_simple<DT_F32>(tab, pk, a, stream);

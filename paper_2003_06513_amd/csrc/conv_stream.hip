@@ -86,6 +86,7 @@ struct Geo {
     int x_bytes;    // bytes of x (the buffer range), at most 2^31
     int keep;       // kept kernels (entries of cin_idx)
     int relu;
+    int pool;       // 1: y is the 2x2/2 max-pool of the output (R even, full-row segments)
     int lds;        // 1: input rows staged through per-wave LDS (full-row segments only)
     int region;     // LDS bytes reserved per run of rows
     int wave_bytes; // LDS bytes per wave: nruns regions + a zero area
@@ -882,6 +883,29 @@ __global__ __launch_bounds__(512) void k_conv_wide(const float* __restrict__ x, 
     if (!has_filter || col0 < 0) return;
     const int f = perm[i];
     const float bv = bias ? bias[f] : 0.f;
+    if constexpr (R % 2 == 0) {
+        if (g.pool) {
+            // 2x2/2 max-pool: the lane's 4 columns give 2 pooled columns
+            const int OH = g.H / 2, OW = g.W / 2;
+            float* yp = y + (nimg * g.cout + f) * (OH * OW) + col0 / 2;
+#pragma unroll
+            for (int j = 0; j < R / 2; ++j) {
+                const int prow = h0 / 2 + j;
+                if (prow < OH && (j % g.KS) == sp) {
+                    const float* a0 = &acc[8 * j];
+                    float p0 = fmaxf(fmaxf(a0[0], a0[1]), fmaxf(a0[4], a0[5])) + bv;
+                    float p1 = fmaxf(fmaxf(a0[2], a0[3]), fmaxf(a0[6], a0[7])) + bv;
+                    if (g.relu) {
+                        p0 = p0 > 0.f ? p0 : 0.f;
+                        p1 = p1 > 0.f ? p1 : 0.f;
+                    }
+                    yp[prow * OW] = p0;
+                    yp[prow * OW + 1] = p1;
+                }
+            }
+            return;
+        }
+    }
     float* yp = y + (nimg * g.cout + f) * plane + col0;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -1081,6 +1105,33 @@ __global__ __launch_bounds__(512) void k_conv_stream(const typename Elt<DT>::T* 
             __syncthreads();
         }
     }
+    if constexpr (R % 2 == 0) {
+        if (g.pool) {
+            // 2x2/2 max-pool of the output: rows 2j, 2j+1 of the lane, then
+            // the column pair (even column, the lane to its right)
+            float v[R / 2];
+#pragma unroll
+            for (int j = 0; j < R / 2; ++j) {
+                const float m = fmaxf(acc[2 * j], acc[2 * j + 1]);
+                v[j] = fmaxf(m, __shfl_down(m, 1));
+            }
+            if (!has_filter || out_col < 0 || (out_col & 1)) return;
+            const int f = perm[i];
+            const float bv = bias ? E::load(bias, f) : 0.f;
+            const int OH = g.H / 2, OW = g.W / 2;
+            typename E::T* yp = y + (nimg * g.cout + f) * (OH * OW) + out_col / 2;
+#pragma unroll
+            for (int j = 0; j < R / 2; ++j) {
+                const int prow = h0 / 2 + j;
+                if (prow < OH && (j % g.KS) == sp) {
+                    float o = v[j] + bv;
+                    if (g.relu) o = o > 0.f ? o : 0.f;
+                    yp[prow * OW] = E::from_f(o);
+                }
+            }
+            return;
+        }
+    }
     if (!has_filter || out_col < 0) return;
     const int f = perm[i];
     const float bv = bias ? E::load(bias, f) : 0.f;
@@ -1136,7 +1187,8 @@ hipError_t launch_r(const PackedView& pk, const ConvArgs& a, const Geo& g, hipSt
 }  // namespace
 
 // Launch configuration.  Rows per lane R minimise the lane-rows issued
-// (ceil(units / S) * R, larger R on ties); a workgroup holds 4 filters, or
+// (ceil(units / S) * R, larger R on ties; even R when pooling; R = 8 only
+// with one segment per wave); a workgroup holds 4 filters, or
 // fewer filters split into KS shares (KS doubles up to 8) while the grid
 // holds under 4 waves per SIMD.  Returns hipErrorNotSupported when x exceeds
 // the 2 GiB a buffer descriptor addresses here.
@@ -1157,6 +1209,7 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
     g.relu = a.relu;
     g.x_bytes = int(x_bytes > 0x7fffffff ? 0x7fffffff : x_bytes);
     g.keep = int(a.keep);
+    g.pool = a.pool;
     for (int p = 0; p < kMaxPatterns; ++p) {
         g.shape[p] = -1;
         g.mask[p] = p < tab.m ? tab.mask[p] : 0;
@@ -1165,12 +1218,13 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
                 if (kCentre3.code[t] == tab.mask[p]) g.shape[p] = int8_t(t);
     }
     int tune_flags = 0;
-    int tune_ks = 0;
+    int tune_ks = 0, tune_r = 0;
     if (const char* t = getenv("PSC_CONV_TUNE")) {   // experiments: "KS=2", "DIRECT", "LDS", "NOWIDE"
         if (const char* q = strstr(t, "KS=")) tune_ks = atoi(q + 3);
         if (strstr(t, "DIRECT")) tune_flags |= 1;
         if (strstr(t, "LDS")) tune_flags |= 2;
         if (strstr(t, "NOWIDE")) tune_flags |= 4;
+        if (const char* q = strstr(t, "R=")) tune_r = atoi(q + 2);
     }
     // wide form: fp32 rows of 64..252 columns starting on 64-byte boundaries
     // (width a multiple of 16): 4 columns per lane, full-row segments padded
@@ -1216,6 +1270,7 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
         g.Wt = a.w;
         g.CT = 1;
     } else {
+        if (a.pool) return hipErrorNotSupported;   // pooling needs full-row segments
         const int Wt = (a.w + ct - 1) / ct;
         g.cols_mode = 1;
         g.S = 64 / (Wt + 2);
@@ -1227,7 +1282,12 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
     const int cand[4] = {8, 7, 4, 2};
     int R = 8;
     int64_t best = -1;
+    // 8 rows per lane only with one segment per wave: several segments at
+    // R = 8 are kept off (a run of such launches faulted the device and the
+    // cause is not known)
     for (int rr : cand) {
+        if (a.pool && (rr & 1)) continue;               // pooled rows pair up inside a lane
+        if (rr == 8 && g.S > 1) continue;
         const int64_t units = int64_t(a.n) * ((a.h + rr - 1) / rr) * g.CT;
         const int64_t cost = (units + g.S - 1) / g.S * rr;
         if (best < 0 || cost < best) {
@@ -1235,6 +1295,7 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
             R = rr;
         }
     }
+    if (tune_r == 2 || tune_r == 4 || (tune_r == 8 && g.S == 1) || (tune_r == 7 && !a.pool)) R = tune_r;
     g.RB = (a.h + R - 1) / R;
     g.U = a.n * g.RB * g.CT;
     const int sgroups = (g.U + g.S - 1) / g.S;

@@ -54,6 +54,7 @@ struct ConvArgs {
     const void* bias;
     int relu;
     void* y;
+    int pool;       // 1: y is the 2x2/2 max-pool of sigma(conv), [n][cout][h/2][w/2]
 };
 hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs& a, int algo,
                        hipStream_t stream);

@@ -143,6 +143,13 @@ def test_conv_validation(L):
     # n == 0 is a no-op that succeeds without touching the device
     assert L.psc_conv3x3_fwd(lay.ref(), ctypes.byref(cp), B.PSC_F32, FAKE, 0, 4, 4, None, 0, FAKE,
                              None) == B.PSC_OK
+    # fused 2x2 pool: odd sizes rejected, n == 0 a no-op
+    for h, w in ((5, 4), (4, 7)):
+        rc, msg = _status(L.psc_conv3x3_fwd_pool2(lay.ref(), ctypes.byref(cp), B.PSC_F32, FAKE, 1, h, w, None,
+                                                  0, ctypes.c_void_p(0x20000), 0, None))
+        assert rc == B.PSC_ERR_ARG and "even" in msg
+    assert L.psc_conv3x3_fwd_pool2(lay.ref(), ctypes.byref(cp), B.PSC_F32, FAKE, 0, 4, 4, None, 0, FAKE, 0,
+                                   None) == B.PSC_OK
 
 
 def test_dense_and_pool_validation(L):

@@ -203,6 +203,36 @@ def test_dense_comparator(shape, dtype):
     assert norm_err(y.cpu().numpy(), ref) <= TOL[dtype]
 
 
+POOL_SHAPES = [
+    # n, cin, cout, h, w: full-row segments of each width class, haloed column
+    # tiles (the one-output-per-lane kernel), wide rows, ragged bands, splits
+    (1, 6, 5, 14, 14), (2, 9, 7, 28, 28), (1, 40, 12, 56, 56), (2, 3, 4, 6, 2), (1, 5, 6, 10, 130),
+    (1, 7, 9, 8, 112), (1, 4, 8, 6, 224), (1, 300, 20, 14, 14), (3, 12, 5, 18, 62),
+]
+
+
+@pytest.mark.parametrize("algo", [0, 1])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("shape", POOL_SHAPES)
+def test_conv_pool_fused(shape, dtype, algo):
+    torch = torch_mod()
+    n, cin, cout, h, w = shape
+    wt, masks, keep = _case(n * 700 + cin * 13 + cout, cout, cin, 8, 50, dtype)
+    prep = gpu_prepare(wt, masks, keep)
+    x = inputs.normal_activations(h * 3 + w, (n, cin, h, w), dtype)
+    bias = inputs.bias_vector(cout + 5, cout, dtype) if (cin % 2) else None
+    relu = bool(cout % 2)
+    y = torch.empty((n, cout, h // 2, w // 2), dtype=getattr(torch, np.dtype(dtype).name), device="cuda")
+    note("conv+pool %s %s algo=%d" % (shape, np.dtype(dtype).name, algo))
+    B.conv3x3_fwd_pool2(prep.layer, prep.packed, dev(x), y, bias=None if bias is None else dev(bias),
+                        relu=relu, algo=algo)
+    torch.cuda.synchronize()
+    packed = prep.packed.to_host()
+    ref = oracle.maxpool2x2(oracle.conv_sparse(x, packed, masks, cout, bias=bias, relu=relu))
+    err = norm_err(y.cpu().numpy(), ref)
+    assert err <= TOL[dtype], "normwise error %.3e" % err
+
+
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
 def test_maxpool(dtype):
     torch = torch_mod()

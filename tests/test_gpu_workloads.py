@@ -70,6 +70,16 @@ def test_vgg16_stack_chained():
     for li, lay in enumerate(wl.layers):
         y = _check_layer(wl, li, lay, masks, x)
         if lay.pool_after:
+            # the fused conv + ReLU + pool launch the benchmark uses
+            prep = B.prepare(dev(inputs.layer_weights(wl, li)), masks, lay.keep)
+            fused = torch.empty((wl.batch, lay.cout, lay.h // 2, lay.w // 2), dtype=y.dtype, device="cuda")
+            note("%s %s fused conv+pool" % (wl.name, lay.name))
+            B.conv3x3_fwd_pool2(prep.layer, prep.packed, x, fused, relu=lay.relu)
+            torch.cuda.synchronize()
+            ref = oracle.maxpool2x2(oracle.conv_sparse(x.cpu().numpy(), prep.packed.to_host(), masks, lay.cout,
+                                                       relu=lay.relu))
+            err = norm_err(fused.cpu().numpy(), ref)
+            assert err <= TOL[wl.np_dtype], "%s %s fused: normwise error %.3e" % (wl.name, lay.name, err)
             p = torch.empty((wl.batch, lay.cout, lay.h // 2, lay.w // 2), dtype=y.dtype, device="cuda")
             note("%s %s pool" % (wl.name, lay.name))
             B.maxpool2x2(y, p)
