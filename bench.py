@@ -135,6 +135,7 @@ class Net:
                 torch.cuda.synchronize()
                 t[fused] = s.elapsed_time(e)
             L["fused"] = t[True] < t[False]
+            L["fusion_us"] = [round(t[False] * 1e3 / reps, 2), round(t[True] * 1e3 / reps, 2)]
 
     def output(self):
         L = self.layers[-1]
@@ -321,6 +322,7 @@ def main():
         "config": {"workload": wl.name, "batch": wl.batch, "layers": len(wl.layers), "m": wl.m,
                    "stack": "conv+relu, 2x2 max-pool after conv2/4/7/10" if wl.chained else "independent layers",
                    "pool_fused_into": [L["lay"].name for L in net.layers if L["fused"]]},
+        "pool_fusion_us_unfused_fused": {L["lay"].name: L["fusion_us"] for L in net.layers if "fusion_us" in L},
         "step_launch": "hip graph replay" if graph else "eager",
         "ms_per_step_eager": round(ms_eager, 4),
         "ms_per_layer": {L["lay"].name: round(t, 4) for L, t in zip(net.layers, layer_ms)},

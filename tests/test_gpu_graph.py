@@ -1,6 +1,7 @@
 """HIP graph capture of the conv and pool launches (the benchmark replays a
-captured step): every replay must equal the eager result bit for bit, also
-with eager work and synchronisations between the replays."""
+captured step, with the pool either its own launch or fused into the conv
+launch): every replay must equal the eager result bit for bit, also with
+eager work and synchronisations between the replays."""
 import numpy as np
 import pytest
 
@@ -19,8 +20,9 @@ def _need_gpu():
     B.lib()
 
 
+@pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
-def test_graph_replays_match_eager(dtype):
+def test_graph_replays_match_eager(dtype, fused):
     torch = torch_mod()
     tdt = torch.float32 if dtype == np.float32 else torch.float16
     # conv 8->16 @ 28x28 (+ReLU, pool) -> conv 16->32 @ 14x14 (split shares) -> conv 32->32 @ 14x14
@@ -37,12 +39,15 @@ def test_graph_replays_match_eager(dtype):
     x = dev(inputs.normal_activations(71, (n, 8, 28, 28), dtype))
 
     def step():
-        B.conv3x3_fwd(preps[0].layer, preps[0].packed, x, bufs[0], relu=True)
-        B.maxpool2x2(bufs[0], pooled)
+        if fused:
+            B.conv3x3_fwd_pool2(preps[0].layer, preps[0].packed, x, pooled, relu=True)
+        else:
+            B.conv3x3_fwd(preps[0].layer, preps[0].packed, x, bufs[0], relu=True)
+            B.maxpool2x2(bufs[0], pooled)
         B.conv3x3_fwd(preps[1].layer, preps[1].packed, pooled, bufs[1], relu=True)
         B.conv3x3_fwd(preps[2].layer, preps[2].packed, bufs[1], bufs[2], relu=False)
 
-    note("graph eager reference %s" % np.dtype(dtype).name)
+    note("graph eager reference %s fused=%s" % (np.dtype(dtype).name, fused))
     step()
     torch.cuda.synchronize()
     ref = bufs[2].clone()
