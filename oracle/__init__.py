@@ -66,11 +66,13 @@ def _load():
     lib.pso_unpack.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P, P]
     lib.pso_conv_sparse.argtypes = [P, i32, i32, i32, i32, i32, i32, i32, P,
                                     P, P, P, P, P, P, i32, P, P]
+    lib.pso_conv_sparse_strided.argtypes = [P, i32, i32, i32, i32, i32, i32, i32, P,
+                                            P, P, P, P, P, P, i32, i32, P]
     lib.pso_conv_dense.argtypes = [P, i32, i32, i32, i32, i32, P, i32, P, i32, P]
     lib.pso_maxpool2x2.argtypes = [P, i64, i32, i32, P]
     for name in ("pso_select_library", "pso_project", "pso_select", "pso_pack",
                  "pso_mask_weights", "pso_unpack", "pso_conv_sparse",
-                 "pso_conv_dense", "pso_maxpool2x2"):
+                 "pso_conv_sparse_strided", "pso_conv_dense", "pso_maxpool2x2"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -208,6 +210,30 @@ def conv_sparse(x: np.ndarray, packed: dict, masks, cout: int, bias=None,
         _ptr(vals), _ptr(bias), int(bool(relu)), _ptr(y), _ptr(s)),
         "conv_sparse")
     return (y, s) if want_scale else y
+
+
+def conv_sparse_strided(x: np.ndarray, packed: dict, masks, cout: int, stride: int, bias=None,
+                        relu: bool = False):
+    """Sec. 4.1 Eq. 1 with a stride (1 or 2; zero padding 1), from the
+    compressed storage: fp64 output [n][cout][(h-1)//stride+1][(w-1)//stride+1]."""
+    x = np.ascontiguousarray(x)
+    n, cin, h, w = (int(d) for d in x.shape)
+    masks = np.ascontiguousarray(masks, dtype=np.uint16)
+    vals = np.ascontiguousarray(packed["values"])
+    if vals.size and vals.dtype != x.dtype:
+        raise TypeError("weights and activations must share a dtype")
+    if bias is not None:
+        bias = np.ascontiguousarray(bias, dtype=x.dtype)
+    y = np.zeros((n, cout, (h - 1) // stride + 1, (w - 1) // stride + 1), dtype=np.float64)
+    _check(_load().pso_conv_sparse_strided(
+        _ptr(x), _dtype_code(x), n, cin, h, w, cout, len(masks), _ptr(masks),
+        _ptr(np.ascontiguousarray(packed["filter_perm"], dtype=np.int32)),
+        _ptr(np.ascontiguousarray(packed["filter_ptr"], dtype=np.int32)),
+        _ptr(np.ascontiguousarray(packed["cin_idx"], dtype=np.int32)),
+        _ptr(np.ascontiguousarray(packed["pat_id"], dtype=np.uint8)),
+        _ptr(vals), _ptr(bias), int(bool(relu)), int(stride), _ptr(y)),
+        "conv_sparse_strided")
+    return y
 
 
 def conv_dense(x: np.ndarray, wdense: np.ndarray, bias=None, relu: bool = False):

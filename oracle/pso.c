@@ -18,6 +18,8 @@
  *   pso_unpack          compressed storage -> dense OIHW     (Sec. 3.4)
  *   pso_conv_sparse     X_n = sigma(W_n X_{n-1} + b_n) from
  *                       the compressed storage               (Sec. 4.1, Eq. 1)
+ *   pso_conv_sparse_strided  the same layer with stride 1 or 2
+ *                       (stage-entry convs of the pruned ResNets)
  *   pso_conv_dense      textbook dense direct convolution of
  *                       zero-masked OIHW weights (witness)   (Sec. 4.1, Eq. 1)
  *   pso_maxpool2x2      2x2/2 max-pool between VGG-16 layers
@@ -435,6 +437,59 @@ int pso_conv_sparse(const void *x, int dtype, int n, int cin, int h, int w,
             yp[q] = (relu && v < 0.0) ? 0.0 : v;
             if (sp)
                 sp[q] += fabs(b);
+        }
+    }
+    return bad ? -1 : 0;
+}
+
+/* The same layer with a stride (the stage-entry convolutions of the ResNets
+ * the paper prunes): 3x3, zero padding 1, stride st in {1, 2}.  Output
+ * position (oh, ow) reads input (st*oh + r - 1, st*ow + s - 1); the output is
+ * [n][cout][OH][OW] with OH = (h - 1) / st + 1, OW = (w - 1) / st + 1.  y is
+ * written in full; the loop order is the plain one, per output pixel. */
+int pso_conv_sparse_strided(const void *x, int dtype, int n, int cin, int h, int w,
+                            int cout, int m, const uint16_t *masks,
+                            const int32_t *filter_perm, const int32_t *filter_ptr,
+                            const int32_t *cin_idx, const uint8_t *pat_id,
+                            const void *values, const void *bias, int relu,
+                            int st, double *y)
+{
+    if (n < 0 || cin < 0 || h < 1 || w < 1 || cout < 0 || m < 1 || m > 126 || st < 1 || st > 2)
+        return -1;
+    const int OH = (h - 1) / st + 1, OW = (w - 1) / st + 1;
+    const size_t plane = (size_t)h * w, oplane = (size_t)OH * OW;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t t = 0; t < (int64_t)n * cout; ++t) {
+        int nn = (int)(t / cout);
+        int i = (int)(t % cout);
+        int f = filter_perm[i];
+        double b = bias ? elem(bias, dtype, (size_t)f) : 0.0;
+        for (int oh = 0; oh < OH; ++oh) {
+            for (int ow = 0; ow < OW; ++ow) {
+                double acc = 0.0;
+                for (int32_t k = filter_ptr[i]; k < filter_ptr[i + 1]; ++k) {
+                    int ci = cin_idx[k];
+                    int p = pat_id[k];
+                    if (p >= m || ci < 0 || ci >= cin) {
+                        bad = 1;
+                        continue;
+                    }
+                    int j = 0;
+                    for (int q = 0; q < 9; ++q) {
+                        if (!((masks[p] >> q) & 1))
+                            continue;
+                        double v = elem(values, dtype, (size_t)k * 4 + j);
+                        j += 1;
+                        int ih = st * oh + q / 3 - 1, iw = st * ow + q % 3 - 1;
+                        if (ih < 0 || ih >= h || iw < 0 || iw >= w)
+                            continue;
+                        acc += v * elem(x, dtype, ((size_t)nn * cin + ci) * plane + (size_t)ih * w + iw);
+                    }
+                }
+                double v = acc + b;
+                y[((size_t)nn * cout + f) * oplane + (size_t)oh * OW + ow] = (relu && v < 0.0) ? 0.0 : v;
+            }
         }
     }
     return bad ? -1 : 0;

@@ -434,3 +434,58 @@ def test_maxpool_matches_block_max():
     assert np.array_equal(y, x.reshape(2, 3, 3, 2, 4, 2).max(axis=(3, 5)))
     with pytest.raises(ValueError):
         oracle.maxpool2x2(np.zeros((1, 1, 3, 4)))
+
+
+# ------------------------------------------- Eq. 1 with stride (stage entry)
+@pytest.mark.parametrize("n,cin,cout,h,w", [(2, 5, 7, 9, 11), (1, 3, 4, 1, 1), (1, 6, 5, 2, 2),
+                                            (3, 8, 8, 8, 13), (1, 16, 6, 7, 3)])
+@pytest.mark.parametrize("relu,use_bias", [(False, False), (True, True)])
+def test_conv_strided_equals_torch_and_subsampled_stride1(n, cin, cout, h, w, relu, use_bias):
+    """Stride 2: torch.conv2d (fp64, CPU) on the masked dense weights, and the
+    stride-1 output sampled at even rows and columns; stride 1 reduces to the
+    pinned stride-1 conv."""
+    torch = pytest.importorskip("torch")
+    wt, masks, pat, keep, packed = _prepared(cin * 17 + cout, cout, cin, 8, 40)
+    x = inputs.normal_activations(7, (n, cin, h, w))
+    b = inputs.bias_vector(8, cout) if use_bias else None
+    y2 = oracle.conv_sparse_strided(x, packed, masks, cout, 2, bias=b, relu=relu)
+    assert y2.shape == (n, cout, (h + 1) // 2, (w + 1) // 2)
+    masked = oracle.mask_weights(wt, masks, pat, keep)
+    yt = torch.nn.functional.conv2d(
+        torch.from_numpy(x.astype(np.float64)), torch.from_numpy(masked.astype(np.float64)),
+        None if b is None else torch.from_numpy(b.astype(np.float64)), stride=2, padding=1)
+    if relu:
+        yt = torch.relu(yt)
+    y1 = oracle.conv_sparse(x, packed, masks, cout, bias=b, relu=relu)
+    scale = max(1.0, float(np.abs(y1).max()))
+    assert yt.shape == y2.shape
+    assert float(np.abs(y2 - yt.numpy()).max()) <= 1e-12 * scale
+    assert float(np.abs(y2 - y1[:, :, ::2, ::2]).max()) <= 1e-12 * scale
+    assert float(np.abs(oracle.conv_sparse_strided(x, packed, masks, cout, 1, bias=b, relu=relu) - y1).max()) \
+        <= 1e-12 * scale
+
+
+def test_conv_strided_impulse_footprint():
+    """A unit impulse at input (h0, w0) reaches exactly the stride-2 outputs
+    (oh, ow) with 2*oh + r - 1 = h0 and 2*ow + s - 1 = w0, with weight (r, s)."""
+    cin, cout, h, w = 3, 4, 9, 8
+    wt, masks, pat, keep, packed = _prepared(33, cout, cin, 6, 30)
+    masked = oracle.mask_weights(wt, masks, pat, keep).astype(np.float64)
+    for h0, w0 in [(0, 0), (3, 4), (4, 5), (8, 7)]:
+        x = np.zeros((1, cin, h, w), dtype=np.float32)
+        x[0, 1, h0, w0] = 1.0
+        y = oracle.conv_sparse_strided(x, packed, masks, cout, 2)
+        want = np.zeros_like(y)
+        for r in range(3):
+            for s in range(3):
+                oh2, ow2 = h0 - r + 1, w0 - s + 1
+                if oh2 % 2 == 0 and ow2 % 2 == 0 and 0 <= oh2 // 2 < y.shape[2] and 0 <= ow2 // 2 < y.shape[3]:
+                    want[0, :, oh2 // 2, ow2 // 2] = masked[:, 1, r, s]
+        assert np.array_equal(y, want)
+
+
+def test_conv_strided_rejects_bad_stride():
+    wt, masks, pat, keep, packed = _prepared(3, 2, 2, 4, 0)
+    x = inputs.normal_activations(1, (1, 2, 4, 4))
+    with pytest.raises(Exception):
+        oracle.conv_sparse_strided(x, packed, masks, 2, 3)
