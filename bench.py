@@ -81,7 +81,7 @@ class Net:
             prep = B.prepare(w, self.masks, lay.keep)
             if not wl.chained and li > 0:
                 x = torch.from_numpy(inputs.layer_input(wl, li)).cuda()
-            y = torch.empty((n, lay.cout, lay.h, lay.w), dtype=tdt, device="cuda")
+            y = torch.empty((n, lay.cout) + lay.out_hw, dtype=tdt, device="cuda")
             pooled = None
             if lay.pool_after:
                 pooled = torch.empty((n, lay.cout, lay.h // 2, lay.w // 2), dtype=tdt, device="cuda")
@@ -99,6 +99,9 @@ class Net:
                 # conv, ReLU and the 2x2 max-pool in one launch
                 B.conv3x3_fwd_pool2(L["prep"].layer, L["prep"].packed, L["x"], L["pooled"], relu=L["lay"].relu,
                                     algo=self.algo)
+            elif L["lay"].stride != 1:
+                B.conv3x3_fwd_strided(L["prep"].layer, L["prep"].packed, L["x"], L["y"], L["lay"].stride,
+                                      relu=L["lay"].relu, algo=self.algo)
             else:
                 B.conv3x3_fwd(L["prep"].layer, L["prep"].packed, L["x"], L["y"], relu=L["lay"].relu,
                               algo=self.algo)
@@ -143,7 +146,8 @@ class Net:
 
     def nz_flops(self, li):
         lay = self.layers[li]["lay"]
-        return 8.0 * self.wl.batch * lay.h * lay.w * lay.keep
+        oh, ow = lay.out_hw
+        return 8.0 * self.wl.batch * oh * ow * lay.keep
 
 
 def cpu_baseline(net, budget_s=10.0):
@@ -157,9 +161,12 @@ def cpu_baseline(net, budget_s=10.0):
     while secs < budget_s:
         for lay, packed, x in host:
             t0 = time.perf_counter()
-            oracle.conv_sparse(x, packed, net.masks, lay.cout, relu=lay.relu)
+            if lay.stride == 1:
+                oracle.conv_sparse(x, packed, net.masks, lay.cout, relu=lay.relu)
+            else:
+                oracle.conv_sparse_strided(x, packed, net.masks, lay.cout, lay.stride, relu=lay.relu)
             secs += time.perf_counter() - t0
-            flops += 8.0 * lay.h * lay.w * lay.keep
+            flops += 8.0 * lay.out_hw[0] * lay.out_hw[1] * lay.keep
             layers += 1
             if secs >= budget_s:
                 break
@@ -204,6 +211,8 @@ def compare_dense(net, reps=20):
     out = []
     for L in net.layers:
         lay, prep = L["lay"], L["prep"]
+        if lay.stride != 1:
+            continue                     # the dense comparators are stride 1
         wd = torch.empty(L["w"].shape, dtype=net.tdt, device="cuda")
         B.unpack_dense(prep.layer, prep.packed, wd)
         yd = torch.empty_like(L["y"])
@@ -310,7 +319,10 @@ def main():
                                    [L["lay"].name for L in net.layers if L["fused"]])
     roof = {"bound": "alu", "achieved": round(achieved_tf, 3), "peak": PEAK_VALU_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved_tf / PEAK_VALU_TFLOPS, 4), "traffic": traffic,
-            "kernel": "k_conv_wide (224- and 112-wide layers) + k_conv_stream (the others)",
+            "kernel": ("k_conv_wide (224- and 112-wide layers) + k_conv_stream (the others)"
+                   if wl.name == "vgg16_224_b1_f32" else
+                   "k_conv_stream / k_conv_wide" + (" + k_conv_simple (stride-2 layers)"
+                                                    if any(L["lay"].stride != 1 for L in net.layers) else "")),
             "per_launch": "8*N*H*W*keep nonzero-MAC flops averaged over the %d conv launches of a step, "
                           "/ their mean duration (HIP events on the launch stream)" % len(net.layers),
             "avg_launch_us": round(conv_ms * 1e3 / len(net.layers), 3)}

@@ -169,6 +169,22 @@ psc_status psc_conv3x3_fwd_pool2(const psc_layer *layer, const psc_packed *packe
                                  int32_t h, int32_t w, const void *d_bias,
                                  int32_t relu, void *d_y, int32_t algo, void *stream);
 
+/* Sec. 4.1, Eq. 1 with a stride, for the stage-entry convolutions of the
+ * ResNets the paper prunes: 3x3, zero padding 1, stride 1 or 2.  d_y is
+ * [n][cout][OH][OW] (original filter order), OH = (h-1)/stride + 1,
+ * OW = (w-1)/stride + 1, and
+ *   y[n,f,i,j] = sigma(b[f] + sum over kept (ci, p) of f of
+ *                sum_{(r,s) in p} v * x[n, ci, stride*i + r - 1, stride*j + s - 1])
+ * with out-of-image taps reading zero.  stride 1 is psc_conv3x3_fwd_algo.
+ * Stride 2 runs on the one-output-per-lane kernel for either algo.  Other
+ * conventions and errors as in psc_conv3x3_fwd_algo; a stride other than 1
+ * or 2 returns PSC_ERR_ARG. */
+psc_status psc_conv3x3_fwd_strided(const psc_layer *layer, const psc_packed *packed,
+                                   int32_t act_dtype, const void *d_x, int32_t n,
+                                   int32_t h, int32_t w, const void *d_bias,
+                                   int32_t relu, void *d_y, int32_t stride, int32_t algo,
+                                   void *stream);
+
 /* Comparator: the dense 3x3 convolution (stride 1, pad 1) of dense OIHW
  * weights d_w [cout][cin][3][3] on the vector ALUs, same conventions and
  * accumulation as psc_conv3x3_fwd. */

@@ -84,6 +84,7 @@ def lib() -> ctypes.CDLL:
         "psc_conv3x3_fwd": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, P], ctypes.c_int),
         "psc_conv3x3_fwd_algo": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, P], ctypes.c_int),
         "psc_conv3x3_fwd_pool2": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, P], ctypes.c_int),
+        "psc_conv3x3_fwd_strided": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, i32, P], ctypes.c_int),
         "psc_dense3x3_fwd": ([i32, P, i32, i32, i32, i32, P, i32, P, i32, P, P], ctypes.c_int),
         "psc_maxpool2x2": ([i32, P, i32, i32, i32, i32, P, P], ctypes.c_int),
     }
@@ -255,6 +256,21 @@ def conv3x3_fwd_pool2(layer: Layer, packed: Packed, x, y, bias=None, relu: bool 
     _check(lib().psc_conv3x3_fwd_pool2(layer.ref(), ctypes.byref(cp), dtype_code(x), _dev(x, "x"), n, h,
                                        w, _dev(bias, "bias"), int(bool(relu)), _dev(y, "y"), int(algo),
                                        _stream(stream)), "psc_conv3x3_fwd_pool2")
+
+
+def conv3x3_fwd_strided(layer: Layer, packed: Packed, x, y, stride: int, bias=None, relu: bool = False,
+                        algo: int = 0, stream=None):
+    """psc_conv3x3_fwd_strided: y is [n][cout][(h-1)//stride+1][(w-1)//stride+1]."""
+    n, cin, h, w = (int(d) for d in x.shape)
+    stride = int(stride)
+    if stride not in (1, 2):
+        raise ValueError("stride must be 1 or 2")
+    if cin != layer.cin or tuple(y.shape) != (n, layer.cout, (h - 1) // stride + 1, (w - 1) // stride + 1):
+        raise ValueError("x/y shapes do not match the layer and the stride")
+    cp = packed.c()
+    _check(lib().psc_conv3x3_fwd_strided(layer.ref(), ctypes.byref(cp), dtype_code(x), _dev(x, "x"), n, h, w,
+                                         _dev(bias, "bias"), int(bool(relu)), _dev(y, "y"), stride,
+                                         int(algo), _stream(stream)), "psc_conv3x3_fwd_strided")
 
 
 def dense3x3_fwd(x, wd, y, bias=None, relu: bool = False, stream=None):

@@ -13,7 +13,8 @@ namespace {
 
 // One output pixel per lane; with pool, one pooled pixel: the maximum of
 // the four outputs of its 2x2 window (sigma and max commute, the bias is
-// common to the window).
+// common to the window).  With stride 2 (no pool) output (oh, ow) reads the
+// input around (2 oh, 2 ow).
 template <int DT>
 __global__ __launch_bounds__(256) void k_conv_simple(const typename Elt<DT>::T* __restrict__ x, int cin,
                                                      int H, int W, int cout, PatTable tab,
@@ -23,14 +24,16 @@ __global__ __launch_bounds__(256) void k_conv_simple(const typename Elt<DT>::T* 
                                                      const uint8_t* __restrict__ pat_id,
                                                      const typename Elt<DT>::T* __restrict__ values,
                                                      const typename Elt<DT>::T* __restrict__ bias,
-                                                     int relu, int pool, typename Elt<DT>::T* __restrict__ y) {
+                                                     int relu, int pool, int stride,
+                                                     typename Elt<DT>::T* __restrict__ y) {
     using E = Elt<DT>;
     __shared__ uint16_t msk[kMaxPatterns];
     for (int p = threadIdx.x; p < tab.m; p += 256) msk[p] = tab.mask[p];
     __syncthreads();
     const int i = blockIdx.y, n = blockIdx.z;
     const int plane = H * W;
-    const int OW = pool ? W / 2 : W, oplane = pool ? plane / 4 : plane;
+    const int OW = pool ? W / 2 : (W - 1) / stride + 1;
+    const int oplane = pool ? plane / 4 : ((H - 1) / stride + 1) * OW;
     const int pix = blockIdx.x * 256 + threadIdx.x;
     if (pix >= oplane) return;
     const int ph = pix / OW, pw = pix - ph * OW;
@@ -39,7 +42,8 @@ __global__ __launch_bounds__(256) void k_conv_simple(const typename Elt<DT>::T* 
     float best = 0.f;
     const int nwin = pool ? 4 : 1;
     for (int t = 0; t < nwin; ++t) {
-        const int oh = pool ? 2 * ph + (t >> 1) : ph, ow = pool ? 2 * pw + (t & 1) : pw;
+        // output position in stride-1 coordinates (centre of the 3x3 window)
+        const int oh = pool ? 2 * ph + (t >> 1) : stride * ph, ow = pool ? 2 * pw + (t & 1) : stride * pw;
         float acc = 0.f;
         for (int k = fptr[i]; k < fptr[i + 1]; ++k) {
             const int ci = cin_idx[k], p = pat_id[k];
@@ -144,12 +148,12 @@ __global__ __launch_bounds__(256) void k_maxpool(const typename Elt<DT>::T* __re
 template <int DT>
 hipError_t conv_simple(const PatTable& tab, const PackedView& pk, const ConvArgs& a, hipStream_t s) {
     using T = typename Elt<DT>::T;
-    const int outs = a.pool ? (a.h / 2) * (a.w / 2) : a.h * a.w;
+    const int outs = a.pool ? (a.h / 2) * (a.w / 2) : ((a.h - 1) / a.stride + 1) * ((a.w - 1) / a.stride + 1);
     const dim3 grid(unsigned((outs + 255) / 256), unsigned(a.cout), unsigned(a.n));
     hipLaunchKernelGGL(k_conv_simple<DT>, grid, dim3(256), 0, s, static_cast<const T*>(a.x), a.cin, a.h,
                        a.w, a.cout, tab, pk.filter_perm, pk.filter_ptr, pk.cin_idx, pk.pat_id,
                        static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), a.relu, a.pool,
-                       static_cast<T*>(a.y));
+                       a.stride, static_cast<T*>(a.y));
     return hipGetLastError();
 }
 
@@ -157,11 +161,12 @@ hipError_t conv_simple(const PatTable& tab, const PackedView& pk, const ConvArgs
 
 hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs& a, int algo,
                        hipStream_t stream) {
-    if (algo == 0) {
+    if (algo == 0 && a.stride == 1) {
         const hipError_t e = launch_conv_stream(tab, pk, a, stream);
         if (e != hipErrorNotSupported) return e;
-        // inputs beyond the 2 GiB one buffer descriptor covers, and pooled
-        // outputs of haloed column tiles, take the one-output-per-lane kernel
+        // inputs beyond the 2 GiB one buffer descriptor covers, pooled
+        // outputs of haloed column tiles and strided layers take the
+        // one-output-per-lane kernel
     }
     return a.dtype == DT_F16 ? conv_simple<DT_F16>(tab, pk, a, stream)
                              : conv_simple<DT_F32>(tab, pk, a, stream);

@@ -55,6 +55,7 @@ struct ConvArgs {
     int relu;
     void* y;
     int pool;       // 1: y is the 2x2/2 max-pool of sigma(conv), [n][cout][h/2][w/2]
+    int stride = 1; // 1 or 2 (zero padding 1): y is [n][cout][(h-1)/stride+1][(w-1)/stride+1]
 };
 hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs& a, int algo,
                        hipStream_t stream);

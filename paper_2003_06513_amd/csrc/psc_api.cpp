@@ -266,7 +266,7 @@ psc_status psc_unpack_dense(const psc_layer* L, const psc_packed* pk, void* d_w_
 
 static psc_status conv_common(const psc_layer* L, const psc_packed* pk, int32_t act_dtype, const void* d_x,
                               int32_t n, int32_t h, int32_t w, const void* d_bias, int32_t relu, void* d_y,
-                              int32_t algo, int pool, void* stream) {
+                              int32_t algo, int pool, int32_t stride, void* stream) {
     if (psc_status s = check_layer(L, true)) return s;
     if (psc_status s = check_packed(L, pk)) return s;
     if (!dtype_ok(act_dtype)) return fail(PSC_ERR_ARG, "act_dtype=%d is not a psc_dtype", act_dtype);
@@ -277,8 +277,10 @@ static psc_status conv_common(const psc_layer* L, const psc_packed* pk, int32_t 
         return fail(PSC_ERR_ARG, "h=%d, w=%d outside 1..32768", h, w);
     if (algo < 0 || algo > 1) return fail(PSC_ERR_ARG, "algo=%d is not 0 or 1", algo);
     if (pool && ((h & 1) || (w & 1))) return fail(PSC_ERR_ARG, "h=%d, w=%d must be even for the 2x2 pool", h, w);
+    if (stride != 1 && stride != 2) return fail(PSC_ERR_ARG, "stride=%d is not 1 or 2", stride);
     const int64_t plane = int64_t(h) * w;
-    const int64_t xe = int64_t(n) * L->cin * plane, ye = int64_t(n) * L->cout * (pool ? plane / 4 : plane);
+    const int64_t oplane = pool ? plane / 4 : int64_t((h - 1) / stride + 1) * ((w - 1) / stride + 1);
+    const int64_t xe = int64_t(n) * L->cin * plane, ye = int64_t(n) * L->cout * oplane;
     if (xe > kMaxElems || ye > kMaxElems)
         return fail(PSC_ERR_ARG, "x or y holds more than 2^31-1 elements");
     if (n == 0) return ok();
@@ -291,7 +293,7 @@ static psc_status conv_common(const psc_layer* L, const psc_packed* pk, int32_t 
     const psc::PatTable t = table_of(L);
     const psc::PackedView v{pk->filter_perm, pk->filter_ptr, pk->seg_ptr,
                             pk->cin_idx,     pk->pat_id,     pk->values};
-    const psc::ConvArgs a{act_dtype, n, L->cin, h, w, L->cout, L->keep, d_x, d_bias, relu != 0, d_y, pool};
+    const psc::ConvArgs a{act_dtype, n, L->cin, h, w, L->cout, L->keep, d_x, d_bias, relu != 0, d_y, pool, stride};
     return device_status(psc::launch_conv(t, v, a, algo, as_stream(stream)), "psc_conv3x3_fwd launch");
 }
 
@@ -299,19 +301,25 @@ psc_status psc_conv3x3_fwd_algo(const psc_layer* L, const psc_packed* pk, int32_
                                 const void* d_x, int32_t n, int32_t h, int32_t w,
                                 const void* d_bias, int32_t relu, void* d_y, int32_t algo,
                                 void* stream) {
-    return conv_common(L, pk, act_dtype, d_x, n, h, w, d_bias, relu, d_y, algo, 0, stream);
+    return conv_common(L, pk, act_dtype, d_x, n, h, w, d_bias, relu, d_y, algo, 0, 1, stream);
 }
 
 psc_status psc_conv3x3_fwd(const psc_layer* L, const psc_packed* pk, int32_t act_dtype,
                            const void* d_x, int32_t n, int32_t h, int32_t w, const void* d_bias,
                            int32_t relu, void* d_y, void* stream) {
-    return conv_common(L, pk, act_dtype, d_x, n, h, w, d_bias, relu, d_y, 0, 0, stream);
+    return conv_common(L, pk, act_dtype, d_x, n, h, w, d_bias, relu, d_y, 0, 0, 1, stream);
 }
 
 psc_status psc_conv3x3_fwd_pool2(const psc_layer* L, const psc_packed* pk, int32_t act_dtype,
                                  const void* d_x, int32_t n, int32_t h, int32_t w, const void* d_bias,
                                  int32_t relu, void* d_y, int32_t algo, void* stream) {
-    return conv_common(L, pk, act_dtype, d_x, n, h, w, d_bias, relu, d_y, algo, 1, stream);
+    return conv_common(L, pk, act_dtype, d_x, n, h, w, d_bias, relu, d_y, algo, 1, 1, stream);
+}
+
+psc_status psc_conv3x3_fwd_strided(const psc_layer* L, const psc_packed* pk, int32_t act_dtype,
+                                   const void* d_x, int32_t n, int32_t h, int32_t w, const void* d_bias,
+                                   int32_t relu, void* d_y, int32_t stride, int32_t algo, void* stream) {
+    return conv_common(L, pk, act_dtype, d_x, n, h, w, d_bias, relu, d_y, algo, 0, stride, stream);
 }
 
 psc_status psc_dense3x3_fwd(int32_t dtype, const void* d_x, int32_t n, int32_t cin, int32_t h,

@@ -28,7 +28,7 @@ DTYPES = {"f32": np.float32, "f16": np.float16}
 
 @dataclasses.dataclass(frozen=True)
 class ConvLayer:
-    """One 3x3, stride-1, pad-1 layer of a workload."""
+    """One 3x3, pad-1 layer of a workload (h, w: input size)."""
     name: str
     cin: int
     cout: int
@@ -37,6 +37,11 @@ class ConvLayer:
     keep: int            # beta: exact number of kernels kept
     relu: bool = False
     pool_after: bool = False   # 2x2/2 max-pool follows (VGG stack only)
+    stride: int = 1            # 2: output (h-1)//2+1 x (w-1)//2+1 (ResNet stage entries)
+
+    @property
+    def out_hw(self) -> Tuple[int, int]:
+        return (self.h - 1) // self.stride + 1, (self.w - 1) // self.stride + 1
 
     @property
     def n_kernels(self) -> int:
@@ -122,6 +127,18 @@ def resnet18_cifar_3x3(batch: int = 256) -> Workload:
     return Workload("resnet18_cifar_3x3_b%d_f32" % batch, 4, batch, "f32", 6, tuple(layers))
 
 
+def resnet18_cifar_entry(batch: int = 256) -> Workload:
+    """The 3x3 convolutions of a CIFAR-shaped ResNet-18 that change the
+    channel count: the stem 3->64 at 32x32 (stride 1, every kernel kept) and
+    the stride-2 stage entries 64->128 at 32x32, 128->256 at 16x16 and
+    256->512 at 8x8 (70 % of kernels dropped); fp32, 6 patterns."""
+    layers = [ConvLayer("stem", 3, 64, 32, 32, 3 * 64, relu=True)]
+    for ci, s in ((64, 32), (128, 16), (256, 8)):
+        layers.append(ConvLayer("entry%d_s%d" % (2 * ci, s), ci, 2 * ci, s, s,
+                                keep_after_drop(ci * 2 * ci, 70), relu=True, stride=2))
+    return Workload("resnet18_cifar_entry_b%d_f32" % batch, 6, batch, "f32", 6, tuple(layers))
+
+
 def sweep_512(m: int, drop: int, batch: int = 64) -> Workload:
     """One 512->512 layer at 28x28, fp16, library size m, drop ratio drop %."""
     return Workload("sweep_512c_28x28_b%d_f16_m%d_d%d" % (batch, m, drop), 5, batch,
@@ -132,7 +149,7 @@ def sweep_512(m: int, drop: int, batch: int = 64) -> Workload:
 
 def all_workloads() -> List[Workload]:
     out = [single_layer_64(), vgg16_stack(1), resnet50_3x3(1), resnet50_3x3(32),
-           resnet18_cifar_3x3(256)]
+           resnet18_cifar_3x3(256), resnet18_cifar_entry(256)]
     for m in (4, 8, 12):
         for d in (0, 40, 60, 80):
             out.append(sweep_512(m, d))

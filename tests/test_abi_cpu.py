@@ -150,6 +150,13 @@ def test_conv_validation(L):
         assert rc == B.PSC_ERR_ARG and "even" in msg
     assert L.psc_conv3x3_fwd_pool2(lay.ref(), ctypes.byref(cp), B.PSC_F32, FAKE, 0, 4, 4, None, 0, FAKE, 0,
                                    None) == B.PSC_OK
+    # strided conv: only stride 1 or 2; the output size follows the stride
+    for st in (0, 3, -1):
+        rc, msg = _status(L.psc_conv3x3_fwd_strided(lay.ref(), ctypes.byref(cp), B.PSC_F32, FAKE, 1, 5, 5, None,
+                                                    0, ctypes.c_void_p(0x20000), st, 0, None))
+        assert rc == B.PSC_ERR_ARG and "stride" in msg
+    assert L.psc_conv3x3_fwd_strided(lay.ref(), ctypes.byref(cp), B.PSC_F32, FAKE, 0, 5, 5, None, 0, FAKE, 2, 0,
+                                     None) == B.PSC_OK
 
 
 def test_dense_and_pool_validation(L):

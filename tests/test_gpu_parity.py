@@ -233,6 +233,46 @@ def test_conv_pool_fused(shape, dtype, algo):
     assert err <= TOL[dtype], "normwise error %.3e" % err
 
 
+STRIDE_SHAPES = [
+    # n, cin, cout, h, w: ResNet stage entries (even sizes), odd and ragged
+    # sizes, 1x1 and 1-row images, more outputs than one block of lanes
+    (2, 64, 128, 32, 32), (1, 128, 256, 16, 16), (2, 256, 64, 8, 8), (1, 5, 7, 9, 11), (3, 4, 5, 1, 1),
+    (1, 6, 4, 2, 3), (2, 7, 9, 13, 6), (1, 3, 8, 1, 40), (1, 9, 6, 45, 37),
+]
+
+
+@pytest.mark.parametrize("algo", [0, 1])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("shape", STRIDE_SHAPES)
+def test_conv_strided(shape, dtype, algo):
+    torch = torch_mod()
+    tdt = getattr(torch, np.dtype(dtype).name)
+    n, cin, cout, h, w = shape
+    wt, masks, keep = _case(n * 500 + cin * 7 + cout, cout, cin, 8, 60, dtype)
+    prep = gpu_prepare(wt, masks, keep)
+    x = inputs.normal_activations(h * 5 + w, (n, cin, h, w), dtype)
+    bias = inputs.bias_vector(cout + 9, cout, dtype) if (cout % 2) else None
+    relu = bool(cin % 2)
+    xd = dev(x)
+    bd = None if bias is None else dev(bias)
+    y = torch.empty((n, cout, (h - 1) // 2 + 1, (w - 1) // 2 + 1), dtype=tdt, device="cuda")
+    note("conv stride 2 %s %s algo=%d" % (shape, np.dtype(dtype).name, algo))
+    B.conv3x3_fwd_strided(prep.layer, prep.packed, xd, y, 2, bias=bd, relu=relu, algo=algo)
+    torch.cuda.synchronize()
+    packed = prep.packed.to_host()
+    ref = oracle.conv_sparse_strided(x, packed, masks, cout, 2, bias=bias, relu=relu)
+    err = norm_err(y.cpu().numpy(), ref)
+    assert err <= TOL[dtype], "normwise error %.3e" % err
+    # stride 1 through the strided entry point is the plain conv, bit for bit
+    y1 = torch.empty((n, cout, h, w), dtype=tdt, device="cuda")
+    y1s = torch.empty_like(y1)
+    note("conv stride 1 via strided entry %s" % (shape,))
+    B.conv3x3_fwd_strided(prep.layer, prep.packed, xd, y1s, 1, bias=bd, relu=relu, algo=algo)
+    B.conv3x3_fwd(prep.layer, prep.packed, xd, y1, bias=bd, relu=relu, algo=algo)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y1s)
+
+
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
 def test_maxpool(dtype):
     torch = torch_mod()

@@ -45,11 +45,16 @@ def _check_layer(wl, li, lay, masks, x_dev, bias=None):
     torch.cuda.synchronize()
     _, _, _, packed = compare_prepared(prep, w, masks, lay.keep)
     note("%s %s conv" % (wl.name, lay.name))
-    y = B.conv(prep, x_dev, bias=None if bias is None else dev(bias), relu=lay.relu)
+    bd = None if bias is None else dev(bias)
+    if lay.stride == 1:
+        y = B.conv(prep, x_dev, bias=bd, relu=lay.relu)
+    else:
+        y = torch.empty((wl.batch, lay.cout) + lay.out_hw, dtype=x_dev.dtype, device="cuda")
+        B.conv3x3_fwd_strided(prep.layer, prep.packed, x_dev, y, lay.stride, bias=bd, relu=lay.relu)
     torch.cuda.synchronize()
     imgs = _sample(wl.batch)
     xs = x_dev[imgs].cpu().numpy()
-    ref = oracle.conv_sparse(xs, packed, masks, lay.cout, bias=bias, relu=lay.relu)
+    ref = oracle.conv_sparse_strided(xs, packed, masks, lay.cout, lay.stride, bias=bias, relu=lay.relu)
     err = norm_err(y[imgs].cpu().numpy(), ref)
     assert err <= TOL[wl.np_dtype], "%s %s: normwise error %.3e" % (wl.name, lay.name, err)
     return y
@@ -98,7 +103,7 @@ def test_workload_layers(name):
     # configuration: check the first layer of each distinct shape
     seen = set()
     for li, lay in enumerate(wl.layers):
-        key = (lay.cin, lay.cout, lay.h, lay.w, lay.keep)
+        key = (lay.cin, lay.cout, lay.h, lay.w, lay.keep, lay.stride)
         if key in seen:
             continue
         seen.add(key)
