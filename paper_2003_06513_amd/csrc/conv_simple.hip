@@ -11,13 +11,14 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
 
 namespace {
 
-// One output pixel per lane; with pool, one pooled pixel: the maximum of
+// One output pixel per lane, the batch folded into the lane index (small
+// planes still fill the blocks); with pool, one pooled pixel: the maximum of
 // the four outputs of its 2x2 window (sigma and max commute, the bias is
 // common to the window).  With stride 2 (no pool) output (oh, ow) reads the
 // input around (2 oh, 2 ow).
 template <int DT>
 __global__ __launch_bounds__(256) void k_conv_simple(const typename Elt<DT>::T* __restrict__ x, int cin,
-                                                     int H, int W, int cout, PatTable tab,
+                                                     int H, int W, int cout, int nimg, PatTable tab,
                                                      const int32_t* __restrict__ perm,
                                                      const int32_t* __restrict__ fptr,
                                                      const int32_t* __restrict__ cin_idx,
@@ -30,12 +31,14 @@ __global__ __launch_bounds__(256) void k_conv_simple(const typename Elt<DT>::T* 
     __shared__ uint16_t msk[kMaxPatterns];
     for (int p = threadIdx.x; p < tab.m; p += 256) msk[p] = tab.mask[p];
     __syncthreads();
-    const int i = blockIdx.y, n = blockIdx.z;
+    const int i = blockIdx.y;
     const int plane = H * W;
     const int OW = pool ? W / 2 : (W - 1) / stride + 1;
     const int oplane = pool ? plane / 4 : ((H - 1) / stride + 1) * OW;
-    const int pix = blockIdx.x * 256 + threadIdx.x;
-    if (pix >= oplane) return;
+    // n * oplane + pix; n * oplane < 2^31, so the unsigned index cannot wrap
+    const unsigned gid = blockIdx.x * 256u + threadIdx.x;
+    if (gid >= unsigned(nimg * oplane)) return;
+    const int n = int(gid / unsigned(oplane)), pix = int(gid - unsigned(n) * unsigned(oplane));
     const int ph = pix / OW, pw = pix - ph * OW;
     const int f = perm[i];
     const typename E::T* xn = x + int64_t(n) * cin * plane;
@@ -149,9 +152,10 @@ template <int DT>
 hipError_t conv_simple(const PatTable& tab, const PackedView& pk, const ConvArgs& a, hipStream_t s) {
     using T = typename Elt<DT>::T;
     const int outs = a.pool ? (a.h / 2) * (a.w / 2) : ((a.h - 1) / a.stride + 1) * ((a.w - 1) / a.stride + 1);
-    const dim3 grid(unsigned((outs + 255) / 256), unsigned(a.cout), unsigned(a.n));
+    const int64_t lanes = int64_t(a.n) * outs;          // at most 2^31 - 1 (y size is checked)
+    const dim3 grid(unsigned((lanes + 255) / 256), unsigned(a.cout), 1);
     hipLaunchKernelGGL(k_conv_simple<DT>, grid, dim3(256), 0, s, static_cast<const T*>(a.x), a.cin, a.h,
-                       a.w, a.cout, tab, pk.filter_perm, pk.filter_ptr, pk.cin_idx, pk.pat_id,
+                       a.w, a.cout, a.n, tab, pk.filter_perm, pk.filter_ptr, pk.cin_idx, pk.pat_id,
                        static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), a.relu, a.pool,
                        a.stride, static_cast<T*>(a.y));
     return hipGetLastError();
