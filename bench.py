@@ -54,7 +54,7 @@ def parse():
 
 
 def find_workload(name):
-    from paper_2003_06513_amd import inputs
+    from synthetic import inputs
     for wl in inputs.all_workloads():
         if wl.name == name:
             return wl
@@ -67,7 +67,7 @@ class Net:
     def __init__(self, wl, algo):
         import torch
         from paper_2003_06513_amd import binding as B
-        from paper_2003_06513_amd import inputs
+        from synthetic import inputs
         self.wl, self.algo = wl, algo
         tdt = torch.float16 if wl.dtype == "f16" else torch.float32
         self.tdt = tdt
@@ -242,7 +242,7 @@ def compare_dense(net, reps=20):
 def main():
     args = parse()
     if args.list:
-        from paper_2003_06513_amd import inputs
+        from synthetic import inputs
         for wl in inputs.all_workloads():
             print(wl.name)
         return

@@ -295,9 +295,13 @@ def maxpool2x2(x, y, stream=None):
 class Prepared:
     """A pruned, packed layer: the result of project -> select -> pack."""
 
-    def __init__(self, layer: Layer, packed: Packed, pat, energy, keep_mask):
+    def __init__(self, layer: Layer, packed: Packed, pat, energy, keep_mask, workspaces=()):
         self.layer, self.packed = layer, packed
         self.pat, self.energy, self.keep_mask = pat, energy, keep_mask
+        # the select and pack workspaces live as long as the result: the
+        # kernels that use them may still run on a stream other than torch's
+        # current one, whose allocator would otherwise hand them out again
+        self.workspaces = tuple(workspaces)
 
 
 def prepare(w, masks, keep: int, stream=None) -> Prepared:
@@ -311,10 +315,12 @@ def prepare(w, masks, keep: int, stream=None) -> Prepared:
     energy = torch.empty(K, dtype=torch.float64, device=w.device)
     keep_mask = torch.empty(K, dtype=torch.uint8, device=w.device)
     packed = Packed(layer, w.device)
+    ws_sel = workspace(layer, PSC_OP_SELECT, w.device)
+    ws_pack = workspace(layer, PSC_OP_PACK, w.device)
     project(layer, w, pat, energy, stream)
-    select(layer, energy, keep_mask, workspace(layer, PSC_OP_SELECT, w.device), stream)
-    pack(layer, w, pat, keep_mask, packed, workspace(layer, PSC_OP_PACK, w.device), stream)
-    return Prepared(layer, packed, pat, energy, keep_mask)
+    select(layer, energy, keep_mask, ws_sel, stream)
+    pack(layer, w, pat, keep_mask, packed, ws_pack, stream)
+    return Prepared(layer, packed, pat, energy, keep_mask, (ws_sel, ws_pack))
 
 
 def conv(prep: Prepared, x, bias=None, relu: bool = False, algo: int = 0, out=None, stream=None):

@@ -1,7 +1,8 @@
 """Build libpsc.so in-tree with hipcc for gfx950.
 
 Every .hip / .cpp file under csrc/ is compiled to an object under _build/
-and linked into paper_2003_06513_amd/libpsc.so.  Run as a module
+(in parallel: the tuned conv kernels are split over several translation
+units) and linked into paper_2003_06513_amd/libpsc.so.  Run as a module
 (``python -m paper_2003_06513_amd.build``) or call ``build()``.
 """
 from __future__ import annotations
@@ -26,8 +27,16 @@ COMMON = ["--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17",
           "-I", os.path.join(ROOT, "include"), "-Wall", "-Wno-unused-function"]
 
 
-def _compile(src: str) -> str:
+def _headers():
+    return glob.glob(os.path.join(CSRC, "*.h")) + glob.glob(os.path.join(ROOT, "include", "*.h"))
+
+
+def _compile(src: str, incremental: bool = False) -> str:
     obj = os.path.join(OUT_DIR, os.path.basename(src) + ".o")
+    if incremental and os.path.exists(obj):
+        newest = max(os.path.getmtime(f) for f in [src] + _headers())
+        if os.path.getmtime(obj) >= newest:
+            return obj
     cmd = [HIPCC, "-c", src, "-o", obj] + COMMON
     if src.endswith(".cpp"):
         cmd = [HIPCC, "-x", "hip", "-c", src, "-o", obj] + COMMON
@@ -41,11 +50,15 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, incremental: bool = False) -> str:
+    """Compile every source (``incremental``: only those newer than their
+    object, counting the headers) and link libpsc.so."""
     os.makedirs(OUT_DIR, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
+    # the largest translation units first, so the pool finishes early
+    srcs.sort(key=lambda f: -os.path.getsize(f) - (1 << 20) * f.endswith("_r8.hip"))
     with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        objs = list(ex.map(_compile, srcs))
+        objs = list(ex.map(lambda s: _compile(s, incremental), srcs))
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=" + ARCH, "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -58,4 +71,4 @@ def build(verbose: bool = False) -> str:
 
 
 if __name__ == "__main__":
-    build(verbose=True)
+    build(verbose=True, incremental="--incremental" in sys.argv)

@@ -1,0 +1,9 @@
+// Instantiation of the tuned conv kernels for fp16 storage, 4 rows per lane
+// (direct, staged and multi-run staged forms).
+#include "conv_stream.h"
+
+namespace psc {
+namespace cs {
+template hipError_t launch_r<DT_F16, 4>(const PackedView&, const ConvArgs&, const Geo&, hipStream_t);
+}  // namespace cs
+}  // namespace psc

@@ -1,0 +1,182 @@
+// Launch configuration of the tuned pattern-sparse 3x3 convolution (Sec. 4.1
+// Eq. 1): lane layout, rows per lane, filter shares and load form are chosen
+// here on the host; the kernels are the templates of conv_stream.h, each
+// instantiation set compiled in its own translation unit (conv_stream_*.hip).
+#include <cstring>
+
+#include "conv_stream.h"
+
+namespace psc {
+using namespace cs;
+
+#define PSC_EXTERN_R(DT, R) \
+    extern template hipError_t cs::launch_r<DT, R>(const PackedView&, const ConvArgs&, const Geo&, hipStream_t);
+PSC_EXTERN_R(DT_F32, 2)
+PSC_EXTERN_R(DT_F32, 4)
+PSC_EXTERN_R(DT_F32, 7)
+PSC_EXTERN_R(DT_F32, 8)
+PSC_EXTERN_R(DT_F16, 2)
+PSC_EXTERN_R(DT_F16, 4)
+PSC_EXTERN_R(DT_F16, 7)
+PSC_EXTERN_R(DT_F16, 8)
+#undef PSC_EXTERN_R
+extern template hipError_t cs::launch_wide<2>(const PackedView&, const ConvArgs&, const Geo&, hipStream_t);
+
+// Launch configuration.  Rows per lane R minimise the lane-rows issued
+// (ceil(units / S) * R, larger R on ties; even R when pooling; R = 8 only
+// with one segment per wave); a workgroup holds 4 filters, or
+// fewer filters split into KS shares (KS doubles up to 8) while the grid
+// holds under 4 waves per SIMD.  Returns hipErrorNotSupported when x exceeds
+// the 2 GiB a buffer descriptor addresses here.
+hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const ConvArgs& a,
+                              hipStream_t stream) {
+    const int64_t x_bytes = int64_t(a.n) * a.cin * a.h * a.w * (a.dtype == DT_F16 ? 2 : 4);
+    // buffer descriptors address at most 2 GiB (x) and the packed weights
+    if (x_bytes > (int64_t(1) << 31) || a.keep * 4 * (a.dtype == DT_F16 ? 2 : 4) > 0x7fffffff)
+        return hipErrorNotSupported;
+    Geo g;
+    std::memset(&g, 0, sizeof g);
+    g.n = a.n;
+    g.cin = a.cin;
+    g.H = a.h;
+    g.W = a.w;
+    g.cout = a.cout;
+    g.m = tab.m;
+    g.relu = a.relu;
+    g.x_bytes = int(x_bytes > 0x7fffffff ? 0x7fffffff : x_bytes);
+    g.keep = int(a.keep);
+    g.pool = a.pool;
+    for (int p = 0; p < kMaxPatterns; ++p) {
+        g.shape[p] = -1;
+        g.mask[p] = p < tab.m ? tab.mask[p] : 0;
+        if (p < tab.m)
+            for (int t = 0; t < 56; ++t)
+                if (kCentre3.code[t] == tab.mask[p]) g.shape[p] = int8_t(t);
+    }
+    // wide form: fp32 rows of 64..252 columns starting on 64-byte boundaries
+    // (width a multiple of 16): 4 columns per lane, full-row segments padded
+    // to a multiple of 4 lanes
+    if (a.dtype == DT_F32 && a.w % 16 == 0 && a.w >= 64 && a.w / 4 + 1 <= 64) {
+        g.cols_mode = 0;
+        g.seg_len = (a.w / 4 + 1 + 3) / 4 * 4;
+        g.S = 64 / g.seg_len;
+        g.Wt = a.w;
+        g.CT = 1;
+        // two rows per lane: 4(R+2) row values a kernel, twice for the
+        // prefetch, keep the wave near 80 VGPRs (6 waves per SIMD)
+        constexpr int R = 2;
+        g.RB = (a.h + R - 1) / R;
+        g.U = a.n * g.RB;
+        const int sgroups = (g.U + g.S - 1) / g.S;
+        g.KS = 1;
+        while (g.KS < kMaxSplit && int64_t(sgroups) * a.cout * g.KS < 4096 && a.cin >= 16 * g.KS) g.KS *= 2;
+        g.FW = g.KS >= 4 ? 1 : 4 / g.KS;
+        if (g.FW > a.cout) g.FW = a.cout;
+        g.groups_x = (a.cout + g.FW - 1) / g.FW;
+        g.nblocks = g.groups_x * sgroups;
+        return launch_wide<R>(pk, a, g, stream);
+    }
+    // lane layout: full-row segments if they use the lanes at least as well
+    // as haloed column tiles
+    const int S_rows = a.w <= 63 ? 65 / (a.w + 1) : 0;
+    const int use_rows = S_rows * a.w;
+    int ct = (a.w + 61) / 62, use_cols = 0;
+    for (int t = ct; t <= a.w && t <= 64; ++t) {
+        const int wt = (a.w + t - 1) / t;
+        const int use = (64 / (wt + 2)) * a.w / t;
+        if (use > use_cols) {
+            use_cols = use;
+            ct = t;
+        }
+    }
+    if (S_rows > 0 && use_rows >= use_cols) {
+        g.cols_mode = 0;
+        g.S = S_rows;
+        g.seg_len = a.w + 1;
+        g.Wt = a.w;
+        g.CT = 1;
+    } else {
+        if (a.pool) return hipErrorNotSupported;   // pooling needs full-row segments
+        const int Wt = (a.w + ct - 1) / ct;
+        g.cols_mode = 1;
+        g.S = 64 / (Wt + 2);
+        g.seg_len = Wt + 2;
+        g.Wt = Wt;
+        g.CT = ct;
+    }
+    // rows per lane
+    const int cand[4] = {8, 7, 4, 2};
+    int R = 8;
+    int64_t best = -1;
+    // 8 rows per lane only with one segment per wave (several segments at
+    // R = 8 are kept off: see the note on the launch configuration)
+    for (int rr : cand) {
+        if (a.pool && (rr & 1)) continue;               // pooled rows pair up inside a lane
+        if (rr == 8 && g.S > 1) continue;
+        const int64_t units = int64_t(a.n) * ((a.h + rr - 1) / rr) * g.CT;
+        const int64_t cost = (units + g.S - 1) / g.S * rr;
+        if (best < 0 || cost < best) {
+            best = cost;
+            R = rr;
+        }
+    }
+    g.RB = (a.h + R - 1) / R;
+    g.U = a.n * g.RB * g.CT;
+    const int sgroups = (g.U + g.S - 1) / g.S;
+    g.KS = 1;
+    while (g.KS < kMaxSplit && int64_t(sgroups) * a.cout * g.KS < 4096 && a.cin >= 16 * g.KS) g.KS *= 2;
+    g.FW = g.KS >= 4 ? 1 : 4 / g.KS;
+    if (g.FW > a.cout) g.FW = a.cout;
+    const int fgroups = (a.cout + g.FW - 1) / g.FW;
+    g.groups_x = fgroups;
+    g.nblocks = fgroups * sgroups;
+    // LDS staging for full-row segments: runs per wave (images its segments
+    // touch) and the LDS bytes of the largest run
+    if (!g.cols_mode) {
+        const int esz = a.dtype == DT_F16 ? 2 : 4;
+        int nruns_max = 0, bytes_max = 0;
+        for (int sg = 0; sg < sgroups; ++sg) {
+            const int uf = sg * g.S, ul = (uf + g.S < g.U ? uf + g.S : g.U) - 1;
+            const int nf = uf / g.RB, nl = ul / g.RB;
+            nruns_max = nruns_max > nl - nf + 1 ? nruns_max : nl - nf + 1;
+            for (int n = nf; n <= nl; ++n) {
+                const int ua = uf > n * g.RB ? uf : n * g.RB;
+                const int ub = ul < n * g.RB + g.RB - 1 ? ul : n * g.RB + g.RB - 1;
+                int lo = (ua - n * g.RB) * R - 1, hi = (ub - n * g.RB + 1) * R + 1;
+                lo = lo < 0 ? 0 : lo;
+                hi = hi > a.h ? a.h : hi;
+                const int bytes = (hi - lo) * a.w * esz;
+                bytes_max = bytes_max > bytes ? bytes_max : bytes;
+            }
+        }
+        // a run's copy spans [data - 63, data + bytes + 1024) around its data
+        g.region = (64 + bytes_max + 1024 + 63) / 64 * 64;
+        // copy 0: the runs, then 64 zero bytes; copy 1 kLdsCopy bytes later
+        g.wave_bytes = kLdsCopy + nruns_max * g.region + 64;
+        // fp16 copies shift the LDS destination in 4-byte steps only: rows of
+        // even width keep every offset a multiple of 4 bytes
+        const bool fits = (bytes_max + 63 + 1023) / 1024 <= kMaxDma && nruns_max <= kMaxRuns &&
+                          nruns_max * g.region + 64 <= kLdsCopy &&
+                          int64_t(g.FW) * g.KS * g.wave_bytes <= 64 * 1024 &&
+                          (a.dtype != DT_F16 || a.w % 2 == 0);
+        // one full-row segment per wave and a grid of about one round of
+        // waves (batch 1 at W >= 32) is bound by the per-kernel latency,
+        // which the direct loads keep shorter
+        const int64_t waves = int64_t(g.nblocks) * g.FW * g.KS;
+        const bool throughput = g.S >= 2 || waves >= 2 * 6 * 1024;
+        g.lds = fits && throughput ? 1 : 0;
+        if (g.lds && nruns_max > 1) g.lds = 2;             // several runs per wave: the general form
+    }
+    switch (R) {
+        case 8: return a.dtype == DT_F16 ? launch_r<DT_F16, 8>(pk, a, g, stream)
+                                         : launch_r<DT_F32, 8>(pk, a, g, stream);
+        case 7: return a.dtype == DT_F16 ? launch_r<DT_F16, 7>(pk, a, g, stream)
+                                         : launch_r<DT_F32, 7>(pk, a, g, stream);
+        case 4: return a.dtype == DT_F16 ? launch_r<DT_F16, 4>(pk, a, g, stream)
+                                         : launch_r<DT_F32, 4>(pk, a, g, stream);
+        default: return a.dtype == DT_F16 ? launch_r<DT_F16, 2>(pk, a, g, stream)
+                                          : launch_r<DT_F32, 2>(pk, a, g, stream);
+    }
+}
+
+}  // namespace psc

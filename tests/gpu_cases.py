@@ -6,7 +6,7 @@ import numpy as np
 
 import oracle
 from paper_2003_06513_amd import binding as B
-from paper_2003_06513_amd import inputs
+from synthetic import inputs
 
 NP2TORCH = {np.float32: "float32", np.float16: "float16"}
 TOL = {np.float32: 1e-4, np.float16: 1e-2}

@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 from paper_2003_06513_amd import binding as B
-from paper_2003_06513_amd import inputs
+from synthetic import inputs
 
 FAKE = ctypes.c_void_p(0x10000)      # never dereferenced: every call below fails validation
 

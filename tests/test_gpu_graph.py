@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 from paper_2003_06513_amd import binding as B
-from paper_2003_06513_amd import inputs
+from synthetic import inputs
 from gpu_cases import dev, note, torch_mod
 
 pytestmark = pytest.mark.gpu

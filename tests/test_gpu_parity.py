@@ -7,7 +7,7 @@ import pytest
 
 import oracle
 from paper_2003_06513_amd import binding as B
-from paper_2003_06513_amd import inputs
+from synthetic import inputs
 from gpu_cases import (TOL, check_conv, compare_prepared, dev, gpu_prepare, host_prepare, norm_err,
                        note, torch_mod)
 

@@ -16,7 +16,7 @@ import pytest
 
 import oracle
 from paper_2003_06513_amd import binding as B
-from paper_2003_06513_amd import inputs
+from synthetic import inputs
 from gpu_cases import TOL, compare_prepared, dev, note, norm_err, torch_mod
 
 pytestmark = pytest.mark.gpu

@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 
 import oracle
-from paper_2003_06513_amd import inputs
+from synthetic import inputs
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_examples.json")
 CENTRE3 = [c for c in range(512) if (c >> 4) & 1 and bin(c).count("1") == 4]
