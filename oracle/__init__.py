@@ -15,6 +15,8 @@ Mobile Acceleration Framework" (GLSVLSI'20), that it implements:
   pack / unpack   Sec. 3.4   filter kernel reorder + compressed weight storage
   mask_weights    Sec. 3.2   M o W with dropped kernels zeroed
   conv_sparse     Sec. 4.1   Eq. 1 layer, 3x3 stride 1 pad 1, from the storage
+  conv_sparse_strided        the same layer with stride 2 (ResNet stage entries)
+  conv_sparse_f32acc         the same loop in fp32 (timed CPU baseline only)
   conv_dense      Sec. 4.1   the same layer as a textbook dense loop (witness)
   maxpool2x2                 2x2/2 max-pool between the VGG-16 layers
 
@@ -32,29 +34,32 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "pso.c")
 _LIB_PATH = os.path.join(_HERE, "libpso.so")
+_BENCH_PATH = os.path.join(_HERE, "libpso_bench.so")
 _lib = None
+_bench_lib = None
 
 F32, F16 = 0, 1
 
 
+def _compile(out: str, flags) -> None:
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = ["gcc"] + list(flags) + ["-std=c99", "-fopenmp", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, out)
+
+
 def build(force: bool = True) -> str:
-    """Compile pso.c into oracle/libpso.so (gcc, OpenMP, no fast-math)."""
+    """Compile pso.c into oracle/libpso.so (gcc, OpenMP, no fast-math, no
+    contraction: every add and multiply rounds as written) and, for the
+    timed CPU baseline only, into oracle/libpso_bench.so (-O3 -march=native)."""
     if force or not os.path.exists(_LIB_PATH):
-        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
-        cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-ffp-contract=off",
-               "-fno-fast-math", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"]
-        subprocess.run(cmd, check=True)
-        os.replace(tmp, _LIB_PATH)
+        _compile(_LIB_PATH, ["-O3", "-ffp-contract=off", "-fno-fast-math"])
+    if force or not os.path.exists(_BENCH_PATH):
+        _compile(_BENCH_PATH, ["-O3", "-march=native"])
     return _LIB_PATH
 
 
-def _load():
-    global _lib
-    if _lib is not None:
-        return _lib
-    if not os.path.exists(_LIB_PATH):
-        build(force=True)
-    lib = ctypes.CDLL(_LIB_PATH)
+def _declare(lib):
     P = ctypes.c_void_p
     i32, i64 = ctypes.c_int32, ctypes.c_int64
     lib.pso_num_threads.restype = ctypes.c_int
@@ -64,18 +69,37 @@ def _load():
     lib.pso_pack.argtypes = [P, i32, i32, i32, i32, P, P, P, P, P, P, P, P, P]
     lib.pso_mask_weights.argtypes = [P, i32, i64, P, i32, P, P, P]
     lib.pso_unpack.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P, P]
-    lib.pso_conv_sparse.argtypes = [P, i32, i32, i32, i32, i32, i32, i32, P,
-                                    P, P, P, P, P, P, i32, P, P]
-    lib.pso_conv_sparse_strided.argtypes = [P, i32, i32, i32, i32, i32, i32, i32, P,
-                                            P, P, P, P, P, P, i32, i32, P]
+    lib.pso_conv_sparse_st.argtypes = [P, i32, i32, i32, i32, i32, i32, P,
+                                       P, P, P, P, P, i32, P, i32, i32, P, P]
+    lib.pso_conv_sparse_f32acc.argtypes = [P, i32, i32, i32, i32, i32, i32, P,
+                                           P, P, P, P, P, i32, P, i32, i32, P]
     lib.pso_conv_dense.argtypes = [P, i32, i32, i32, i32, i32, P, i32, P, i32, P]
     lib.pso_maxpool2x2.argtypes = [P, i64, i32, i32, P]
     for name in ("pso_select_library", "pso_project", "pso_select", "pso_pack",
-                 "pso_mask_weights", "pso_unpack", "pso_conv_sparse",
-                 "pso_conv_sparse_strided", "pso_conv_dense", "pso_maxpool2x2"):
+                 "pso_mask_weights", "pso_unpack", "pso_conv_sparse_st",
+                 "pso_conv_sparse_f32acc", "pso_conv_dense", "pso_maxpool2x2"):
         getattr(lib, name).restype = ctypes.c_int
-    _lib = lib
     return lib
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        build(force=True)
+    _lib = _declare(ctypes.CDLL(_LIB_PATH))
+    return _lib
+
+
+def _load_bench():
+    global _bench_lib
+    if _bench_lib is not None:
+        return _bench_lib
+    if not os.path.exists(_BENCH_PATH):
+        build(force=True)
+    _bench_lib = _declare(ctypes.CDLL(_BENCH_PATH))
+    return _bench_lib
 
 
 def _ptr(a):
@@ -187,53 +211,66 @@ def unpack(packed: dict, masks, cout: int, cin: int) -> np.ndarray:
     return out
 
 
-def conv_sparse(x: np.ndarray, packed: dict, masks, cout: int, bias=None,
-                relu: bool = False, want_scale: bool = False):
-    """Sec. 4.1 Eq. 1 with the compressed storage: fp64 NCHW output
-    (and, with ``want_scale``, the per-output sum of |v*x| plus |b|)."""
+def _conv_args(x, packed, masks):
     x = np.ascontiguousarray(x)
-    n, cin, h, w = (int(d) for d in x.shape)
     masks = np.ascontiguousarray(masks, dtype=np.uint16)
     vals = np.ascontiguousarray(packed["values"])
     if vals.size and vals.dtype != x.dtype:
         raise TypeError("weights and activations must share a dtype")
-    if bias is not None:
-        bias = np.ascontiguousarray(bias, dtype=x.dtype)
-    y = np.zeros((n, cout, h, w), dtype=np.float64)
-    s = np.zeros_like(y) if want_scale else None
-    _check(_load().pso_conv_sparse(
-        _ptr(x), _dtype_code(x), n, cin, h, w, cout, len(masks), _ptr(masks),
-        _ptr(np.ascontiguousarray(packed["filter_perm"], dtype=np.int32)),
-        _ptr(np.ascontiguousarray(packed["filter_ptr"], dtype=np.int32)),
-        _ptr(np.ascontiguousarray(packed["cin_idx"], dtype=np.int32)),
-        _ptr(np.ascontiguousarray(packed["pat_id"], dtype=np.uint8)),
-        _ptr(vals), _ptr(bias), int(bool(relu)), _ptr(y), _ptr(s)),
-        "conv_sparse")
-    return (y, s) if want_scale else y
+    idx = [np.ascontiguousarray(packed["filter_perm"], dtype=np.int32),
+           np.ascontiguousarray(packed["filter_ptr"], dtype=np.int32),
+           np.ascontiguousarray(packed["cin_idx"], dtype=np.int32),
+           np.ascontiguousarray(packed["pat_id"], dtype=np.uint8)]
+    vcode = _dtype_code(vals) if vals.size else F32
+    return x, masks, vals, vcode, idx
 
 
 def conv_sparse_strided(x: np.ndarray, packed: dict, masks, cout: int, stride: int, bias=None,
-                        relu: bool = False):
-    """Sec. 4.1 Eq. 1 with a stride (1 or 2; zero padding 1), from the
-    compressed storage: fp64 output [n][cout][(h-1)//stride+1][(w-1)//stride+1]."""
-    x = np.ascontiguousarray(x)
+                        relu: bool = False, want_scale: bool = False):
+    """Sec. 4.1 Eq. 1 with the compressed storage, stride 1 or 2, zero
+    padding 1: fp64 output [n][cout][(h-1)//stride+1][(w-1)//stride+1] (and,
+    with ``want_scale``, the per-output sum of |v*x| plus |b|).  fp32 and
+    fp16 activations and bias are widened to fp64 (exactly) before the call."""
+    x, masks, vals, vcode, idx = _conv_args(x, packed, masks)
     n, cin, h, w = (int(d) for d in x.shape)
-    masks = np.ascontiguousarray(masks, dtype=np.uint16)
-    vals = np.ascontiguousarray(packed["values"])
-    if vals.size and vals.dtype != x.dtype:
-        raise TypeError("weights and activations must share a dtype")
-    if bias is not None:
-        bias = np.ascontiguousarray(bias, dtype=x.dtype)
+    x64 = np.ascontiguousarray(x, dtype=np.float64)
+    b64 = None if bias is None else np.ascontiguousarray(np.asarray(bias, dtype=x.dtype), dtype=np.float64)
     y = np.zeros((n, cout, (h - 1) // stride + 1, (w - 1) // stride + 1), dtype=np.float64)
-    _check(_load().pso_conv_sparse_strided(
-        _ptr(x), _dtype_code(x), n, cin, h, w, cout, len(masks), _ptr(masks),
-        _ptr(np.ascontiguousarray(packed["filter_perm"], dtype=np.int32)),
-        _ptr(np.ascontiguousarray(packed["filter_ptr"], dtype=np.int32)),
-        _ptr(np.ascontiguousarray(packed["cin_idx"], dtype=np.int32)),
-        _ptr(np.ascontiguousarray(packed["pat_id"], dtype=np.uint8)),
-        _ptr(vals), _ptr(bias), int(bool(relu)), int(stride), _ptr(y)),
-        "conv_sparse_strided")
+    s = np.zeros_like(y) if want_scale else None
+    _check(_load().pso_conv_sparse_st(
+        _ptr(x64), n, cin, h, w, cout, len(masks), _ptr(masks), _ptr(idx[0]), _ptr(idx[1]),
+        _ptr(idx[2]), _ptr(idx[3]), _ptr(vals), vcode, _ptr(b64), int(bool(relu)), int(stride),
+        _ptr(y), _ptr(s)), "conv_sparse")
+    return (y, s) if want_scale else y
+
+
+def conv_sparse(x: np.ndarray, packed: dict, masks, cout: int, bias=None,
+                relu: bool = False, want_scale: bool = False):
+    """Sec. 4.1 Eq. 1 with the compressed storage, stride 1, zero padding 1:
+    fp64 NCHW output (and, with ``want_scale``, the per-output sum of |v*x|
+    plus |b|)."""
+    return conv_sparse_strided(x, packed, masks, cout, 1, bias=bias, relu=relu, want_scale=want_scale)
+
+
+def conv_sparse_f32acc(x: np.ndarray, packed: dict, masks, cout: int, stride: int = 1, bias=None,
+                       relu: bool = False) -> np.ndarray:
+    """The same loop accumulating in fp32 (-O3 -march=native build): the CPU
+    baseline the benchmark times, never a parity reference.  Activations
+    are taken as fp32 (fp16 widened before the call)."""
+    x, masks, vals, vcode, idx = _conv_args(x, packed, masks)
+    n, cin, h, w = (int(d) for d in x.shape)
+    x32 = np.ascontiguousarray(x, dtype=np.float32)
+    b32 = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+    y = np.zeros((n, cout, (h - 1) // stride + 1, (w - 1) // stride + 1), dtype=np.float32)
+    _check(_load_bench().pso_conv_sparse_f32acc(
+        _ptr(x32), n, cin, h, w, cout, len(masks), _ptr(masks), _ptr(idx[0]), _ptr(idx[1]),
+        _ptr(idx[2]), _ptr(idx[3]), _ptr(vals), vcode, _ptr(b32), int(bool(relu)), int(stride),
+        _ptr(y)), "conv_sparse_f32acc")
     return y
+
+
+def bench_num_threads() -> int:
+    return int(_load_bench().pso_num_threads())
 
 
 def conv_dense(x: np.ndarray, wdense: np.ndarray, bias=None, relu: bool = False):

@@ -16,10 +16,12 @@
  *                       weight storage                       (Sec. 3.4)
  *   pso_mask_weights    M o W with dropped kernels zeroed    (Sec. 3.2)
  *   pso_unpack          compressed storage -> dense OIHW     (Sec. 3.4)
- *   pso_conv_sparse     X_n = sigma(W_n X_{n-1} + b_n) from
- *                       the compressed storage               (Sec. 4.1, Eq. 1)
- *   pso_conv_sparse_strided  the same layer with stride 1 or 2
- *                       (stage-entry convs of the pruned ResNets)
+ *   pso_conv_sparse_st  X_n = sigma(W_n X_{n-1} + b_n) from
+ *                       the compressed storage, stride 1 or 2
+ *                       (stride 2: stage-entry convs of the
+ *                       pruned ResNets)                      (Sec. 4.1, Eq. 1)
+ *   pso_conv_sparse_f32acc  the same loop accumulating in fp32
+ *                       (timed CPU baseline only)
  *   pso_conv_dense      textbook dense direct convolution of
  *                       zero-masked OIHW weights (witness)   (Sec. 4.1, Eq. 1)
  *   pso_maxpool2x2      2x2/2 max-pool between VGG-16 layers
@@ -53,6 +55,7 @@
 
 #define PSO_F32 0
 #define PSO_F16 1
+#define PSO_F64 2   /* activations widened to double before the call */
 
 /* IEEE 754 binary16 -> double, from the format's definition (exact). */
 static double half_bits_to_double(uint16_t h)
@@ -74,10 +77,12 @@ static double elem(const void *p, int dtype, size_t i)
 {
     if (dtype == PSO_F16)
         return half_bits_to_double(((const uint16_t *)p)[i]);
+    if (dtype == PSO_F64)
+        return ((const double *)p)[i];
     return (double)((const float *)p)[i];
 }
 
-static size_t elem_size(int dtype) { return dtype == PSO_F16 ? 2 : 4; }
+static size_t elem_size(int dtype) { return dtype == PSO_F16 ? 2 : (dtype == PSO_F64 ? 8 : 4); }
 
 static int popcount9(unsigned v)
 {
@@ -370,89 +375,58 @@ int pso_unpack(int dtype, int cout, int cin, int m, const uint16_t *masks,
 
 /* ------------------------------------------------------------------------ */
 /* Sec. 4.1, Eq. 1: a layer computes X_n = sigma(W_n X_{n-1} + b_n).  For a
- * 3x3 convolution, stride 1, zero padding 1, read from the compressed
- * storage: y[n,f,h,w] = sigma(b[f] + sum over the kept kernels (ci, p) of f
- * of sum_j v_j * x[n, ci, h + r_j - 1, w + s_j - 1]), where (r_j, s_j) is
- * the j-th set position of pattern p in ascending 3r+s order.
+ * 3x3 convolution with zero padding 1, read from the compressed storage:
+ *   y[n,f,i,j] = sigma(b[f] + sum over the kept kernels (ci, p) of f of
+ *                sum_t v_t * x[n, ci, st*i + r_t - 1, st*j + s_t - 1]),
+ * where (r_t, s_t) is the t-th set position of pattern p in ascending 3r+s
+ * order, st the stride (1, or 2 for the stage-entry convolutions of the
+ * ResNets the paper prunes) and taps outside the image read zero.  The
+ * output is [n][cout][OH][OW], OH = (h-1)/st + 1, OW = (w-1)/st + 1.
  *
- * y (and s, if non-null) are [n][cout][h][w] doubles.  s receives the sum of
- * |v*x| over the same terms plus |b|, used to scale element-wise errors. */
-int pso_conv_sparse(const void *x, int dtype, int n, int cin, int h, int w,
-                    int cout, int m, const uint16_t *masks,
-                    const int32_t *filter_perm, const int32_t *filter_ptr,
-                    const int32_t *cin_idx, const uint8_t *pat_id,
-                    const void *values, const void *bias, int relu,
-                    double *y, double *s)
+ * Every output starts at +0 and receives its products in storage order
+ * (kernels in order, the 4 taps in ascending position), then the bias; each
+ * tap is applied to the rows and columns whose input lies inside the image
+ * (the range is computed instead of testing every pixel; the adds are the
+ * same).  x is double [n][cin][h][w] (fp32 and fp16 activations widen to
+ * double exactly); values are in vdtype; bias is double [cout] or NULL.
+ * If s is non-null it receives the sum of |v*x| over the same terms plus |b|,
+ * the scale of an element-wise rounding-error bound. */
+static void out_range(int st, int off, int in_size, int out_size, int *lo, int *hi)
 {
-    if (n < 0 || cin < 0 || h < 0 || w < 0 || cout < 0 || m < 1 || m > 126)
-        return -1;
-    size_t plane = (size_t)h * w;
-    int bad = 0;
-#pragma omp parallel for schedule(dynamic, 1)
-    for (int64_t t = 0; t < (int64_t)n * cout; ++t) {
-        int nn = (int)(t / cout);
-        int i = (int)(t % cout);
-        int f = filter_perm[i];
-        double *yp = y + ((size_t)nn * cout + f) * plane;
-        double *sp = s ? s + ((size_t)nn * cout + f) * plane : NULL;
-        for (size_t q = 0; q < plane; ++q) {
-            yp[q] = 0.0;
-            if (sp)
-                sp[q] = 0.0;
-        }
-        for (int32_t k = filter_ptr[i]; k < filter_ptr[i + 1]; ++k) {
-            int ci = cin_idx[k];
-            int p = pat_id[k];
-            if (p >= m || ci < 0 || ci >= cin) {
-                bad = 1;
-                continue;
-            }
-            const size_t xoff = ((size_t)nn * cin + ci) * plane;
-            int j = 0;
-            for (int q = 0; q < 9; ++q) {
-                if (!((masks[p] >> q) & 1))
-                    continue;
-                int r = q / 3, c = q % 3;
-                double v = elem(values, dtype, (size_t)k * 4 + j);
-                j += 1;
-                for (int oh = 0; oh < h; ++oh) {
-                    int ih = oh + r - 1;
-                    if (ih < 0 || ih >= h)
-                        continue;
-                    for (int ow = 0; ow < w; ++ow) {
-                        int iw = ow + c - 1;
-                        if (iw < 0 || iw >= w)
-                            continue;
-                        double prod = v * elem(x, dtype, xoff + (size_t)ih * w + iw);
-                        yp[(size_t)oh * w + ow] += prod;
-                        if (sp)
-                            sp[(size_t)oh * w + ow] += fabs(prod);
-                    }
-                }
-            }
-        }
-        double b = bias ? elem(bias, dtype, (size_t)f) : 0.0;
-        for (size_t q = 0; q < plane; ++q) {
-            double v = yp[q] + b;
-            yp[q] = (relu && v < 0.0) ? 0.0 : v;
-            if (sp)
-                sp[q] += fabs(b);
-        }
-    }
-    return bad ? -1 : 0;
+    /* outputs o in [0, out_size) with 0 <= st*o + off - 1 < in_size */
+    int a = 0, b = out_size;
+    while (a < b && st * a + off - 1 < 0)
+        ++a;
+    while (b > a && st * (b - 1) + off - 1 >= in_size)
+        --b;
+    *lo = a;
+    *hi = b;
 }
 
-/* The same layer with a stride (the stage-entry convolutions of the ResNets
- * the paper prunes): 3x3, zero padding 1, stride st in {1, 2}.  Output
- * position (oh, ow) reads input (st*oh + r - 1, st*ow + s - 1); the output is
- * [n][cout][OH][OW] with OH = (h - 1) / st + 1, OW = (w - 1) / st + 1.  y is
- * written in full; the loop order is the plain one, per output pixel. */
-int pso_conv_sparse_strided(const void *x, int dtype, int n, int cin, int h, int w,
-                            int cout, int m, const uint16_t *masks,
-                            const int32_t *filter_perm, const int32_t *filter_ptr,
-                            const int32_t *cin_idx, const uint8_t *pat_id,
-                            const void *values, const void *bias, int relu,
-                            int st, double *y)
+/* One output row of one tap: y[o] += v * x[st*o], and s[o] += |v * x[st*o]|
+ * when s is non-null, for o in [o0, o1).  st is a compile-time 1 or 2 at
+ * each call, so the unit-stride loop vectorises. */
+static inline void tap_row(double *restrict y, double *restrict s, const double *restrict x,
+                           const int st, double v, int o0, int o1)
+{
+    if (s) {
+        for (int o = o0; o < o1; ++o) {
+            double prod = v * x[(size_t)st * o];
+            y[o] += prod;
+            s[o] += fabs(prod);
+        }
+    } else {
+        for (int o = o0; o < o1; ++o)
+            y[o] += v * x[(size_t)st * o];
+    }
+}
+
+int pso_conv_sparse_st(const double *x, int n, int cin, int h, int w,
+                       int cout, int m, const uint16_t *masks,
+                       const int32_t *filter_perm, const int32_t *filter_ptr,
+                       const int32_t *cin_idx, const uint8_t *pat_id,
+                       const void *values, int vdtype, const double *bias, int relu,
+                       int st, double *y, double *s)
 {
     if (n < 0 || cin < 0 || h < 1 || w < 1 || cout < 0 || m < 1 || m > 126 || st < 1 || st > 2)
         return -1;
@@ -464,32 +438,105 @@ int pso_conv_sparse_strided(const void *x, int dtype, int n, int cin, int h, int
         int nn = (int)(t / cout);
         int i = (int)(t % cout);
         int f = filter_perm[i];
-        double b = bias ? elem(bias, dtype, (size_t)f) : 0.0;
-        for (int oh = 0; oh < OH; ++oh) {
-            for (int ow = 0; ow < OW; ++ow) {
-                double acc = 0.0;
-                for (int32_t k = filter_ptr[i]; k < filter_ptr[i + 1]; ++k) {
-                    int ci = cin_idx[k];
-                    int p = pat_id[k];
-                    if (p >= m || ci < 0 || ci >= cin) {
-                        bad = 1;
-                        continue;
-                    }
-                    int j = 0;
-                    for (int q = 0; q < 9; ++q) {
-                        if (!((masks[p] >> q) & 1))
-                            continue;
-                        double v = elem(values, dtype, (size_t)k * 4 + j);
-                        j += 1;
-                        int ih = st * oh + q / 3 - 1, iw = st * ow + q % 3 - 1;
-                        if (ih < 0 || ih >= h || iw < 0 || iw >= w)
-                            continue;
-                        acc += v * elem(x, dtype, ((size_t)nn * cin + ci) * plane + (size_t)ih * w + iw);
-                    }
-                }
-                double v = acc + b;
-                y[((size_t)nn * cout + f) * oplane + (size_t)oh * OW + ow] = (relu && v < 0.0) ? 0.0 : v;
+        double *yp = y + ((size_t)nn * cout + f) * oplane;
+        double *sp = s ? s + ((size_t)nn * cout + f) * oplane : NULL;
+        for (size_t q = 0; q < oplane; ++q) {
+            yp[q] = 0.0;
+            if (sp)
+                sp[q] = 0.0;
+        }
+        for (int32_t k = filter_ptr[i]; k < filter_ptr[i + 1]; ++k) {
+            int ci = cin_idx[k];
+            int p = pat_id[k];
+            if (p >= m || ci < 0 || ci >= cin) {
+                bad = 1;
+                continue;
             }
+            const double *xc = x + ((size_t)nn * cin + ci) * plane;
+            int j = 0;
+            for (int q = 0; q < 9; ++q) {
+                if (!((masks[p] >> q) & 1))
+                    continue;
+                int r = q / 3, c = q % 3;
+                double v = elem(values, vdtype, (size_t)k * 4 + j);
+                j += 1;
+                int oh0, oh1, ow0, ow1;
+                out_range(st, r, h, OH, &oh0, &oh1);
+                out_range(st, c, w, OW, &ow0, &ow1);
+                for (int oh = oh0; oh < oh1; ++oh) {
+                    const double *xr = xc + (size_t)(st * oh + r - 1) * w + (c - 1);
+                    double *yr = yp + (size_t)oh * OW;
+                    double *sr = sp ? sp + (size_t)oh * OW : NULL;
+                    if (st == 1)
+                        tap_row(yr, sr, xr, 1, v, ow0, ow1);
+                    else
+                        tap_row(yr, sr, xr, 2, v, ow0, ow1);
+                }
+            }
+        }
+        double b = bias ? bias[f] : 0.0;
+        for (size_t q = 0; q < oplane; ++q) {
+            double v = yp[q] + b;
+            yp[q] = (relu && v < 0.0) ? 0.0 : v;
+            if (sp)
+                sp[q] += fabs(b);
+        }
+    }
+    return bad ? -1 : 0;
+}
+
+/* The same loop with fp32 accumulation (float activations, outputs and
+ * bias): the CPU baseline the benchmark times.  Never used for parity. */
+int pso_conv_sparse_f32acc(const float *x, int n, int cin, int h, int w,
+                           int cout, int m, const uint16_t *masks,
+                           const int32_t *filter_perm, const int32_t *filter_ptr,
+                           const int32_t *cin_idx, const uint8_t *pat_id,
+                           const void *values, int vdtype, const float *bias, int relu,
+                           int st, float *y)
+{
+    if (n < 0 || cin < 0 || h < 1 || w < 1 || cout < 0 || m < 1 || m > 126 || st < 1 || st > 2)
+        return -1;
+    const int OH = (h - 1) / st + 1, OW = (w - 1) / st + 1;
+    const size_t plane = (size_t)h * w, oplane = (size_t)OH * OW;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t t = 0; t < (int64_t)n * cout; ++t) {
+        int nn = (int)(t / cout);
+        int i = (int)(t % cout);
+        int f = filter_perm[i];
+        float *yp = y + ((size_t)nn * cout + f) * oplane;
+        for (size_t q = 0; q < oplane; ++q)
+            yp[q] = 0.0f;
+        for (int32_t k = filter_ptr[i]; k < filter_ptr[i + 1]; ++k) {
+            int ci = cin_idx[k];
+            int p = pat_id[k];
+            if (p >= m || ci < 0 || ci >= cin) {
+                bad = 1;
+                continue;
+            }
+            const float *xc = x + ((size_t)nn * cin + ci) * plane;
+            int j = 0;
+            for (int q = 0; q < 9; ++q) {
+                if (!((masks[p] >> q) & 1))
+                    continue;
+                int r = q / 3, c = q % 3;
+                float v = (float)elem(values, vdtype, (size_t)k * 4 + j);
+                j += 1;
+                int oh0, oh1, ow0, ow1;
+                out_range(st, r, h, OH, &oh0, &oh1);
+                out_range(st, c, w, OW, &ow0, &ow1);
+                for (int oh = oh0; oh < oh1; ++oh) {
+                    const float *xr = xc + (size_t)(st * oh + r - 1) * w + (c - 1);
+                    float *yr = yp + (size_t)oh * OW;
+                    for (int ow = ow0; ow < ow1; ++ow)
+                        yr[ow] += v * xr[(size_t)st * ow];
+                }
+            }
+        }
+        float b = bias ? bias[f] : 0.0f;
+        for (size_t q = 0; q < oplane; ++q) {
+            float v = yp[q] + b;
+            yp[q] = (relu && v < 0.0f) ? 0.0f : v;
         }
     }
     return bad ? -1 : 0;

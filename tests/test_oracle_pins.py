@@ -489,3 +489,41 @@ def test_conv_strided_rejects_bad_stride():
     x = inputs.normal_activations(1, (1, 2, 4, 4))
     with pytest.raises(Exception):
         oracle.conv_sparse_strided(x, packed, masks, 2, 3)
+
+
+# ------------------------------------------- error scale and the CPU baseline
+@pytest.mark.parametrize("stride", [1, 2])
+def test_conv_scale_equals_abs_conv_torch(stride):
+    """The element-wise error scale s = sum |v*x| + |b| is the convolution of
+    |x| with the absolute masked weights plus |b| (torch.conv2d in fp64 on
+    the CPU), at stride 1 and 2."""
+    torch = pytest.importorskip("torch")
+    cin, cout = 7, 5
+    wt, masks, pat, keep, packed = _prepared(41 + stride, cout, cin, 8, 35)
+    x = inputs.normal_activations(9, (2, cin, 9, 10))
+    b = inputs.bias_vector(11, cout)
+    y, s = oracle.conv_sparse_strided(x, packed, masks, cout, stride, bias=b, want_scale=True)
+    masked = np.abs(oracle.mask_weights(wt, masks, pat, keep).astype(np.float64))
+    st = torch.nn.functional.conv2d(torch.from_numpy(np.abs(x.astype(np.float64))), torch.from_numpy(masked),
+                                    torch.from_numpy(np.abs(b.astype(np.float64))), stride=stride, padding=1)
+    assert st.shape == s.shape
+    assert float(np.abs(s - st.numpy()).max()) <= 1e-12 * float(st.abs().max())
+    assert (np.abs(y) <= s * (1 + 1e-12)).all()
+    if stride == 2:
+        _, s1 = oracle.conv_sparse(x, packed, masks, cout, bias=b, want_scale=True)
+        assert np.array_equal(s, s1[:, :, ::2, ::2])
+
+
+@pytest.mark.parametrize("stride", [1, 2])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_conv_f32acc_baseline_close_to_fp64(stride, dtype):
+    """The fp32-accumulating build of the conv loop (the timed CPU baseline)
+    stays within fp32 summation error of the fp64 oracle."""
+    cin, cout = 40, 12
+    wt, masks, pat, keep, packed = _prepared(52, cout, cin, 8, 50, dtype)
+    x = inputs.normal_activations(13, (2, cin, 11, 12), dtype)
+    b = inputs.bias_vector(14, cout, dtype)
+    y, s = oracle.conv_sparse_strided(x, packed, masks, cout, stride, bias=b, relu=True, want_scale=True)
+    y32 = oracle.conv_sparse_f32acc(x, packed, masks, cout, stride, bias=b, relu=True)
+    nterms = 4 * cin + 1
+    assert (np.abs(y32 - y) <= nterms * 2.0 ** -24 * s + 1e-30).all()
