@@ -1,22 +1,30 @@
 """Benchmark of the pattern-sparse 3x3 convolution forward on one MI355X.
 
-A step is one forward pass of the whole workload through the HIP path: for
-the VGG-16 stack (default) the 13 pattern-sparse conv layers with fused ReLU
-and the four 2x2 max-pools (fused into the conv launch they follow where
-that is faster, as timed at start-up) on a 1x3x224x224 synthetic image; for
-the other workloads every listed layer on its own resident input.  Weights are pruned
-and packed on the GPU (projection, selection, packing) before timing.  The
-step's launches are captured once in a HIP graph and the timed steps are its
-replays (--no-graph times eager launches); per-layer times come from an eager
-pass with HIP events.
+A step is one forward pass of a whole workload through the HIP path: for the
+VGG-16 stack (the headline workload) the 13 pattern-sparse conv layers with
+fused ReLU and the four 2x2 max-pools (fused into the conv launch they follow
+where that is faster, as timed at start-up) on a 1x3x224x224 synthetic
+image; for the other workloads every listed layer on its own resident input.
+Weights are pruned and packed on the GPU (projection, selection, packing)
+before timing.  The step's launches are captured once in a HIP graph and the
+timed steps are its replays (--no-graph times eager launches).
 
-Prints ONE JSON line: nonzero-MAC GFLOP/s of the step, ms/step, per-layer
-ms, the roofline of the conv kernel (measured with HIP events on the stream
-it runs on) and the CPU oracle as a baseline.  --details writes per-layer
-comparisons with the dense comparators (our dense HIP conv, MIOpen through
-torch) to a JSON file.
+The same run measures the other workloads the metric is quoted on (by
+default the 16 ResNet-50 3x3 layers in fp16 at batch 1 and 32).  For every
+workload it reports, per layer, the median, p10 and p90 of 30 samples of 5
+back-to-back launches timed with HIP events on the launch stream (after 10
+warm-up launches), the nonzero-MAC GFLOP/s, the roofline fraction, and the
+time of MIOpen's dense convolution of the same masked weights (torch
+conv2d) with the speedup over it; and the oracle's fp32-accumulating conv
+loop timed on the host cores, on all threads and on one.
+
+Prints ONE JSON line: the headline workload's nonzero-MAC GFLOP/s and
+ms/step, its conv kernels' roofline, the CPU baseline, and a "configs"
+object with the per-workload results.
 """
 import argparse
+import hashlib
+import glob
 import json
 import os
 import sys
@@ -29,8 +37,13 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "nonzero-MAC GFLOP/s + ms/layer, pattern-sparse 3x3 conv fwd, batch 1 and 32"
-PEAK_VALU_TFLOPS = 157.3     # MI355X fp32 vector peak (256 CU x 2.4 GHz x 256 flop/clk)
+# MI355X: 256 CUs x 4 SIMDs x 16 lanes x 2 flop (FMA) x 2.4 GHz.  Packed fp32
+# instructions (which double it to the published 157.3 TFLOP/s) are disabled
+# in this build, so the reachable vector ceiling is the non-packed one.
+PEAK_VALU_TFLOPS = 78.6
+PEAK_VALU_PACKED_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
+DEFAULT_CONFIGS = "vgg16_224_b1_f32,resnet50_3x3_b1_f16,resnet50_3x3_b32_f16"
 
 
 def parse():
@@ -38,10 +51,13 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="vgg16_224_b1_f32")
+    ap.add_argument("--workload", default="vgg16_224_b1_f32", help="the headline workload")
+    ap.add_argument("--configs", default=DEFAULT_CONFIGS,
+                    help="workloads measured in the same run (comma-separated); 'all' for every one")
     ap.add_argument("--algo", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--details", default=None, help="write per-layer comparisons to this JSON file")
+    ap.add_argument("--no-miopen", action="store_true")
+    ap.add_argument("--details", default=None, help="also write the per-layer results to this JSON file")
     ap.add_argument("--list", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
                     help="time eager launches instead of replays of a captured HIP graph of the step")
@@ -50,6 +66,8 @@ def parse():
                          "timed at start-up), all, none, or layer names separated by commas")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 256 MiB device-to-device copy (reference for HBM counters)")
+    ap.add_argument("--profile-only", action="store_true",
+                    help="only the headline workload's warm-up and timed eager steps (for profiler runs)")
     return ap.parse_args()
 
 
@@ -85,28 +103,28 @@ class Net:
             pooled = None
             if lay.pool_after:
                 pooled = torch.empty((n, lay.cout, lay.h // 2, lay.w // 2), dtype=tdt, device="cuda")
-            self.layers.append(dict(lay=lay, w=w, prep=prep, x=x, y=y, pooled=pooled, fused=False))
+            cfg = B.conv3x3_config(prep.layer, prep.layer.dtype, n, lay.h, lay.w, False, lay.stride, algo)
+            self.layers.append(dict(lay=lay, w=w, prep=prep, x=x, y=y, pooled=pooled, fused=False, cfg=cfg))
             if wl.chained:
                 x = pooled if pooled is not None else y
         torch.cuda.synchronize()
 
-    def step(self, events=None):
+    def launch(self, L):
         from paper_2003_06513_amd import binding as B
-        for li, L in enumerate(self.layers):
-            if events is not None:
-                events[li][0].record()
-            if L["fused"]:
-                # conv, ReLU and the 2x2 max-pool in one launch
-                B.conv3x3_fwd_pool2(L["prep"].layer, L["prep"].packed, L["x"], L["pooled"], relu=L["lay"].relu,
-                                    algo=self.algo)
-            elif L["lay"].stride != 1:
-                B.conv3x3_fwd_strided(L["prep"].layer, L["prep"].packed, L["x"], L["y"], L["lay"].stride,
-                                      relu=L["lay"].relu, algo=self.algo)
-            else:
-                B.conv3x3_fwd(L["prep"].layer, L["prep"].packed, L["x"], L["y"], relu=L["lay"].relu,
-                              algo=self.algo)
-            if events is not None:
-                events[li][1].record()
+        if L["fused"]:
+            # conv, ReLU and the 2x2 max-pool in one launch
+            B.conv3x3_fwd_pool2(L["prep"].layer, L["prep"].packed, L["x"], L["pooled"], relu=L["lay"].relu,
+                                algo=self.algo)
+        elif L["lay"].stride != 1:
+            B.conv3x3_fwd_strided(L["prep"].layer, L["prep"].packed, L["x"], L["y"], L["lay"].stride,
+                                  relu=L["lay"].relu, algo=self.algo)
+        else:
+            B.conv3x3_fwd(L["prep"].layer, L["prep"].packed, L["x"], L["y"], relu=L["lay"].relu, algo=self.algo)
+
+    def step(self):
+        from paper_2003_06513_amd import binding as B
+        for L in self.layers:
+            self.launch(L)
             if L["pooled"] is not None and not L["fused"]:
                 B.maxpool2x2(L["y"], L["pooled"])
 
@@ -127,7 +145,7 @@ class Net:
             for fused in (False, True):
                 L["fused"] = fused
                 one = [dict(L)]
-                run = lambda: Net.step(SimpleNamespace(layers=one, algo=self.algo))
+                run = lambda: Net.step(SimpleNamespace(layers=one, algo=self.algo, launch=self.launch))
                 for _ in range(3):
                     run()
                 s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -150,93 +168,212 @@ class Net:
         return 8.0 * self.wl.batch * oh * ow * lay.keep
 
 
-def cpu_baseline(net, budget_s=10.0):
-    """The oracle's sparse conv, as it stands, on the host cores."""
-    import oracle
-    oracle.build(force=False)
-    # bounded sample: image 0 of the batch through the layers in order,
-    # repeated whole passes until about budget_s of CPU work
-    host = [(L["lay"], L["prep"].packed.to_host(), L["x"][:1].cpu().numpy()) for L in net.layers]
-    flops, secs, passes, layers = 0.0, 0.0, 0, 0
-    while secs < budget_s:
-        for lay, packed, x in host:
-            t0 = time.perf_counter()
-            if lay.stride == 1:
-                oracle.conv_sparse(x, packed, net.masks, lay.cout, relu=lay.relu)
-            else:
-                oracle.conv_sparse_strided(x, packed, net.masks, lay.cout, lay.stride, relu=lay.relu)
-            secs += time.perf_counter() - t0
-            flops += 8.0 * lay.out_hw[0] * lay.out_hw[1] * lay.keep
-            layers += 1
-            if secs >= budget_s:
-                break
-        passes += 1
-    return {"value": round(flops / secs / 1e9, 3), "unit": "GFLOP/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": "fp64-accumulating oracle sparse conv on image 0 of the batch: %d layer runs "
-                      "(%d passes over the %d layers), %.2f nonzero-MAC GFLOP in %.2f s"
-                      % (layers, passes, len(host), flops / 1e9, secs)}
+def time_launches(fn, warm=10, samples=30, reps=5):
+    """Median, p10, p90 and mean in ms of one launch of fn: ``samples``
+    samples of ``reps`` back-to-back launches bracketed by HIP events on the
+    current stream (the one the launches use), after ``warm`` launches."""
+    import torch
+    for _ in range(warm):
+        fn()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(samples)]
+    for s, e in ev:
+        s.record()
+        for _ in range(reps):
+            fn()
+        e.record()
+    torch.cuda.synchronize()
+    t = np.array([s.elapsed_time(e) / reps for s, e in ev])
+    return float(np.median(t)), float(np.percentile(t, 10)), float(np.percentile(t, 90)), float(t.mean())
 
 
-def profiled_traffic(kernel_src, fused):
-    """HBM bytes per conv launch from the committed rocprofv3 counter summary
-    of this workload, or None when the kernel source or the set of layers
-    with the pool fused into the conv launch differ from the profiled ones."""
-    import hashlib
-    path = os.path.join(ROOT, "profiles", "k_conv_stream_vgg16_224_b1_f32.md")
-    if not os.path.exists(path):
-        return None
-    with open(kernel_src, "rb") as f:
-        digest = hashlib.sha256(f.read()).hexdigest()
-    fields = {}
-    with open(path) as f:
-        for line in f:
-            if line.startswith("- ") and ": " in line:
-                k, v = line[2:].strip().split(": ", 1)
-                fields[k.strip("`")] = v.strip().strip("`")
-    if fields.get("conv_stream.hip sha256") != digest:
-        return None
-    if fields.get("pool fused into") != (",".join(fused) or "none"):
-        return None
-    try:
-        return int(fields["hbm bytes per conv launch"])
-    except (KeyError, ValueError):
-        return None
+def time_step(net, steps, warmup, graph):
+    """ms per step: ``steps`` timed steps (eager, or replays of a HIP graph of
+    the step whose output is checked against the eager step's)."""
+    import torch
+    for _ in range(warmup):
+        net.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        net.step()
+    torch.cuda.synchronize()
+    ms_eager = (time.perf_counter() - t0) * 1e3 / steps
+    if not graph:
+        return ms_eager, ms_eager
+    eager_out = net.output().clone()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        net.step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        net.step()
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    if not torch.equal(net.output(), eager_out):
+        raise SystemExit("graph replay of the step differs from the eager step")
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        g.replay()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps, ms_eager
 
 
-def compare_dense(net, reps=20):
-    """Per-layer times of the dense comparators on the masked weights."""
+def layer_table(net, miopen):
+    """Per layer: the sparse conv launch as the step runs it, and MIOpen's
+    dense conv of the same masked weights (torch conv2d, + ReLU where the
+    layer has it; stride as the layer's)."""
     import torch
     from paper_2003_06513_amd import binding as B
-    out = []
-    for L in net.layers:
+    rows = []
+    for li, L in enumerate(net.layers):
         lay, prep = L["lay"], L["prep"]
-        if lay.stride != 1:
-            continue                     # the dense comparators are stride 1
-        wd = torch.empty(L["w"].shape, dtype=net.tdt, device="cuda")
-        B.unpack_dense(prep.layer, prep.packed, wd)
-        yd = torch.empty_like(L["y"])
-
-        def timeit(fn):
-            for _ in range(3):
-                fn()
-            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        med, p10, p90, mean = time_launches(lambda: net.launch(L))
+        nz = net.nz_flops(li)
+        row = dict(layer=lay.name, cin=lay.cin, cout=lay.cout, h=lay.h, w=lay.w, stride=lay.stride, keep=lay.keep,
+                   fused_pool=bool(L["fused"]), ms=round(med, 5), p10=round(p10, 5), p90=round(p90, 5),
+                   mean_ms=round(mean, 5), nz_gflops=round(nz / (med * 1e-3) / 1e9, 1),
+                   kernel=["stream", "wide", "simple"][L["cfg"]["kernel"]] + ("-staged" if L["cfg"]["staged"] else ""),
+                   R=L["cfg"]["rows_per_lane"], KS=L["cfg"]["shares"])
+        if miopen:
+            wd = torch.empty(L["w"].shape, dtype=net.tdt, device="cuda")
+            B.unpack_dense(prep.layer, prep.packed, wd)
             torch.cuda.synchronize()
-            s.record()
-            for _ in range(reps):
-                fn()
-            e.record()
-            torch.cuda.synchronize()
-            return s.elapsed_time(e) / reps
+            st = lay.stride
 
-        t_sparse = timeit(lambda: B.conv3x3_fwd(prep.layer, prep.packed, L["x"], L["y"], relu=lay.relu))
-        t_dense = timeit(lambda: B.dense3x3_fwd(L["x"], wd, yd, relu=lay.relu))
-        t_miopen = timeit(lambda: torch.relu_(torch.nn.functional.conv2d(L["x"], wd, padding=1))
-                          if lay.relu else torch.nn.functional.conv2d(L["x"], wd, padding=1))
-        out.append(dict(layer=lay.name, cin=lay.cin, cout=lay.cout, h=lay.h, w=lay.w, keep=lay.keep,
-                        sparse_ms=t_sparse, dense_hip_ms=t_dense, miopen_ms=t_miopen,
-                        nz_gflops=8.0 * net.wl.batch * lay.h * lay.w * lay.keep / t_sparse / 1e6))
-    return out
+            def dense():
+                y = torch.nn.functional.conv2d(L["x"], wd, padding=1, stride=st)
+                return torch.relu_(y) if lay.relu else y
+            if L["fused"]:
+                def dense_pool():
+                    return torch.nn.functional.max_pool2d(dense(), 2)
+                dmed = time_launches(dense_pool, warm=3)[0]
+            else:
+                dmed = time_launches(dense, warm=3)[0]
+            row["miopen_ms"] = round(dmed, 5)
+            row["speedup_vs_miopen"] = round(dmed / med, 3)
+        rows.append(row)
+    return rows
+
+
+def cpu_baseline(net, budget_s=8.0):
+    """The oracle's conv loop built with fp32 accumulation (-O3, x86-64-v3: AVX2 + FMA)
+    on the host cores: one full step of the workload (every layer, every
+    image, on the inputs the GPU layers received) on all threads, median of
+    up to 5 runs within budget_s; and on 1 thread the first image's pass,
+    median of up to 3 runs."""
+    import oracle
+    oracle.build(force=False)
+    host = [(L["lay"], L["prep"].packed.to_host(), L["x"].cpu().numpy()) for L in net.layers]
+    flops = sum(8.0 * x.shape[0] * lay.out_hw[0] * lay.out_hw[1] * lay.keep for lay, _, x in host)
+    flops1 = sum(8.0 * lay.out_hw[0] * lay.out_hw[1] * lay.keep for lay, _, _ in host)
+
+    def run(images):
+        t0 = time.perf_counter()
+        for lay, packed, x in host:
+            oracle.conv_sparse_f32acc(x[:images], packed, net.masks, lay.cout, lay.stride, relu=lay.relu)
+        return time.perf_counter() - t0
+
+    ncores = os.cpu_count() or 1
+    oracle.bench_set_num_threads(ncores)
+    cores = oracle.bench_num_threads()
+    ts, spent = [], 0.0
+    while len(ts) < 5 and (spent < budget_s or len(ts) < 1):
+        ts.append(run(net.wl.batch))
+        spent += ts[-1]
+    oracle.bench_set_num_threads(1)
+    t1, spent = [], 0.0
+    while len(t1) < 3 and (spent < budget_s or len(t1) < 1):
+        t1.append(run(1))
+        spent += t1[-1]
+    oracle.bench_set_num_threads(ncores)
+    t, tt = float(np.median(ts)), float(np.median(t1))
+    return {"value": round(flops / t / 1e9, 3), "unit": "GFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": "fp32-accumulating build of the oracle's sparse conv loop (-O3 x86-64-v3, OpenMP over "
+                      "(image, filter)); all %d threads: one full step (%d layers x %d images, %.3f nonzero-MAC "
+                      "GFLOP), median of %d runs = %.2f ms; 1 thread: image 0 of every layer, median of %d runs"
+                      % (cores, len(host), net.wl.batch, flops / 1e9, len(ts), t * 1e3, len(t1)),
+            "ms_per_step": round(t * 1e3, 3),
+            "value_1thread": round(flops1 / tt / 1e9, 3)}
+
+
+def conv_sources_digest():
+    """sha256 over the conv kernel sources (a committed counter summary is
+    valid only for the kernels it measured)."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2003_06513_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "conv_*.h")) + glob.glob(os.path.join(csrc, "conv_*.hip"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def profiled_traffic(workload, fused):
+    """HBM bytes per conv launch from the committed rocprofv3 counter summary
+    of this workload, or None when the conv sources or the set of layers with
+    the pool fused into the conv launch differ from the profiled ones."""
+    paths = glob.glob(os.path.join(ROOT, "profiles", "*_%s.md" % workload))
+    for path in paths:
+        fields = {}
+        with open(path) as f:
+            for line in f:
+                if line.startswith("- ") and ": " in line:
+                    k, v = line[2:].strip().split(": ", 1)
+                    fields[k.strip("`")] = v.strip().strip("`")
+        if "hbm bytes per conv launch" not in fields:
+            continue
+        if fields.get("conv sources sha256") != conv_sources_digest():
+            return None
+        if fields.get("pool fused into") not in (None, ",".join(fused) or "none"):
+            return None
+        try:
+            return int(fields["hbm bytes per conv launch"])
+        except ValueError:
+            return None
+    return None
+
+
+def measure(wl, args, headline):
+    """Everything reported for one workload."""
+    net = Net(wl, args.algo)
+    net.choose_fusion(args.fuse_pool)
+    ms_step, ms_eager = time_step(net, args.steps, args.warmup, not args.no_graph)
+    rows = layer_table(net, not args.no_miopen)
+    nz = [net.nz_flops(li) for li in range(len(net.layers))]
+    conv_ms = sum(r["mean_ms"] for r in rows)
+    achieved = sum(nz) / (conv_ms * 1e-3) / 1e12
+    res = {
+        "batch": wl.batch, "dtype": wl.dtype, "m": wl.m, "layers": len(wl.layers),
+        "ms_per_step": round(ms_step, 4), "ms_per_step_eager": round(ms_eager, 4),
+        "step_launch": "eager" if args.no_graph else "hip graph replay",
+        "nz_gflops": round(sum(nz) / (ms_step * 1e-3) / 1e9, 2),
+        "conv_ms_per_step": round(conv_ms, 4),
+        "roofline_frac": round(achieved / PEAK_VALU_TFLOPS, 4),
+        "pool_fused_into": [L["lay"].name for L in net.layers if L["fused"]],
+        "ms_per_layer": {r["layer"]: r["ms"] for r in rows},
+        "layer_detail": rows,
+    }
+    if not args.no_miopen:
+        dense_ms = sum(r["miopen_ms"] for r in rows)
+        sparse_ms = sum(r["ms"] for r in rows)
+        res["miopen_ms_per_step"] = round(dense_ms, 4)
+        res["speedup_vs_miopen"] = round(dense_ms / sparse_ms, 3)
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(net)
+    roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_VALU_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_VALU_TFLOPS, 4),
+            "peak_packed_fp32": PEAK_VALU_PACKED_TFLOPS,
+            "frac_of_packed_peak": round(achieved / PEAK_VALU_PACKED_TFLOPS, 4),
+            "traffic": profiled_traffic(wl.name, res["pool_fused_into"]),
+            "kernel": ", ".join(sorted({r["kernel"] for r in rows})),
+            "per_launch": "8*N*H*W*keep nonzero-MAC flops averaged over the %d conv launches of a step, / their "
+                          "mean duration (HIP events around back-to-back launches on the launch stream); peak: "
+                          "non-packed fp32 FMA, 256 CU x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz" % len(rows),
+            "avg_launch_us": round(conv_ms * 1e3 / len(rows), 3)}
+    return net, res, roof
 
 
 def main():
@@ -263,94 +400,60 @@ def main():
                           "launches": 5}))
         return
     B.lib()
-    wl = find_workload(args.workload)
-    net = Net(wl, args.algo)
-    net.choose_fusion(args.fuse_pool)
-
-    for _ in range(args.warmup):
-        net.step()
-    torch.cuda.synchronize()
-    K = args.steps
-    # eager steps with HIP events around every conv launch (on the stream the
-    # launches use): per-layer times and the kernel's roofline
-    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
-           for _ in net.layers] for _ in range(K)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(K):
-        net.step(ev[k])
-    torch.cuda.synchronize()
-    ms_eager = (time.perf_counter() - t0) * 1e3 / K
-    ms_step, graph = ms_eager, False
-    if not args.no_graph:
-        # the step's conv and pool launches captured once in a HIP graph
-        # and replayed: the timed region is the replays alone
-        eager_out = net.output().clone()
-        g = torch.cuda.CUDAGraph()
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
+    head = find_workload(args.workload)
+    if args.profile_only:
+        net = Net(head, args.algo)
+        net.choose_fusion(args.fuse_pool)
+        for _ in range(args.warmup + args.steps):
             net.step()
-        torch.cuda.current_stream().wait_stream(side)
         torch.cuda.synchronize()
-        with torch.cuda.graph(g):
-            net.step()
-        for _ in range(args.warmup):
-            g.replay()
-        torch.cuda.synchronize()
-        if not torch.equal(net.output(), eager_out):
-            raise SystemExit("graph replay of the step differs from the eager step")
-        t0 = time.perf_counter()
-        for _ in range(K):
-            g.replay()
-        torch.cuda.synchronize()
-        ms_step, graph = (time.perf_counter() - t0) * 1e3 / K, True
-    layer_ms = [float(np.median([ev[k][li][0].elapsed_time(ev[k][li][1]) for k in range(K)]))
-                for li in range(len(net.layers))]
-    layer_mean_ms = [float(np.mean([ev[k][li][0].elapsed_time(ev[k][li][1]) for k in range(K)]))
-                     for li in range(len(net.layers))]
-    nz = [net.nz_flops(li) for li in range(len(net.layers))]
-    total_nz = sum(nz)
-    conv_ms = sum(layer_mean_ms)
-    achieved_tf = total_nz / (conv_ms * 1e-3) / 1e12
-    traffic = None
-    if wl.name == "vgg16_224_b1_f32":
-        traffic = profiled_traffic(os.path.join(ROOT, "paper_2003_06513_amd", "csrc", "conv_stream.hip"),
-                                   [L["lay"].name for L in net.layers if L["fused"]])
-    roof = {"bound": "alu", "achieved": round(achieved_tf, 3), "peak": PEAK_VALU_TFLOPS,
-            "unit": "TFLOP/s", "frac": round(achieved_tf / PEAK_VALU_TFLOPS, 4), "traffic": traffic,
-            "kernel": ("k_conv_wide (224- and 112-wide layers) + k_conv_stream (the others)"
-                   if wl.name == "vgg16_224_b1_f32" else
-                   "k_conv_stream / k_conv_wide" + (" + k_conv_simple (stride-2 layers)"
-                                                    if any(L["lay"].stride != 1 for L in net.layers) else "")),
-            "per_launch": "8*N*H*W*keep nonzero-MAC flops averaged over the %d conv launches of a step, "
-                          "/ their mean duration (HIP events on the launch stream)" % len(net.layers),
-            "avg_launch_us": round(conv_ms * 1e3 / len(net.layers), 3)}
+        print(json.dumps({"workload": head.name, "steps": args.steps, "warmup": args.warmup,
+                          "pool_fused_into": [L["lay"].name for L in net.layers if L["fused"]]}), flush=True)
+        return
+    if args.configs == "all":
+        from synthetic import inputs
+        names = [wl.name for wl in inputs.all_workloads()]
+    else:
+        names = [n for n in args.configs.split(",") if n]
+    if head.name not in names:
+        names.insert(0, head.name)
+    configs, roofs = {}, {}
+    for name in names:
+        print("[bench] %s" % name, file=sys.stderr, flush=True)
+        _, res, roof = measure(find_workload(name), args, name == head.name)
+        configs[name] = res
+        roofs[name] = roof
+    hr = configs[head.name]
     line = {
-        "metric": METRIC, "value": round(total_nz / (ms_step * 1e-3) / 1e9, 2), "unit": "GFLOP/s",
-        "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "metric": METRIC, "value": hr["nz_gflops"], "unit": "GFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": hr["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": wl.dtype, "data": "synthetic",
-        "config": {"workload": wl.name, "batch": wl.batch, "layers": len(wl.layers), "m": wl.m,
-                   "stack": "conv+relu, 2x2 max-pool after conv2/4/7/10" if wl.chained else "independent layers",
-                   "pool_fused_into": [L["lay"].name for L in net.layers if L["fused"]]},
-        "pool_fusion_us_unfused_fused": {L["lay"].name: L["fusion_us"] for L in net.layers if "fusion_us" in L},
-        "step_launch": "hip graph replay" if graph else "eager",
-        "ms_per_step_eager": round(ms_eager, 4),
-        "ms_per_layer": {L["lay"].name: round(t, 4) for L, t in zip(net.layers, layer_ms)},
-        "conv_ms_per_step": round(conv_ms, 4),
-        "roofline": roof,
+        "dtype": head.dtype, "data": "synthetic",
+        "config": {"workload": head.name, "batch": head.batch, "layers": len(head.layers), "m": head.m,
+                   "stack": "conv+relu, 2x2 max-pool after conv2/4/7/10" if head.chained else "independent layers",
+                   "pool_fused_into": hr["pool_fused_into"]},
+        "step_launch": hr["step_launch"], "ms_per_step_eager": hr["ms_per_step_eager"],
+        "ms_per_layer": hr["ms_per_layer"],
+        "roofline": roofs[head.name],
     }
-    details = {}
-    if args.details:
-        details["dense_compare"] = compare_dense(net)
-    if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(net)
+    if "cpu_baseline" in hr:
+        line["cpu_baseline"] = hr["cpu_baseline"]
+    line["configs"] = {}
+    for name, res in configs.items():
+        c = {k: v for k, v in res.items() if k not in ("layer_detail", "cpu_baseline")}
+        c["roofline"] = {k: roofs[name][k] for k in ("achieved", "peak", "frac", "traffic")}
+        if "cpu_baseline" in res:
+            c["cpu_gflops_all_cores"] = res["cpu_baseline"]["value"]
+            c["cpu_gflops_1thread"] = res["cpu_baseline"]["value_1thread"]
+            c["cpu_cores"] = res["cpu_baseline"]["cores"]
+        c["layers_detail"] = [{k: r[k] for k in ("layer", "ms", "p10", "p90", "nz_gflops", "kernel", "R", "KS")
+                               + (("miopen_ms", "speedup_vs_miopen") if "miopen_ms" in r else ())}
+                              for r in res["layer_detail"]]
+        line["configs"][name] = c
     print(json.dumps(line), flush=True)
     if args.details:
-        details["line"] = line
         with open(args.details, "w") as f:
-            json.dump(details, f, indent=1)
+            json.dump({"line": line, "configs": configs}, f, indent=1)
 
 
 if __name__ == "__main__":

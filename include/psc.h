@@ -185,6 +185,32 @@ psc_status psc_conv3x3_fwd_strided(const psc_layer *layer, const psc_packed *pac
                                    int32_t relu, void *d_y, int32_t stride, int32_t algo,
                                    void *stream);
 
+/* The launch configuration the conv entry points would use for a call with
+ * these arguments: which kernel runs and how work maps onto it.  Host only,
+ * no device work; arguments are validated as by psc_conv3x3_fwd_strided
+ * (pool != 0 as by psc_conv3x3_fwd_pool2, which needs stride 1), except that
+ * no pointer is needed.  Meant for tests and benchmark reports. */
+typedef struct psc_conv_config {
+    int32_t kernel;            /* 0: tuned kernel, one output column per lane
+                                  1: tuned kernel, 4 output columns per lane
+                                  2: one-output-per-lane kernel */
+    int32_t staged;            /* 0: input rows loaded straight into registers,
+                                  1: staged through LDS, one run per wave,
+                                  2: staged through LDS, several runs per wave */
+    int32_t rows_per_lane;     /* output rows per lane */
+    int32_t cols_per_lane;     /* output columns per lane */
+    int32_t segments_per_wave; /* row bands (or column tiles) per wave */
+    int32_t column_tiles;      /* column tiles per image row (1: full rows) */
+    int32_t shares;            /* waves that split one filter's kernels */
+    int32_t filters_per_block;
+    int32_t blocks;
+    int32_t threads_per_block;
+} psc_conv_config;
+
+psc_status psc_conv3x3_config(const psc_layer *layer, int32_t act_dtype, int32_t n,
+                              int32_t h, int32_t w, int32_t pool, int32_t stride,
+                              int32_t algo, psc_conv_config *out);
+
 /* Comparator: the dense 3x3 convolution (stride 1, pad 1) of dense OIHW
  * weights d_w [cout][cin][3][3] on the vector ALUs, same conventions and
  * accumulation as psc_conv3x3_fwd. */

@@ -51,11 +51,12 @@ def _compile(out: str, flags) -> None:
 def build(force: bool = True) -> str:
     """Compile pso.c into oracle/libpso.so (gcc, OpenMP, no fast-math, no
     contraction: every add and multiply rounds as written) and, for the
-    timed CPU baseline only, into oracle/libpso_bench.so (-O3 -march=native)."""
+    timed CPU baseline only, into oracle/libpso_bench.so (-O3, AVX2 + FMA:
+    x86-64-v3, which this container and the GPU hosts both run)."""
     if force or not os.path.exists(_LIB_PATH):
         _compile(_LIB_PATH, ["-O3", "-ffp-contract=off", "-fno-fast-math"])
     if force or not os.path.exists(_BENCH_PATH):
-        _compile(_BENCH_PATH, ["-O3", "-march=native"])
+        _compile(_BENCH_PATH, ["-O3", "-march=x86-64-v3"])
     return _LIB_PATH
 
 
@@ -63,6 +64,8 @@ def _declare(lib):
     P = ctypes.c_void_p
     i32, i64 = ctypes.c_int32, ctypes.c_int64
     lib.pso_num_threads.restype = ctypes.c_int
+    lib.pso_set_num_threads.argtypes = [ctypes.c_int]
+    lib.pso_set_num_threads.restype = None
     lib.pso_select_library.argtypes = [P, i32, i64, i32, P]
     lib.pso_project.argtypes = [P, i32, i64, P, i32, P, P]
     lib.pso_select.argtypes = [P, i64, i64, P]
@@ -254,7 +257,7 @@ def conv_sparse(x: np.ndarray, packed: dict, masks, cout: int, bias=None,
 
 def conv_sparse_f32acc(x: np.ndarray, packed: dict, masks, cout: int, stride: int = 1, bias=None,
                        relu: bool = False) -> np.ndarray:
-    """The same loop accumulating in fp32 (-O3 -march=native build): the CPU
+    """The same loop accumulating in fp32 (-O3 x86-64-v3 build): the CPU
     baseline the benchmark times, never a parity reference.  Activations
     are taken as fp32 (fp16 widened before the call)."""
     x, masks, vals, vcode, idx = _conv_args(x, packed, masks)
@@ -271,6 +274,11 @@ def conv_sparse_f32acc(x: np.ndarray, packed: dict, masks, cout: int, stride: in
 
 def bench_num_threads() -> int:
     return int(_load_bench().pso_num_threads())
+
+
+def bench_set_num_threads(n: int) -> None:
+    """Threads the fp32-accumulating baseline build uses from now on."""
+    _load_bench().pso_set_num_threads(int(n))
 
 
 def conv_dense(x: np.ndarray, wdense: np.ndarray, bias=None, relu: bool = False):

@@ -101,6 +101,18 @@ int pso_num_threads(void)
 #endif
 }
 
+/* Threads for the following parallel loops (the benchmark times the
+ * baseline on all cores and on one). */
+void pso_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------------ */
 /* Sec. 4.2: for every kernel, the positions of its 3 largest non-centre
  * weights plus the centre form a 4-entry pattern; the m patterns that occur

@@ -41,6 +41,12 @@ class CLayer(ctypes.Structure):
                 ("masks", ctypes.c_uint16 * MAX_PATTERNS)]
 
 
+class CConvConfig(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "kernel", "staged", "rows_per_lane", "cols_per_lane", "segments_per_wave", "column_tiles",
+        "shares", "filters_per_block", "blocks", "threads_per_block")]
+
+
 PACKED_FIELDS = ("filter_perm", "filter_ptr", "seg_ptr", "cin_idx", "pat_id", "values")
 
 
@@ -85,6 +91,8 @@ def lib() -> ctypes.CDLL:
         "psc_conv3x3_fwd_algo": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, P], ctypes.c_int),
         "psc_conv3x3_fwd_pool2": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, P], ctypes.c_int),
         "psc_conv3x3_fwd_strided": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, i32, P], ctypes.c_int),
+        "psc_conv3x3_config": ([LP, i32, i32, i32, i32, i32, i32, i32, ctypes.POINTER(CConvConfig)],
+                               ctypes.c_int),
         "psc_dense3x3_fwd": ([i32, P, i32, i32, i32, i32, P, i32, P, i32, P, P], ctypes.c_int),
         "psc_maxpool2x2": ([i32, P, i32, i32, i32, i32, P, P], ctypes.c_int),
     }
@@ -271,6 +279,15 @@ def conv3x3_fwd_strided(layer: Layer, packed: Packed, x, y, stride: int, bias=No
     _check(lib().psc_conv3x3_fwd_strided(layer.ref(), ctypes.byref(cp), dtype_code(x), _dev(x, "x"), n, h, w,
                                          _dev(bias, "bias"), int(bool(relu)), _dev(y, "y"), stride,
                                          int(algo), _stream(stream)), "psc_conv3x3_fwd_strided")
+
+
+def conv3x3_config(layer: Layer, dtype: int, n: int, h: int, w: int, pool: bool = False, stride: int = 1,
+                   algo: int = 0) -> dict:
+    """psc_conv3x3_config: the launch configuration of a conv call (host only)."""
+    c = CConvConfig()
+    _check(lib().psc_conv3x3_config(layer.ref(), int(dtype), int(n), int(h), int(w), int(bool(pool)),
+                                    int(stride), int(algo), ctypes.byref(c)), "psc_conv3x3_config")
+    return {name: int(getattr(c, name)) for name, _ in CConvConfig._fields_}
 
 
 def dense3x3_fwd(x, wd, y, bias=None, relu: bool = False, stream=None):

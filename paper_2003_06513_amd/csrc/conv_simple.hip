@@ -8,6 +8,7 @@ namespace psc {
 
 hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const ConvArgs& a,
                               hipStream_t stream);
+bool describe_conv_stream(const PatTable& tab, const ConvArgs& a, ConvForm& out);
 
 namespace {
 
@@ -174,6 +175,13 @@ hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs
     }
     return a.dtype == DT_F16 ? conv_simple<DT_F16>(tab, pk, a, stream)
                              : conv_simple<DT_F32>(tab, pk, a, stream);
+}
+
+void describe_conv(const PatTable& tab, const ConvArgs& a, int algo, ConvForm& out) {
+    if (algo == 0 && a.stride == 1 && describe_conv_stream(tab, a, out)) return;
+    const int outs = a.pool ? (a.h / 2) * (a.w / 2) : ((a.h - 1) / a.stride + 1) * ((a.w - 1) / a.stride + 1);
+    const int64_t lanes = int64_t(a.n) * outs;
+    out = ConvForm{2, 0, 1, 1, 1, 1, 1, 1, int((lanes + 255) / 256) * a.cout, 256};
 }
 
 hipError_t launch_dense(int dtype, const void* x, int n, int cin, int h, int w, const void* wd, int cout,

@@ -90,6 +90,8 @@ struct Geo {
     int lds;        // 1: input rows staged through per-wave LDS (full-row segments only)
     int region;     // LDS bytes reserved per run of rows
     int wave_bytes; // LDS bytes per wave: nruns regions + a zero area
+    int R;          // rows per lane (the kernel's template argument)
+    int form;       // 0: one column per lane (k_conv_stream), 1: 4 columns per lane (k_conv_wide)
     int8_t shape[kMaxPatterns];  // centre+3 shape index of each library pattern, -1 = generic
     uint16_t mask[kMaxPatterns];
 };

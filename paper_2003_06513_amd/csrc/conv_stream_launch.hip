@@ -26,15 +26,14 @@ extern template hipError_t cs::launch_wide<2>(const PackedView&, const ConvArgs&
 // (ceil(units / S) * R, larger R on ties; even R when pooling; R = 8 only
 // with one segment per wave); a workgroup holds 4 filters, or
 // fewer filters split into KS shares (KS doubles up to 8) while the grid
-// holds under 4 waves per SIMD.  Returns hipErrorNotSupported when x exceeds
-// the 2 GiB a buffer descriptor addresses here.
-hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const ConvArgs& a,
-                              hipStream_t stream) {
+// holds under 4 waves per SIMD.  Returns false when the tuned kernels do not
+// take the call: x beyond the 2 GiB a buffer descriptor addresses here, or a
+// pooled output of haloed column tiles.  Host only.
+bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
     const int64_t x_bytes = int64_t(a.n) * a.cin * a.h * a.w * (a.dtype == DT_F16 ? 2 : 4);
     // buffer descriptors address at most 2 GiB (x) and the packed weights
     if (x_bytes > (int64_t(1) << 31) || a.keep * 4 * (a.dtype == DT_F16 ? 2 : 4) > 0x7fffffff)
-        return hipErrorNotSupported;
-    Geo g;
+        return false;
     std::memset(&g, 0, sizeof g);
     g.n = a.n;
     g.cin = a.cin;
@@ -74,7 +73,9 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
         if (g.FW > a.cout) g.FW = a.cout;
         g.groups_x = (a.cout + g.FW - 1) / g.FW;
         g.nblocks = g.groups_x * sgroups;
-        return launch_wide<R>(pk, a, g, stream);
+        g.R = R;
+        g.form = 1;
+        return true;
     }
     // lane layout: full-row segments if they use the lanes at least as well
     // as haloed column tiles
@@ -96,7 +97,7 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
         g.Wt = a.w;
         g.CT = 1;
     } else {
-        if (a.pool) return hipErrorNotSupported;   // pooling needs full-row segments
+        if (a.pool) return false;   // pooling needs full-row segments
         const int Wt = (a.w + ct - 1) / ct;
         g.cols_mode = 1;
         g.S = 64 / (Wt + 2);
@@ -167,7 +168,17 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
         g.lds = fits && throughput ? 1 : 0;
         if (g.lds && nruns_max > 1) g.lds = 2;             // several runs per wave: the general form
     }
-    switch (R) {
+    g.R = R;
+    g.form = 0;
+    return true;
+}
+
+hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const ConvArgs& a,
+                              hipStream_t stream) {
+    Geo g;
+    if (!plan_conv_stream(tab, a, g)) return hipErrorNotSupported;
+    if (g.form == 1) return launch_wide<2>(pk, a, g, stream);
+    switch (g.R) {
         case 8: return a.dtype == DT_F16 ? launch_r<DT_F16, 8>(pk, a, g, stream)
                                          : launch_r<DT_F32, 8>(pk, a, g, stream);
         case 7: return a.dtype == DT_F16 ? launch_r<DT_F16, 7>(pk, a, g, stream)
@@ -177,6 +188,24 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
         default: return a.dtype == DT_F16 ? launch_r<DT_F16, 2>(pk, a, g, stream)
                                           : launch_r<DT_F32, 2>(pk, a, g, stream);
     }
+}
+
+// The launch configuration of a tuned-kernel call, for the configuration
+// query of the C ABI.  Host only.
+bool describe_conv_stream(const PatTable& tab, const ConvArgs& a, ConvForm& out) {
+    Geo g;
+    if (!plan_conv_stream(tab, a, g)) return false;
+    out.kernel = g.form == 1 ? 1 : 0;
+    out.staged = g.form == 1 ? 0 : g.lds;
+    out.rows_per_lane = g.R;
+    out.cols_per_lane = g.form == 1 ? 4 : 1;
+    out.segments_per_wave = g.S;
+    out.column_tiles = g.CT;
+    out.shares = g.KS;
+    out.filters_per_block = g.FW;
+    out.blocks = g.nblocks;
+    out.threads_per_block = g.FW * g.KS * 64;
+    return true;
 }
 
 }  // namespace psc

@@ -59,6 +59,15 @@ struct ConvArgs {
 };
 hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs& a, int algo,
                        hipStream_t stream);
+
+// The launch configuration launch_conv would use (host only, no device work).
+struct ConvForm {
+    int kernel;             // 0 k_conv_stream, 1 k_conv_wide, 2 k_conv_simple
+    int staged;             // 0 direct loads, 1 rows staged through LDS, 2 staged, several runs per wave
+    int rows_per_lane, cols_per_lane, segments_per_wave, column_tiles;
+    int shares, filters_per_block, blocks, threads_per_block;
+};
+void describe_conv(const PatTable& tab, const ConvArgs& a, int algo, ConvForm& out);
 hipError_t launch_dense(int dtype, const void* x, int n, int cin, int h, int w, const void* wd,
                         int cout, const void* bias, int relu, void* y, hipStream_t stream);
 hipError_t launch_maxpool(int dtype, const void* x, int n, int c, int h, int w, void* y,

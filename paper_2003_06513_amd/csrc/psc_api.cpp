@@ -264,11 +264,10 @@ psc_status psc_unpack_dense(const psc_layer* L, const psc_packed* pk, void* d_w_
                          "psc_unpack_dense launch");
 }
 
-static psc_status conv_common(const psc_layer* L, const psc_packed* pk, int32_t act_dtype, const void* d_x,
-                              int32_t n, int32_t h, int32_t w, const void* d_bias, int32_t relu, void* d_y,
-                              int32_t algo, int pool, int32_t stride, void* stream) {
+// Shape checks of every conv entry point (no pointers involved).
+static psc_status check_conv_shape(const psc_layer* L, int32_t act_dtype, int32_t n, int32_t h, int32_t w,
+                                   int32_t algo, int pool, int32_t stride) {
     if (psc_status s = check_layer(L, true)) return s;
-    if (psc_status s = check_packed(L, pk)) return s;
     if (!dtype_ok(act_dtype)) return fail(PSC_ERR_ARG, "act_dtype=%d is not a psc_dtype", act_dtype);
     if (act_dtype != L->wdtype)
         return fail(PSC_ERR_UNSUPPORTED, "act_dtype=%d differs from wdtype=%d", act_dtype, L->wdtype);
@@ -283,6 +282,23 @@ static psc_status conv_common(const psc_layer* L, const psc_packed* pk, int32_t 
     const int64_t xe = int64_t(n) * L->cin * plane, ye = int64_t(n) * L->cout * oplane;
     if (xe > kMaxElems || ye > kMaxElems)
         return fail(PSC_ERR_ARG, "x or y holds more than 2^31-1 elements");
+    if (pool && stride != 1) return fail(PSC_ERR_ARG, "the fused 2x2 pool needs stride 1");
+    return PSC_OK;
+}
+
+static psc::ConvArgs conv_args(const psc_layer* L, int32_t act_dtype, const void* d_x, int32_t n, int32_t h,
+                               int32_t w, const void* d_bias, int32_t relu, void* d_y, int pool, int32_t stride) {
+    return psc::ConvArgs{act_dtype, n, L->cin, h, w, L->cout, L->keep, d_x, d_bias, relu != 0, d_y, pool, stride};
+}
+
+static psc_status conv_common(const psc_layer* L, const psc_packed* pk, int32_t act_dtype, const void* d_x,
+                              int32_t n, int32_t h, int32_t w, const void* d_bias, int32_t relu, void* d_y,
+                              int32_t algo, int pool, int32_t stride, void* stream) {
+    if (psc_status s = check_conv_shape(L, act_dtype, n, h, w, algo, pool, stride)) return s;
+    if (psc_status s = check_packed(L, pk)) return s;
+    const int64_t plane = int64_t(h) * w;
+    const int64_t oplane = pool ? plane / 4 : int64_t((h - 1) / stride + 1) * ((w - 1) / stride + 1);
+    const int64_t xe = int64_t(n) * L->cin * plane, ye = int64_t(n) * L->cout * oplane;
     if (n == 0) return ok();
     if (!d_x || !d_y) return fail(PSC_ERR_ARG, "d_x and d_y must be non-NULL");
     const size_t es = elt_size(act_dtype);
@@ -293,8 +309,21 @@ static psc_status conv_common(const psc_layer* L, const psc_packed* pk, int32_t 
     const psc::PatTable t = table_of(L);
     const psc::PackedView v{pk->filter_perm, pk->filter_ptr, pk->seg_ptr,
                             pk->cin_idx,     pk->pat_id,     pk->values};
-    const psc::ConvArgs a{act_dtype, n, L->cin, h, w, L->cout, L->keep, d_x, d_bias, relu != 0, d_y, pool, stride};
+    const psc::ConvArgs a = conv_args(L, act_dtype, d_x, n, h, w, d_bias, relu, d_y, pool, stride);
     return device_status(psc::launch_conv(t, v, a, algo, as_stream(stream)), "psc_conv3x3_fwd launch");
+}
+
+psc_status psc_conv3x3_config(const psc_layer* L, int32_t act_dtype, int32_t n, int32_t h, int32_t w,
+                              int32_t pool, int32_t stride, int32_t algo, psc_conv_config* out) {
+    if (psc_status s = check_conv_shape(L, act_dtype, n, h, w, algo, pool != 0, stride)) return s;
+    if (!out) return fail(PSC_ERR_ARG, "out is NULL");
+    const psc::PatTable t = table_of(L);
+    const psc::ConvArgs a = conv_args(L, act_dtype, nullptr, n, h, w, nullptr, 0, nullptr, pool != 0, stride);
+    psc::ConvForm f{};
+    psc::describe_conv(t, a, algo, f);
+    *out = psc_conv_config{f.kernel, f.staged, f.rows_per_lane, f.cols_per_lane, f.segments_per_wave,
+                           f.column_tiles, f.shares, f.filters_per_block, f.blocks, f.threads_per_block};
+    return ok();
 }
 
 psc_status psc_conv3x3_fwd_algo(const psc_layer* L, const psc_packed* pk, int32_t act_dtype,

@@ -1,0 +1,82 @@
+"""CPU checks of the GPU tests' machinery (no device needed):
+
+* the parity gates accept an fp32 summation of the right terms in another
+  order (the oracle's own fp32-accumulating build) and reject the mistakes a
+  kernel could make -- a dropped tap, a doubled tap, a tap read from the
+  neighbouring column -- planted in copies of the oracle's storage;
+* the launch-form search reaches every kernel, load form, rows-per-lane
+  value and epilogue of the tuned conv, and the configuration query
+  validates its arguments."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2003_06513_amd import binding as B
+from synthetic import inputs
+from gpu_cases import check_output, form_cases, host_prepare, max_terms, oracle_ref
+
+
+def _layer(dtype, seed=3, cout=9, cin=30):
+    w = inputs.he_weights(seed, cout, cin, dtype)
+    masks = oracle.select_library(w, 8)
+    _, _, keep, packed = host_prepare(w, masks, inputs.keep_after_drop(cout * cin, 40))
+    x = inputs.normal_activations(seed + 1, (2, cin, 9, 11), dtype)
+    b = inputs.bias_vector(seed + 2, cout, dtype)
+    return w, masks, packed, x, b
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("stride", [1, 2])
+def test_gate_accepts_fp32_sum_in_another_order(dtype, stride):
+    w, masks, packed, x, b = _layer(dtype)
+    ref, s = oracle_ref(x, packed, masks, w.shape[0], bias=b, relu=True, stride=stride)
+    y = oracle.conv_sparse_f32acc(x, packed, masks, w.shape[0], stride, bias=b, relu=True).astype(dtype)
+    check_output(y, ref, s, dtype, max_terms(packed))
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("mistake", ["drop", "double", "shift"])
+def test_gate_rejects_planted_tap_mistakes(dtype, mistake):
+    w, masks, packed, x, b = _layer(dtype, seed=11)
+    cout = w.shape[0]
+    ref, s = oracle_ref(x, packed, masks, cout, bias=b)
+    bad = {k: v.copy() for k, v in packed.items()}
+    k = len(bad["cin_idx"]) // 2
+    if mistake == "drop":
+        bad["values"][4 * k + 1] = 0
+    elif mistake == "double":
+        bad["values"][4 * k + 1] = bad["values"][4 * k + 1] * 2
+    else:
+        # the kernel's pattern replaced by another library pattern (taps at
+        # other positions, same values)
+        bad["pat_id"][k] = (int(bad["pat_id"][k]) + 1) % len(masks)
+    y = oracle.conv_sparse_f32acc(x, bad, masks, cout, 1, bias=b).astype(dtype)
+    with pytest.raises(AssertionError):
+        check_output(y, ref, s, dtype, max_terms(packed))
+
+
+def test_form_search_reaches_every_form():
+    cases = form_cases()
+    keys = [c[0] for c in cases if isinstance(c[0][0], int)]
+    kinds = {(k[0], k[1]) for k in keys}
+    assert {(0, 0), (0, 1), (0, 2), (1, 0), (2, 0)} <= kinds
+    for dt in (B.PSC_F32, B.PSC_F16):
+        assert {k[5] for k in keys if k[0] == 0 and k[6] == dt} == {2, 4, 7, 8}
+        for staged in (0, 1, 2):
+            assert any(k[0] == 0 and k[1] == staged and k[3] and k[6] == dt for k in keys)   # split filters
+            assert any(k[0] == 0 and k[1] == staged and k[4] and k[6] == dt for k in keys)   # pooled epilogue
+    assert any(k[0] == 1 and k[3] for k in keys) and any(k[0] == 1 and k[4] for k in keys)
+    assert any(k[2] for k in keys)                                                         # column tiles
+    assert {c[0][0] for c in cases if not isinstance(c[0][0], int)} == \
+        {"simple-stride2", "simple-algo1", "simple-algo1-pool"}
+
+
+def test_config_query_validates():
+    L = B.Layer(8, 4, [23, 282], 10, B.PSC_F32)
+    for args in [(B.PSC_F16, 1, 8, 8, False, 1, 0), (B.PSC_F32, 1, 8, 8, False, 3, 0),
+                 (B.PSC_F32, 1, 7, 8, True, 1, 0), (B.PSC_F32, 1, 8, 8, True, 2, 0),
+                 (B.PSC_F32, 1, 8, 8, False, 1, 2), (B.PSC_F32, -1, 8, 8, False, 1, 0)]:
+        with pytest.raises(B.PscError):
+            B.conv3x3_config(L, *args)
+    c = B.conv3x3_config(L, B.PSC_F32, 2, 16, 16, False, 2, 0)
+    assert c["kernel"] == 2
