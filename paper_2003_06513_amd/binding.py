@@ -71,6 +71,10 @@ def lib() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         from . import build as _build
         _build.build()
+    # torch ships its own HIP runtime under the same soname as the system's;
+    # load it first so that libpsc binds to the runtime that owns the tensors
+    # and streams it is given (one runtime per process)
+    import torch  # noqa: F401
     try:
         L = ctypes.CDLL(LIB_PATH)
     except OSError as e:
