@@ -121,6 +121,20 @@ psc_status psc_project(const psc_layer *layer, const void *d_w, uint8_t *d_pat,
 psc_status psc_select(const psc_layer *layer, const double *d_energy,
                       uint8_t *d_keep, void *d_ws, size_t ws_bytes, void *stream);
 
+/* For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation: psc_select
+ * without a workspace argument, with the same results.  Its scratch is a
+ * 64 KiB array in the library's device code, one per GPU, held until the
+ * process ends; the call allocates nothing.  Layers of more than
+ * PSC_SELECT_NOALLOC_MAX_KERNELS kernels (cout*cin) return
+ * PSC_ERR_UNSUPPORTED before any HIP call.  Every call on a GPU uses that
+ * GPU's one array: calls whose work may overlap on one GPU (on different
+ * streams, or from concurrent host threads) race, and the caller must order
+ * them.  stream must belong to the current device. */
+#define PSC_SELECT_NOALLOC_MAX_KERNELS 16449536   /* (64 KiB - 1280 B) / 4 B x 1024 */
+psc_status psc_select_noalloc(const psc_layer *layer, const double *d_energy,
+                              uint8_t *d_keep, void *stream);
+
 /* Sec. 3.4: filter kernel reorder + compressed weight storage.  Filters are
  * ordered by (kept-kernel count descending, per-pattern counts
  * lexicographically descending, filter index ascending); values are bit

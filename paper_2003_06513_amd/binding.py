@@ -89,6 +89,7 @@ def lib() -> ctypes.CDLL:
         "psc_workspace_size": ([LP, i32, ctypes.POINTER(sz)], ctypes.c_int),
         "psc_project": ([LP, P, P, P, P], ctypes.c_int),
         "psc_select": ([LP, P, P, P, sz, P], ctypes.c_int),
+        "psc_select_noalloc": ([LP, P, P, P], ctypes.c_int),
         "psc_pack": ([LP, P, P, P, PP, P, sz, P], ctypes.c_int),
         "psc_unpack_dense": ([LP, PP, P, P], ctypes.c_int),
         "psc_conv3x3_fwd": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, P], ctypes.c_int),
@@ -232,6 +233,13 @@ def project(layer: Layer, w, pat, energy, stream=None):
 def select(layer: Layer, energy, keep_mask, ws, stream=None):
     _check(lib().psc_select(layer.ref(), _dev(energy, "energy"), _dev(keep_mask, "keep"),
                             _dev(ws, "ws"), ws.numel(), _stream(stream)), "psc_select")
+
+
+def select_noalloc(layer: Layer, energy, keep_mask, stream=None):
+    """psc_select_noalloc: psc_select with the library's own device scratch
+    (no workspace, no allocation)."""
+    _check(lib().psc_select_noalloc(layer.ref(), _dev(energy, "energy"), _dev(keep_mask, "keep"),
+                                    _stream(stream)), "psc_select_noalloc")
 
 
 def pack(layer: Layer, w, pat, keep_mask, packed: Packed, ws, stream=None):

@@ -37,6 +37,11 @@ size_t select_workspace_bytes(int64_t n_kernels);
 hipError_t launch_select(int64_t n_kernels, int64_t keep, const double* energy, uint8_t* keep_out,
                          void* ws, hipStream_t stream);
 
+// The select workspace kept in the library's device code (allocates nothing):
+// its size, and its address on the current device.
+size_t select_scratch_bytes();
+hipError_t select_scratch(void** out);
+
 // Sec. 3.4
 size_t pack_workspace_bytes(int cout, int m);
 hipError_t launch_pack(const PatTable& tab, int dtype, int cout, int cin, int64_t n_keep, const void* w,

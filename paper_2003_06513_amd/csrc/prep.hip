@@ -3,6 +3,8 @@
 // storage (Sec. 3.4) and the dense unpacker.  All results are integer or bit
 // copies except the fp64 energies, which are sums of exact squares added in a
 // fixed order, so every output is bit-exact and run-to-run deterministic.
+#include <mutex>
+
 #include "common.h"
 #include "launch.h"
 
@@ -429,6 +431,35 @@ hipError_t launch_select(int64_t n, int64_t keep, const double* energy, uint8_t*
     hipLaunchKernelGGL(k_scan_excl_u32, dim3(1), dim3(1024), 0, stream, blk, int64_t(nblk));
     hipLaunchKernelGGL(k_sel_mark, dim3(nblk), dim3(256), 0, stream, keys, n, st, blk, keep_out);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- static scratch
+// The select workspace of the entry point that allocates nothing: one array
+// in the library's device code.  Each GPU holds its own copy at its own
+// address; in host code the array's name is only a stand-in, so kernels get
+// the address hipGetSymbolAddress reports for the current device.
+constexpr size_t kSelScratchBytes = 64 * 1024;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) uint8_t scratch[kSelScratchBytes];
+
+size_t select_scratch_bytes() { return kSelScratchBytes; }
+
+hipError_t select_scratch(void** out) {
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));   // with this device current
+        if (e != hipSuccess) return e;
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return hipSuccess;
 }
 
 // Pack workspace: cnt[cout*m] | nf[cout] | nf_sorted[cout], each 256-aligned.

@@ -231,6 +231,23 @@ psc_status psc_select(const psc_layer* L, const double* d_energy, uint8_t* d_kee
                          "psc_select launch");
 }
 
+psc_status psc_select_noalloc(const psc_layer* L, const double* d_energy, uint8_t* d_keep, void* stream) {
+    if (psc_status s = check_layer(L, true)) return s;
+    if (!d_energy || !d_keep) return fail(PSC_ERR_ARG, "d_energy and d_keep must be non-NULL");
+    const int64_t K = int64_t(L->cout) * L->cin;
+    if (K > PSC_SELECT_NOALLOC_MAX_KERNELS)
+        return fail(PSC_ERR_UNSUPPORTED, "psc_select_noalloc handles at most %d kernels (cout*cin=%lld); "
+                    "use psc_select with a workspace", PSC_SELECT_NOALLOC_MAX_KERNELS, (long long)K);
+    const size_t need = psc::select_workspace_bytes(K);
+    if (need > psc::select_scratch_bytes())
+        return fail(PSC_ERR_INTERNAL, "select scratch of %zu bytes is smaller than the %zu needed",
+                    psc::select_scratch_bytes(), need);
+    void* ws = nullptr;
+    if (psc_status s = device_status(psc::select_scratch(&ws), "psc_select_noalloc scratch address")) return s;
+    return device_status(psc::launch_select(K, L->keep, d_energy, d_keep, ws, as_stream(stream)),
+                         "psc_select_noalloc launch");
+}
+
 psc_status psc_pack(const psc_layer* L, const void* d_w, const uint8_t* d_pat,
                     const uint8_t* d_keep, const psc_packed* out, void* d_ws, size_t ws_bytes,
                     void* stream) {
