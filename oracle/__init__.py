@@ -17,6 +17,8 @@ Mobile Acceleration Framework" (GLSVLSI'20), that it implements:
   conv_sparse     Sec. 4.1   Eq. 1 layer, 3x3 stride 1 pad 1, from the storage
   conv_sparse_strided        the same layer with stride 2 (ResNet stage entries)
   conv_sparse_f32acc         the same loop in fp32 (timed CPU baseline only)
+  conv_sparse_bwd_data   Sec. 3.3  retraining: dx, the adjoint of the Eq. 1 layer
+  conv_sparse_bwd_weight Sec. 3.3  retraining: masked gradient of the stored values, bias
   conv_dense      Sec. 4.1   the same layer as a textbook dense loop (witness)
   maxpool2x2                 2x2/2 max-pool between the VGG-16 layers
 
@@ -76,11 +78,16 @@ def _declare(lib):
                                        P, P, P, P, P, i32, P, i32, i32, P, P]
     lib.pso_conv_sparse_f32acc.argtypes = [P, i32, i32, i32, i32, i32, i32, P,
                                            P, P, P, P, P, i32, P, i32, i32, P]
+    lib.pso_conv_sparse_bwd_data.argtypes = [P, i32, i32, i32, i32, i32, i32, P,
+                                             P, P, P, P, P, i32, P, P]
+    lib.pso_conv_sparse_bwd_weight.argtypes = [P, P, i32, i32, i32, i32, i32, i32, P,
+                                               P, P, P, P, P, P, P]
     lib.pso_conv_dense.argtypes = [P, i32, i32, i32, i32, i32, P, i32, P, i32, P]
     lib.pso_maxpool2x2.argtypes = [P, i64, i32, i32, P]
     for name in ("pso_select_library", "pso_project", "pso_select", "pso_pack",
                  "pso_mask_weights", "pso_unpack", "pso_conv_sparse_st",
-                 "pso_conv_sparse_f32acc", "pso_conv_dense", "pso_maxpool2x2"):
+                 "pso_conv_sparse_f32acc", "pso_conv_sparse_bwd_data", "pso_conv_sparse_bwd_weight",
+                 "pso_conv_dense", "pso_maxpool2x2"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -279,6 +286,52 @@ def bench_num_threads() -> int:
 def bench_set_num_threads(n: int) -> None:
     """Threads the fp32-accumulating baseline build uses from now on."""
     _load_bench().pso_set_num_threads(int(n))
+
+
+def conv_sparse_bwd_data(dy: np.ndarray, packed: dict, masks, cin: int, want_scale: bool = False):
+    """Sec. 3.3 retraining, backpropagation through the Eq. 1 layer (stride 1,
+    pad 1): dx = the adjoint of the pattern-sparse conv applied to dy
+    [n][cout][h][w]; fp64 [n][cin][h][w] (and, with ``want_scale``, the sum
+    of the absolute terms)."""
+    dy = np.ascontiguousarray(dy)
+    n, cout, h, w = (int(d) for d in dy.shape)
+    masks = np.ascontiguousarray(masks, dtype=np.uint16)
+    vals = np.ascontiguousarray(packed["values"])
+    idx = [np.ascontiguousarray(packed[k], dtype=t) for k, t in
+           (("filter_perm", np.int32), ("filter_ptr", np.int32), ("cin_idx", np.int32), ("pat_id", np.uint8))]
+    dy64 = np.ascontiguousarray(dy, dtype=np.float64)
+    dx = np.zeros((n, cin, h, w), dtype=np.float64)
+    s = np.zeros_like(dx) if want_scale else None
+    _check(_load().pso_conv_sparse_bwd_data(
+        _ptr(dy64), n, cin, h, w, cout, len(masks), _ptr(masks), _ptr(idx[0]), _ptr(idx[1]), _ptr(idx[2]),
+        _ptr(idx[3]), _ptr(vals), _dtype_code(vals) if vals.size else F32, _ptr(dx), _ptr(s)),
+        "conv_sparse_bwd_data")
+    return (dx, s) if want_scale else dx
+
+
+def conv_sparse_bwd_weight(x: np.ndarray, dy: np.ndarray, packed: dict, masks, want_scale: bool = False):
+    """Sec. 3.3 retraining: the masked gradient -- dv [keep*4] of the stored
+    values (storage order; pruned weights get none) and db [cout] of the
+    bias -- of the Eq. 1 layer for the output gradient dy; fp64 (and, with
+    ``want_scale``, the sum of the absolute terms of each dv entry)."""
+    x = np.ascontiguousarray(x)
+    dy = np.ascontiguousarray(dy)
+    n, cin, h, w = (int(d) for d in x.shape)
+    cout = int(dy.shape[1])
+    if dy.shape != (n, cout, h, w):
+        raise ValueError("dy must be [n][cout][h][w] of the layer's input size")
+    masks = np.ascontiguousarray(masks, dtype=np.uint16)
+    idx = [np.ascontiguousarray(packed[k], dtype=t) for k, t in
+           (("filter_perm", np.int32), ("filter_ptr", np.int32), ("cin_idx", np.int32), ("pat_id", np.uint8))]
+    keep = int(idx[2].size)
+    dv = np.zeros(keep * 4, dtype=np.float64)
+    s = np.zeros_like(dv) if want_scale else None
+    db = np.zeros(cout, dtype=np.float64)
+    _check(_load().pso_conv_sparse_bwd_weight(
+        _ptr(np.ascontiguousarray(x, dtype=np.float64)), _ptr(np.ascontiguousarray(dy, dtype=np.float64)),
+        n, cin, h, w, cout, len(masks), _ptr(masks), _ptr(idx[0]), _ptr(idx[1]), _ptr(idx[2]), _ptr(idx[3]),
+        _ptr(dv), _ptr(s), _ptr(db)), "conv_sparse_bwd_weight")
+    return (dv, db, s) if want_scale else (dv, db)
 
 
 def conv_dense(x: np.ndarray, wdense: np.ndarray, bias=None, relu: bool = False):

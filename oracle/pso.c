@@ -22,6 +22,9 @@
  *                       pruned ResNets)                      (Sec. 4.1, Eq. 1)
  *   pso_conv_sparse_f32acc  the same loop accumulating in fp32
  *                       (timed CPU baseline only)
+ *   pso_conv_sparse_bwd_data    dx: adjoint of Eq. 1 (retraining)   (Sec. 3.3)
+ *   pso_conv_sparse_bwd_weight  masked gradient of the stored values
+ *                       and of the bias (retraining)         (Sec. 3.3)
  *   pso_conv_dense      textbook dense direct convolution of
  *                       zero-masked OIHW weights (witness)   (Sec. 4.1, Eq. 1)
  *   pso_maxpool2x2      2x2/2 max-pool between VGG-16 layers
@@ -549,6 +552,149 @@ int pso_conv_sparse_f32acc(const float *x, int n, int cin, int h, int w,
         for (size_t q = 0; q < oplane; ++q) {
             float v = yp[q] + b;
             yp[q] = (relu && v < 0.0f) ? 0.0f : v;
+        }
+    }
+    return bad ? -1 : 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Retraining (Sec. 3.3): the user retrains the pruned model with the pruned
+ * weights' gradients set to zero.  For the layer of Eq. 1 (stride 1, zero
+ * padding 1) with loss gradient dy = dL/dy (taken after sigma), these are
+ * the two products of backpropagation through the linear part:
+ *
+ *   dx[n,ci,i,j] = sum over kept kernels (f, ci, p) of sum_t v_t *
+ *                  dy[n, f, i - r_t + 1, j - s_t + 1]          (adjoint of Eq. 1)
+ *   dv[k,t]      = sum over n, i, j of dy[n, f, i, j] * x[n, ci, i + r_t - 1, j + s_t - 1]
+ *   db[f]        = sum over n, i, j of dy[n, f, i, j]
+ *
+ * dv holds the gradient of the 4 stored values of every kept kernel k (in
+ * storage order): the masked gradient, nothing for pruned weights.  Terms
+ * outside the image are absent.  Inputs are double (widened exactly).  dx
+ * is summed per (image, input channel) over the kernels in storage order;
+ * s, if non-null, receives the sum of the absolute terms. */
+int pso_conv_sparse_bwd_data(const double *dy, int n, int cin, int h, int w,
+                             int cout, int m, const uint16_t *masks,
+                             const int32_t *filter_perm, const int32_t *filter_ptr,
+                             const int32_t *cin_idx, const uint8_t *pat_id,
+                             const void *values, int vdtype, double *dx, double *s)
+{
+    if (n < 0 || cin < 0 || h < 1 || w < 1 || cout < 0 || m < 1 || m > 126)
+        return -1;
+    const size_t plane = (size_t)h * w;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t t = 0; t < (int64_t)n * cin; ++t) {
+        int nn = (int)(t / cin);
+        int ci = (int)(t % cin);
+        double *xp = dx + ((size_t)nn * cin + ci) * plane;
+        double *sp = s ? s + ((size_t)nn * cin + ci) * plane : NULL;
+        for (size_t q = 0; q < plane; ++q) {
+            xp[q] = 0.0;
+            if (sp)
+                sp[q] = 0.0;
+        }
+        for (int i = 0; i < cout; ++i) {
+            int f = filter_perm[i];
+            const double *yp = dy + ((size_t)nn * cout + f) * plane;
+            for (int32_t k = filter_ptr[i]; k < filter_ptr[i + 1]; ++k) {
+                if (cin_idx[k] != ci)
+                    continue;
+                int p = pat_id[k];
+                if (p >= m) {
+                    bad = 1;
+                    continue;
+                }
+                int j = 0;
+                for (int q = 0; q < 9; ++q) {
+                    if (!((masks[p] >> q) & 1))
+                        continue;
+                    int r = q / 3, c = q % 3;
+                    double v = elem(values, vdtype, (size_t)k * 4 + j);
+                    j += 1;
+                    /* dx[i0, j0] += v * dy[i0 - r + 1, j0 - c + 1] */
+                    for (int i0 = 0; i0 < h; ++i0) {
+                        int oi = i0 - r + 1;
+                        if (oi < 0 || oi >= h)
+                            continue;
+                        for (int j0 = 0; j0 < w; ++j0) {
+                            int oj = j0 - c + 1;
+                            if (oj < 0 || oj >= w)
+                                continue;
+                            double prod = v * yp[(size_t)oi * w + oj];
+                            xp[(size_t)i0 * w + j0] += prod;
+                            if (sp)
+                                sp[(size_t)i0 * w + j0] += fabs(prod);
+                        }
+                    }
+                }
+            }
+        }
+    }
+    return bad ? -1 : 0;
+}
+
+/* dv (keep*4 doubles, storage order) and, if non-null, db (cout doubles,
+ * original filter order); s_dv, if non-null, receives the sum of the
+ * absolute terms of each dv entry.  Each entry is summed over images, then
+ * rows, then columns. */
+int pso_conv_sparse_bwd_weight(const double *x, const double *dy, int n, int cin, int h, int w,
+                               int cout, int m, const uint16_t *masks,
+                               const int32_t *filter_perm, const int32_t *filter_ptr,
+                               const int32_t *cin_idx, const uint8_t *pat_id,
+                               double *dv, double *s_dv, double *db)
+{
+    if (n < 0 || cin < 0 || h < 1 || w < 1 || cout < 0 || m < 1 || m > 126)
+        return -1;
+    const size_t plane = (size_t)h * w;
+    int bad = 0;
+    for (int i = 0; i < cout; ++i) {
+        int f = filter_perm[i];
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int32_t k = filter_ptr[i]; k < filter_ptr[i + 1]; ++k) {
+            int ci = cin_idx[k];
+            int p = pat_id[k];
+            if (p >= m || ci < 0 || ci >= cin) {
+                bad = 1;
+                continue;
+            }
+            int j = 0;
+            for (int q = 0; q < 9; ++q) {
+                if (!((masks[p] >> q) & 1))
+                    continue;
+                int r = q / 3, c = q % 3;
+                double acc = 0.0, sacc = 0.0;
+                for (int nn = 0; nn < n; ++nn) {
+                    const double *yp = dy + ((size_t)nn * cout + f) * plane;
+                    const double *xc = x + ((size_t)nn * cin + ci) * plane;
+                    for (int oi = 0; oi < h; ++oi) {
+                        int ii = oi + r - 1;
+                        if (ii < 0 || ii >= h)
+                            continue;
+                        for (int oj = 0; oj < w; ++oj) {
+                            int ij = oj + c - 1;
+                            if (ij < 0 || ij >= w)
+                                continue;
+                            double prod = yp[(size_t)oi * w + oj] * xc[(size_t)ii * w + ij];
+                            acc += prod;
+                            sacc += fabs(prod);
+                        }
+                    }
+                }
+                dv[(size_t)k * 4 + j] = acc;
+                if (s_dv)
+                    s_dv[(size_t)k * 4 + j] = sacc;
+                j += 1;
+            }
+        }
+    }
+    if (db) {
+        for (int f = 0; f < cout; ++f) {
+            double acc = 0.0;
+            for (int nn = 0; nn < n; ++nn)
+                for (size_t q = 0; q < plane; ++q)
+                    acc += dy[((size_t)nn * cout + f) * plane + q];
+            db[f] = acc;
         }
     }
     return bad ? -1 : 0;

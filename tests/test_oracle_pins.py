@@ -527,3 +527,75 @@ def test_conv_f32acc_baseline_close_to_fp64(stride, dtype):
     y32 = oracle.conv_sparse_f32acc(x, packed, masks, cout, stride, bias=b, relu=True)
     nterms = 4 * cin + 1
     assert (np.abs(y32 - y) <= nterms * 2.0 ** -24 * s + 1e-30).all()
+
+
+# ------------------------------------------- retraining (Sec. 3.3): backward
+@pytest.mark.parametrize("n,cin,cout,h,w", [(2, 5, 7, 9, 11), (1, 3, 4, 1, 1), (1, 6, 5, 2, 3), (3, 8, 6, 7, 6)])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_backward_equals_torch_autograd(n, cin, cout, h, w, dtype):
+    """dx, the masked dv and db equal torch autograd (fp64, CPU) of
+    conv2d(x, masked weights, bias) against the output gradient dy; the
+    weight gradient at pruned positions is what the retraining function
+    zeroes, so only the kept positions are compared (all of them)."""
+    torch = pytest.importorskip("torch")
+    wt, masks, pat, keep, packed = _prepared(cin * 13 + cout, cout, cin, 8, 40, dtype)
+    x = inputs.normal_activations(21, (n, cin, h, w), dtype)
+    dy = inputs.normal_activations(22, (n, cout, h, w), dtype)
+    masked = oracle.mask_weights(wt, masks, pat, keep).astype(np.float64)
+    xt = torch.from_numpy(x.astype(np.float64)).requires_grad_(True)
+    wt_t = torch.from_numpy(masked).requires_grad_(True)
+    bt = torch.zeros(cout, dtype=torch.float64, requires_grad=True)
+    y = torch.nn.functional.conv2d(xt, wt_t, bt, padding=1)
+    (y * torch.from_numpy(dy.astype(np.float64))).sum().backward()
+    dx = oracle.conv_sparse_bwd_data(dy, packed, masks, cin)
+    dv, db = oracle.conv_sparse_bwd_weight(x, dy, packed, masks)
+    sc = max(1.0, float(xt.grad.abs().max()))
+    assert float(np.abs(dx - xt.grad.numpy()).max()) <= 1e-12 * sc
+    # dv scattered to the kept positions of a dense array
+    gp = dict(packed)
+    gp["values"] = dv
+    dense = np.zeros((cout, cin, 3, 3))
+    for i, f in enumerate(packed["filter_perm"]):
+        for k in range(packed["filter_ptr"][i], packed["filter_ptr"][i + 1]):
+            pos = [q for q in range(9) if (int(masks[packed["pat_id"][k]]) >> q) & 1]
+            for j, q in enumerate(pos):
+                dense[f, packed["cin_idx"][k], q // 3, q % 3] = dv[4 * k + j]
+    kept = masked != 0
+    kept |= oracle.mask_weights(np.ones_like(wt), masks, pat, keep).astype(bool)
+    sw = max(1.0, float(wt_t.grad.abs().max()))
+    assert float(np.abs(dense - np.where(kept, wt_t.grad.numpy(), 0.0)).max()) <= 1e-12 * sw
+    assert float(np.abs(db - bt.grad.numpy()).max()) <= 1e-12 * max(1.0, float(bt.grad.abs().max()))
+
+
+def test_backward_adjoint_and_linearity_identities():
+    """<conv(x), dy> = <x, dx(dy)> (dx is the adjoint), and since the layer is
+    linear in its stored values, moving one value by e changes <conv(x), dy>
+    by e * dv of that value (brute force through the forward oracle)."""
+    cin, cout, h, w = 6, 5, 7, 8
+    wt, masks, pat, keep, packed = _prepared(71, cout, cin, 6, 30)
+    x = inputs.normal_activations(31, (2, cin, h, w))
+    dy = inputs.normal_activations(32, (2, cout, h, w))
+    y = oracle.conv_sparse(x, packed, masks, cout)
+    dx = oracle.conv_sparse_bwd_data(dy, packed, masks, cin)
+    lhs, rhs = float((y * dy.astype(np.float64)).sum()), float((x.astype(np.float64) * dx).sum())
+    assert abs(lhs - rhs) <= 1e-12 * (abs(lhs) + 1.0)
+    dv, _ = oracle.conv_sparse_bwd_weight(x, dy, packed, masks)
+    rng = np.random.default_rng(5)
+    for e in rng.choice(len(dv), size=6, replace=False):
+        p2 = {k: v.copy() for k, v in packed.items()}
+        p2["values"][e] += np.float32(0.5)
+        step = float(p2["values"][e]) - float(packed["values"][e])   # the fp32 step actually taken
+        y2 = oracle.conv_sparse(x, p2, masks, cout)
+        delta = float(((y2 - y) * dy.astype(np.float64)).sum())
+        assert abs(delta - step * dv[e]) <= 1e-10 * (abs(dv[e]) + 1.0)
+
+
+def test_backward_scales_bound_values():
+    cin, cout = 5, 4
+    wt, masks, pat, keep, packed = _prepared(81, cout, cin, 8, 20)
+    x = inputs.normal_activations(41, (2, cin, 6, 5))
+    dy = inputs.normal_activations(42, (2, cout, 6, 5))
+    dx, s = oracle.conv_sparse_bwd_data(dy, packed, masks, cin, want_scale=True)
+    assert (np.abs(dx) <= s * (1 + 1e-12)).all()
+    dv, db, sv = oracle.conv_sparse_bwd_weight(x, dy, packed, masks, want_scale=True)
+    assert (np.abs(dv) <= sv * (1 + 1e-12)).all() and (sv > 0).all()
