@@ -199,6 +199,47 @@ psc_status psc_conv3x3_fwd_strided(const psc_layer *layer, const psc_packed *pac
                                    int32_t relu, void *d_y, int32_t stride, int32_t algo,
                                    void *stream);
 
+/* ---- Retraining (Sec. 3.3): the user retrains the pruned model like a
+ * dense one, except that the gradients of pruned weights are zero.  For the
+ * layer y = W x of psc_conv3x3_fwd (before sigma; dy is the gradient at
+ * that point):
+ *
+ *   dx = W^T dy  is a pattern-sparse 3x3 convolution of dy by the transposed
+ *                layer: filter ci, input channel f, every kernel rotated by
+ *                180 degrees.  psc_transpose_layer describes that layer (a
+ *                rotated 4-of-9 mask is a 4-of-9 mask, library order kept),
+ *                psc_transpose_prep writes its dense weights, pattern ids
+ *                and keep mask, psc_pack packs it, and psc_conv3x3_fwd (or
+ *                _algo) on dy gives dx;
+ *   dv, db       are the masked gradient: psc_conv3x3_bwd_weight. */
+
+/* Host only: *out = the transposed layer of *layer (cout and cin swapped,
+ * masks[p] rotated: bit q -> bit 8-q, same keep and dtype). */
+psc_status psc_transpose_layer(const psc_layer *layer, psc_layer *out);
+
+/* The transposed layer's dense inputs to psc_pack: for kernel k = f*cin+ci
+ * of layer, kt = ci*cout+f, d_w_t[kt][q] = d_w[k][8-q] (bit copies, OIHW of
+ * the transposed layer), d_pat_t[kt] = d_pat[k], d_keep_t[kt] = d_keep[k].
+ * Outputs must not overlap inputs. */
+psc_status psc_transpose_prep(const psc_layer *layer, const void *d_w, const uint8_t *d_pat,
+                              const uint8_t *d_keep, void *d_w_t, uint8_t *d_pat_t,
+                              uint8_t *d_keep_t, void *stream);
+
+/* The masked weight gradient of the layer for output gradient d_dy
+ * ([n][cout][h][w], act_dtype; d_x [n][cin][h][w] the layer's input):
+ *   d_dvalues[4k+t] = sum over images and pixels (i, j) of
+ *                     dy[n, f, i, j] * x[n, ci, i + r_t - 1, j + s_t - 1]
+ * for every kept kernel k of the storage (filter f, channel ci, t-th kept
+ * position (r_t, s_t)), and, if d_dbias is non-NULL,
+ *   d_dbias[f] = sum over images and pixels of dy[n, f].
+ * Outputs are fp32 (fp32 accumulation for both activation dtypes), written
+ * in full; d_dvalues [keep*4] must be 16-byte aligned, d_dbias is [cout] in
+ * the original filter order.  Stride 1, zero padding 1. */
+psc_status psc_conv3x3_bwd_weight(const psc_layer *layer, const psc_packed *packed,
+                                  int32_t act_dtype, const void *d_x, const void *d_dy,
+                                  int32_t n, int32_t h, int32_t w, float *d_dvalues,
+                                  float *d_dbias, void *stream);
+
 /* The launch configuration the conv entry points would use for a call with
  * these arguments: which kernel runs and how work maps onto it.  Host only,
  * no device work; arguments are validated as by psc_conv3x3_fwd_strided

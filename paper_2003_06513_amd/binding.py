@@ -98,6 +98,9 @@ def lib() -> ctypes.CDLL:
         "psc_conv3x3_fwd_strided": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, i32, P], ctypes.c_int),
         "psc_conv3x3_config": ([LP, i32, i32, i32, i32, i32, i32, i32, ctypes.POINTER(CConvConfig)],
                                ctypes.c_int),
+        "psc_transpose_layer": ([LP, LP], ctypes.c_int),
+        "psc_transpose_prep": ([LP, P, P, P, P, P, P, P], ctypes.c_int),
+        "psc_conv3x3_bwd_weight": ([LP, PP, i32, P, P, i32, i32, i32, P, P, P], ctypes.c_int),
         "psc_dense3x3_fwd": ([i32, P, i32, i32, i32, i32, P, i32, P, i32, P, P], ctypes.c_int),
         "psc_maxpool2x2": ([i32, P, i32, i32, i32, i32, P, P], ctypes.c_int),
     }
@@ -320,6 +323,29 @@ def maxpool2x2(x, y, stream=None):
            "psc_maxpool2x2")
 
 
+def transpose_layer(layer: Layer) -> Layer:
+    """psc_transpose_layer: the layer of dx = W^T dy (host only)."""
+    out = CLayer()
+    _check(lib().psc_transpose_layer(layer.ref(), ctypes.byref(out)), "psc_transpose_layer")
+    return Layer(out.cout, out.cin, [out.masks[i] for i in range(out.m)], out.keep, out.wdtype)
+
+
+def transpose_prep(layer: Layer, w, pat, keep_mask, w_t, pat_t, keep_t, stream=None):
+    _check(lib().psc_transpose_prep(layer.ref(), _dev(w, "w"), _dev(pat, "pat"), _dev(keep_mask, "keep"),
+                                    _dev(w_t, "w_t"), _dev(pat_t, "pat_t"), _dev(keep_t, "keep_t"),
+                                    _stream(stream)), "psc_transpose_prep")
+
+
+def conv3x3_bwd_weight(layer: Layer, packed: Packed, x, dy, dvalues, dbias=None, stream=None):
+    n, cin, h, w = (int(d) for d in x.shape)
+    if cin != layer.cin or tuple(dy.shape) != (n, layer.cout, h, w) or dvalues.numel() != 4 * layer.keep:
+        raise ValueError("x/dy/dvalues shapes do not match the layer")
+    cp = packed.c()
+    _check(lib().psc_conv3x3_bwd_weight(layer.ref(), ctypes.byref(cp), dtype_code(x), _dev(x, "x"), _dev(dy, "dy"),
+                                        n, h, w, _dev(dvalues, "dvalues"), _dev(dbias, "dbias"), _stream(stream)),
+           "psc_conv3x3_bwd_weight")
+
+
 # ------------------------------------------------------------------ conveniences
 class Prepared:
     """A pruned, packed layer: the result of project -> select -> pack."""
@@ -350,6 +376,25 @@ def prepare(w, masks, keep: int, stream=None) -> Prepared:
     select(layer, energy, keep_mask, ws_sel, stream)
     pack(layer, w, pat, keep_mask, packed, ws_pack, stream)
     return Prepared(layer, packed, pat, energy, keep_mask, (ws_sel, ws_pack))
+
+
+def prepare_transposed(prep: Prepared, w, stream=None) -> Prepared:
+    """The packed transposed layer of a prepared one (for dx = W^T dy):
+    psc_transpose_prep on its dense weights ``w``, pattern ids and keep mask,
+    then psc_pack with the rotated library."""
+    torch = _torch()
+    lt = transpose_layer(prep.layer)
+    K = lt.cout * lt.cin
+    w_t = torch.empty((lt.cout, lt.cin, 3, 3), dtype=w.dtype, device=w.device)
+    pat_t = torch.empty(K, dtype=torch.uint8, device=w.device)
+    keep_t = torch.empty(K, dtype=torch.uint8, device=w.device)
+    transpose_prep(prep.layer, w, prep.pat, prep.keep_mask, w_t, pat_t, keep_t, stream)
+    packed = Packed(lt, w.device)
+    ws = workspace(lt, PSC_OP_PACK, w.device)
+    pack(lt, w_t, pat_t, keep_t, packed, ws, stream)
+    out = Prepared(lt, packed, pat_t, None, keep_t, (ws,))
+    out.w = w_t
+    return out
 
 
 def conv(prep: Prepared, x, bias=None, relu: bool = False, algo: int = 0, out=None, stream=None):

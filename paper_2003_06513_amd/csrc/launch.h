@@ -73,6 +73,15 @@ struct ConvForm {
     int shares, filters_per_block, blocks, threads_per_block;
 };
 void describe_conv(const PatTable& tab, const ConvArgs& a, int algo, ConvForm& out);
+// Sec. 3.3 retraining: the transposed, rotated layer (for dx) and the masked
+// weight gradient.
+hipError_t launch_transpose_prep(int dtype, int cout, int cin, const void* w, const uint8_t* pat,
+                                 const uint8_t* keep, void* wt, uint8_t* pat_t, uint8_t* keep_t,
+                                 hipStream_t stream);
+hipError_t launch_bwd_weight(const PatTable& tab, const PackedView& pk, int dtype, int n, int cin, int h, int w,
+                             int cout, int64_t keep, const void* x, const void* dy, float* dv, float* db,
+                             hipStream_t stream);
+
 hipError_t launch_dense(int dtype, const void* x, int n, int cin, int h, int w, const void* wd,
                         int cout, const void* bias, int relu, void* y, hipStream_t stream);
 hipError_t launch_maxpool(int dtype, const void* x, int n, int c, int h, int w, void* y,

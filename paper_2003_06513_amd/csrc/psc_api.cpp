@@ -368,6 +368,57 @@ psc_status psc_conv3x3_fwd_strided(const psc_layer* L, const psc_packed* pk, int
     return conv_common(L, pk, act_dtype, d_x, n, h, w, d_bias, relu, d_y, algo, 0, stride, stream);
 }
 
+psc_status psc_transpose_layer(const psc_layer* L, psc_layer* out) {
+    if (psc_status s = check_layer(L, true)) return s;
+    if (!out) return fail(PSC_ERR_ARG, "out is NULL");
+    psc_layer t;
+    std::memset(&t, 0, sizeof t);
+    t.cout = L->cin;
+    t.cin = L->cout;
+    t.m = L->m;
+    t.wdtype = L->wdtype;
+    t.keep = L->keep;
+    for (int p = 0; p < L->m; ++p) {
+        unsigned r = 0;
+        for (int q = 0; q < 9; ++q)
+            if ((L->masks[p] >> q) & 1u) r |= 1u << (8 - q);   // rotated by 180 degrees
+        t.masks[p] = uint16_t(r);
+    }
+    if (t.cout > 65535) return fail(PSC_ERR_UNSUPPORTED, "cin=%d: the transposed layer needs cin <= 65535", L->cin);
+    *out = t;
+    return ok();
+}
+
+psc_status psc_transpose_prep(const psc_layer* L, const void* d_w, const uint8_t* d_pat, const uint8_t* d_keep,
+                              void* d_w_t, uint8_t* d_pat_t, uint8_t* d_keep_t, void* stream) {
+    if (psc_status s = check_layer(L, true)) return s;
+    if (!d_w || !d_pat || !d_keep || !d_w_t || !d_pat_t || !d_keep_t)
+        return fail(PSC_ERR_ARG, "every pointer must be non-NULL");
+    const size_t K = size_t(L->cout) * L->cin;
+    if (overlaps(d_w, K * 9 * elt_size(L->wdtype), d_w_t, K * 9 * elt_size(L->wdtype)) ||
+        overlaps(d_pat, K, d_pat_t, K) || overlaps(d_keep, K, d_keep_t, K))
+        return fail(PSC_ERR_ARG, "outputs must not overlap inputs");
+    return device_status(psc::launch_transpose_prep(L->wdtype, L->cout, L->cin, d_w, d_pat, d_keep, d_w_t, d_pat_t,
+                                                    d_keep_t, as_stream(stream)),
+                         "psc_transpose_prep launch");
+}
+
+psc_status psc_conv3x3_bwd_weight(const psc_layer* L, const psc_packed* pk, int32_t act_dtype, const void* d_x,
+                                  const void* d_dy, int32_t n, int32_t h, int32_t w, float* d_dvalues,
+                                  float* d_dbias, void* stream) {
+    if (psc_status s = check_conv_shape(L, act_dtype, n, h, w, 0, 0, 1)) return s;
+    if (psc_status s = check_packed(L, pk)) return s;
+    if (n == 0) return ok();
+    if (!d_x || !d_dy) return fail(PSC_ERR_ARG, "d_x and d_dy must be non-NULL");
+    if (L->keep > 0 && !d_dvalues) return fail(PSC_ERR_ARG, "d_dvalues must be non-NULL when keep > 0");
+    if (reinterpret_cast<uintptr_t>(d_dvalues) & 15u) return fail(PSC_ERR_ARG, "d_dvalues must be 16-byte aligned");
+    const psc::PatTable t = table_of(L);
+    const psc::PackedView v{pk->filter_perm, pk->filter_ptr, pk->seg_ptr, pk->cin_idx, pk->pat_id, pk->values};
+    return device_status(psc::launch_bwd_weight(t, v, act_dtype, n, L->cin, h, w, L->cout, L->keep, d_x, d_dy,
+                                                d_dvalues, d_dbias, as_stream(stream)),
+                         "psc_conv3x3_bwd_weight launch");
+}
+
 psc_status psc_dense3x3_fwd(int32_t dtype, const void* d_x, int32_t n, int32_t cin, int32_t h,
                             int32_t w, const void* d_w, int32_t cout, const void* d_bias,
                             int32_t relu, void* d_y, void* stream) {

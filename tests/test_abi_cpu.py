@@ -164,3 +164,24 @@ def test_dense_and_pool_validation(L):
     assert L.psc_dense3x3_fwd(0, FAKE, 1, 0, 4, 4, FAKE, 2, None, 0, FAKE, None) == B.PSC_ERR_ARG
     assert L.psc_maxpool2x2(0, FAKE, 1, 2, 5, 4, FAKE, None) == B.PSC_ERR_ARG
     assert L.psc_maxpool2x2(0, None, 1, 2, 4, 4, FAKE, None) == B.PSC_ERR_ARG
+
+
+def test_transpose_layer_rotates_masks_and_is_an_involution():
+    L = B.Layer(6, 9, [23, 282, 58, 90, 113], 20, B.PSC_F16)
+    T = B.transpose_layer(L)
+    assert (T.cout, T.cin, T.keep, T.dtype) == (9, 6, 20, B.PSC_F16)
+    for a, b in zip(L.masks, T.masks):
+        assert all(((int(a) >> q) & 1) == ((int(b) >> (8 - q)) & 1) for q in range(9))
+    TT = B.transpose_layer(T)
+    assert np.array_equal(TT.masks, L.masks) and (TT.cout, TT.cin) == (6, 9)
+
+
+def test_bwd_weight_validates(L):
+    lay = _layer()
+    pk = B.CPacked()
+    for n_ in B.PACKED_FIELDS:
+        setattr(pk, n_, 0x10000)
+    import ctypes
+    rc = L.psc_conv3x3_bwd_weight(lay.ref(), ctypes.byref(pk), B.PSC_F32, FAKE, FAKE, 1, 4, 4,
+                                  ctypes.c_void_p(0x10004), None, None)
+    assert rc == B.PSC_ERR_ARG and "16-byte" in B.last_error()
