@@ -50,10 +50,14 @@ def dense_weight_grad(x: np.ndarray, g: np.ndarray):
     n, cin, h, w = x.shape
     xp = np.zeros((n, cin, h + 2, w + 2))
     xp[:, :, 1:h + 1, 1:w + 1] = x
-    dw = np.zeros((g.shape[1], cin, 3, 3))
-    for r in range(3):
-        for s in range(3):
-            dw[:, :, r, s] = np.tensordot(g, xp[:, :, r:r + h, s:s + w], axes=([0, 2, 3], [0, 2, 3]))
+    cout = g.shape[1]
+    dw = np.zeros((cout, cin, 3, 3))
+    for img in range(n):
+        gm = g[img].reshape(cout, h * w)                      # [o][(h, w)]
+        for r in range(3):
+            for s in range(3):
+                xs = xp[img, :, r:r + h, s:s + w].reshape(cin, h * w)   # [i][(h, w)], shifted
+                dw[:, :, r, s] += gm @ xs.T
     return dw, g.sum(axis=(0, 2, 3))
 
 
