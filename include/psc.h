@@ -240,6 +240,49 @@ psc_status psc_conv3x3_bwd_weight(const psc_layer *layer, const psc_packed *pack
                                   int32_t n, int32_t h, int32_t w, float *d_dvalues,
                                   float *d_dbias, void *stream);
 
+/* ---- Data-free ADMM pattern pruning of one layer (Sec. 4.3, Eq. 4-7;
+ * Algorithm 1).  With input X (synthetic data), pre-trained W0, b0 and
+ * target X' = relu(W0 X + b0) (psc_dense3x3_fwd with relu), an iteration is
+ *   Z = W X + b                           psc_dense3x3_fwd, relu off
+ *   G, loss = c ||relu(Z) - X'||^2        psc_admm_residual
+ *   dW, db                                psc_dense3x3_bwd_weight
+ *   W -= lr (dW + rho (W - A + D)),
+ *   b -= lr db, V = W + D                 psc_admm_primal            (Eq. 4)
+ *   pattern ids + energies of V           psc_project                (Eq. 6)
+ *   keep mask (beta kernels)              psc_select or _noalloc     (Sec. 4.4)
+ *   A = V on the kept pattern positions,
+ *   0 elsewhere; D = V - A                psc_admm_dual        (Eq. 6, Eq. 7)
+ * starting from A = W0, D = 0.  All tensors fp32, weights OIHW, activations
+ * NCHW, each rounding as written (the loss sums in fp64). */
+
+/* G[i] = 2 scale (relu(z[i]) - t[i]) if z[i] > 0, else 0; *d_loss (device
+ * double) = scale * sum (relu(z) - t)^2, summed in fp64 in a fixed order.
+ * d_ws: PSC_ADMM_RESIDUAL_WS_BYTES bytes, 256-byte aligned, caller-owned. */
+#define PSC_ADMM_RESIDUAL_WS_BYTES 8192
+psc_status psc_admm_residual(const float *d_z, const float *d_target, int64_t numel, float scale,
+                             float *d_g, double *d_loss, void *d_ws, size_t ws_bytes, void *stream);
+
+/* The dense weight gradient of the 3x3 layer (stride 1, zero padding 1):
+ *   d_dw[o][i][r][s] = sum over images and pixels of
+ *                      g[n, o, h, w] * x[n, i, h + r - 1, w + s - 1]
+ * and, if d_db is non-NULL, d_db[o] = sum of g[n, o, :, :]; fp32. */
+psc_status psc_dense3x3_bwd_weight(const float *d_x, const float *d_g, int32_t n, int32_t cin,
+                                   int32_t h, int32_t w, int32_t cout, float *d_dw, float *d_db,
+                                   void *stream);
+
+/* Eq. 4, one SGD step, in place: for each of the n_weights entries
+ *   W = W - lr * (dW + rho * ((W - A) + D)),   V = W + D;
+ * and, if d_b is non-NULL, b[o] = b[o] - lr * db[o] for o < cout. */
+psc_status psc_admm_primal(int64_t n_weights, float *d_w, const float *d_dw, const float *d_a,
+                           const float *d_d, int32_t cout, float *d_b, const float *d_db,
+                           float lr, float rho, float *d_v, void *stream);
+
+/* Eq. 6-7 given the projection's choices for V (d_pat from psc_project on
+ * V, d_keep from psc_select): A = V at the positions of kept kernels' chosen
+ * patterns, +0 elsewhere; D = V - A.  layer->wdtype must be PSC_F32. */
+psc_status psc_admm_dual(const psc_layer *layer, const float *d_v, const uint8_t *d_pat,
+                         const uint8_t *d_keep, float *d_a, float *d_d, void *stream);
+
 /* The launch configuration the conv entry points would use for a call with
  * these arguments: which kernel runs and how work maps onto it.  Host only,
  * no device work; arguments are validated as by psc_conv3x3_fwd_strided

@@ -101,6 +101,10 @@ def lib() -> ctypes.CDLL:
         "psc_transpose_layer": ([LP, LP], ctypes.c_int),
         "psc_transpose_prep": ([LP, P, P, P, P, P, P, P], ctypes.c_int),
         "psc_conv3x3_bwd_weight": ([LP, PP, i32, P, P, i32, i32, i32, P, P, P], ctypes.c_int),
+        "psc_admm_residual": ([P, P, i64, ctypes.c_float, P, P, P, sz, P], ctypes.c_int),
+        "psc_dense3x3_bwd_weight": ([P, P, i32, i32, i32, i32, i32, P, P, P], ctypes.c_int),
+        "psc_admm_primal": ([i64, P, P, P, P, i32, P, P, ctypes.c_float, ctypes.c_float, P, P], ctypes.c_int),
+        "psc_admm_dual": ([LP, P, P, P, P, P, P], ctypes.c_int),
         "psc_dense3x3_fwd": ([i32, P, i32, i32, i32, i32, P, i32, P, i32, P, P], ctypes.c_int),
         "psc_maxpool2x2": ([i32, P, i32, i32, i32, i32, P, P], ctypes.c_int),
     }
@@ -344,6 +348,111 @@ def conv3x3_bwd_weight(layer: Layer, packed: Packed, x, dy, dvalues, dbias=None,
     _check(lib().psc_conv3x3_bwd_weight(layer.ref(), ctypes.byref(cp), dtype_code(x), _dev(x, "x"), _dev(dy, "dy"),
                                         n, h, w, _dev(dvalues, "dvalues"), _dev(dbias, "dbias"), _stream(stream)),
            "psc_conv3x3_bwd_weight")
+
+
+ADMM_RESIDUAL_WS_BYTES = 8192
+
+
+def _f32(t, name):
+    torch = _torch()
+    if t is not None and t.dtype != torch.float32:
+        raise TypeError("%s must be float32" % name)
+    return _dev(t, name)
+
+
+def admm_residual(z, target, scale: float, g, loss, ws, stream=None):
+    """psc_admm_residual: g = 2 scale (relu(z) - t) [z > 0], loss (a float64
+    device scalar) = scale * sum (relu(z) - t)^2."""
+    if z.shape != target.shape or z.shape != g.shape:
+        raise ValueError("z, target and g must have one shape")
+    _check(lib().psc_admm_residual(_f32(z, "z"), _f32(target, "target"), int(z.numel()), float(scale),
+                                   _f32(g, "g"), _dev(loss, "loss"), _dev(ws, "ws"), int(ws.numel()),
+                                   _stream(stream)), "psc_admm_residual")
+
+
+def dense3x3_bwd_weight(x, g, dw, db=None, stream=None):
+    n, cin, h, w = (int(d) for d in x.shape)
+    cout = int(g.shape[1])
+    if tuple(g.shape) != (n, cout, h, w) or tuple(dw.shape) != (cout, cin, 3, 3):
+        raise ValueError("x/g/dw shapes do not match")
+    _check(lib().psc_dense3x3_bwd_weight(_f32(x, "x"), _f32(g, "g"), n, cin, h, w, cout, _f32(dw, "dw"),
+                                         _f32(db, "db"), _stream(stream)), "psc_dense3x3_bwd_weight")
+
+
+def admm_primal(w, dw, a, d, b, db, lr: float, rho: float, v, stream=None):
+    _check(lib().psc_admm_primal(int(w.numel()), _f32(w, "w"), _f32(dw, "dw"), _f32(a, "a"), _f32(d, "d"),
+                                 int(b.numel()) if b is not None else 0, _f32(b, "b"), _f32(db, "db"),
+                                 float(lr), float(rho), _f32(v, "v"), _stream(stream)), "psc_admm_primal")
+
+
+def admm_dual(layer: Layer, v, pat, keep_mask, a, d, stream=None):
+    _check(lib().psc_admm_dual(layer.ref(), _f32(v, "v"), _dev(pat, "pat"), _dev(keep_mask, "keep"),
+                               _f32(a, "a"), _f32(d, "d"), _stream(stream)), "psc_admm_dual")
+
+
+def admm_rho(iteration: int, rho0: float = 1e-4, factor: float = 10.0, every_epochs: int = 11,
+             iters_per_epoch: int = 10, rho_max: float = 1e-1) -> float:
+    """The penalty schedule of the paper's settings (Sec. 5.1): rho starts at
+    1e-4 and grows 10x every 11 epochs of 10 iterations until it reaches
+    1e-1.  ``iteration`` counts from 1."""
+    epoch = (int(iteration) - 1) // iters_per_epoch
+    return min(rho_max, rho0 * factor ** (epoch // every_epochs))
+
+
+class AdmmLayer:
+    """Device state of the data-free ADMM pruning of one fp32 layer
+    (Algorithm 1 for one n): W, b (updated by SGD), A, D, and the buffers of
+    one iteration; every step runs in the library's kernels."""
+
+    def __init__(self, w0, b0, masks, keep: int, lr: float = 1e-3, noalloc: bool = False):
+        torch = _torch()
+        self.w0, self.b0 = w0, b0
+        self.w, self.b = w0.clone(), b0.clone()
+        self.a, self.d = w0.clone(), torch.zeros_like(w0)
+        self.dw, self.db, self.v = torch.empty_like(w0), torch.empty_like(b0), torch.empty_like(w0)
+        cout, cin = int(w0.shape[0]), int(w0.shape[1])
+        self.layer = Layer(cout, cin, masks, keep, PSC_F32)
+        K = cout * cin
+        self.pat = torch.empty(K, dtype=torch.uint8, device=w0.device)
+        self.energy = torch.empty(K, dtype=torch.float64, device=w0.device)
+        self.keep_mask = torch.empty(K, dtype=torch.uint8, device=w0.device)
+        self.ws_sel = None if noalloc else workspace(self.layer, PSC_OP_SELECT, w0.device)
+        self.ws_res = torch.empty(ADMM_RESIDUAL_WS_BYTES, dtype=torch.uint8, device=w0.device)
+        self.loss = torch.zeros(1, dtype=torch.float64, device=w0.device)
+        self.lr, self.k = float(lr), 0
+        self._bufs = {}
+
+    def _buf(self, name, shape):
+        torch = _torch()
+        t = self._bufs.get(name)
+        if t is None or tuple(t.shape) != tuple(shape):
+            t = self._bufs[name] = torch.empty(shape, dtype=torch.float32, device=self.w.device)
+        return t
+
+    def target(self, x, out=None, stream=None):
+        """X' = relu(W0 X + b0): the pre-trained layer's output."""
+        n, _, h, w = x.shape
+        out = out if out is not None else self._buf("target", (n, self.layer.cout, h, w))
+        dense3x3_fwd(x, self.w0, out, bias=self.b0, relu=True, stream=stream)
+        return out
+
+    def iteration(self, x, target, rho: float, scale: float, stream=None):
+        """One iteration (Eq. 4, 6, 7) on the batch x with target X'."""
+        n, _, h, w = x.shape
+        z = self._buf("z", (n, self.layer.cout, h, w))
+        g = self._buf("g", (n, self.layer.cout, h, w))
+        dense3x3_fwd(x, self.w, z, bias=self.b, relu=False, stream=stream)
+        admm_residual(z, target, scale, g, self.loss, self.ws_res, stream)
+        dense3x3_bwd_weight(x, g, self.dw, self.db, stream)
+        admm_primal(self.w, self.dw, self.a, self.d, self.b, self.db, self.lr, rho, self.v, stream)
+        project(self.layer, self.v, self.pat, self.energy, stream)
+        if self.ws_sel is None:
+            select_noalloc(self.layer, self.energy, self.keep_mask, stream)
+        else:
+            select(self.layer, self.energy, self.keep_mask, self.ws_sel, stream)
+        admm_dual(self.layer, self.v, self.pat, self.keep_mask, self.a, self.d, stream)
+        self.k += 1
+        return self.loss
 
 
 # ------------------------------------------------------------------ conveniences

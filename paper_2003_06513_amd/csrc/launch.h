@@ -82,6 +82,17 @@ hipError_t launch_bwd_weight(const PatTable& tab, const PackedView& pk, int dtyp
                              int cout, int64_t keep, const void* x, const void* dy, float* dv, float* db,
                              hipStream_t stream);
 
+// Sec. 4.3 Eq. 4-7: the data-free ADMM pruning of one layer (fp32).
+size_t admm_residual_workspace_bytes();
+hipError_t launch_admm_residual(const float* z, const float* t, int64_t numel, float scale, float* g,
+                                double* loss, void* ws, hipStream_t stream);
+hipError_t launch_dense_wgrad(const float* x, const float* g, int n, int cin, int h, int w, int cout, float* dw,
+                              float* db, hipStream_t stream);
+hipError_t launch_admm_primal(float* w, const float* dw, const float* a, const float* d, int64_t nw, float* b,
+                              const float* db, int cout, float lr, float rho, float* v, hipStream_t stream);
+hipError_t launch_admm_dual(const PatTable& tab, const float* v, const uint8_t* pat, const uint8_t* keep, int64_t nk,
+                            float* a, float* d, hipStream_t stream);
+
 hipError_t launch_dense(int dtype, const void* x, int n, int cin, int h, int w, const void* wd,
                         int cout, const void* bias, int relu, void* y, hipStream_t stream);
 hipError_t launch_maxpool(int dtype, const void* x, int n, int c, int h, int w, void* y,

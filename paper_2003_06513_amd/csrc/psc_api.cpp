@@ -3,6 +3,7 @@
 // the HIP launchers.  Every check runs before the first HIP call.
 #include <hip/hip_runtime_api.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -417,6 +418,59 @@ psc_status psc_conv3x3_bwd_weight(const psc_layer* L, const psc_packed* pk, int3
     return device_status(psc::launch_bwd_weight(t, v, act_dtype, n, L->cin, h, w, L->cout, L->keep, d_x, d_dy,
                                                 d_dvalues, d_dbias, as_stream(stream)),
                          "psc_conv3x3_bwd_weight launch");
+}
+
+psc_status psc_admm_residual(const float* d_z, const float* d_target, int64_t numel, float scale, float* d_g,
+                             double* d_loss, void* d_ws, size_t ws_bytes, void* stream) {
+    if (numel < 0 || numel > kMaxElems) return fail(PSC_ERR_ARG, "numel=%lld outside 0..2^31-1", (long long)numel);
+    if (!(scale > 0.f) || !std::isfinite(scale)) return fail(PSC_ERR_ARG, "scale must be positive and finite");
+    if (!d_loss || (numel > 0 && (!d_z || !d_target || !d_g)))
+        return fail(PSC_ERR_ARG, "d_z, d_target, d_g and d_loss must be non-NULL");
+    if (!d_ws || ws_bytes < psc::admm_residual_workspace_bytes())
+        return fail(PSC_ERR_WORKSPACE, "psc_admm_residual needs %zu workspace bytes, got %zu",
+                    psc::admm_residual_workspace_bytes(), ws_bytes);
+    if (reinterpret_cast<uintptr_t>(d_ws) & 255u) return fail(PSC_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    return device_status(psc::launch_admm_residual(d_z, d_target, numel, scale, d_g, d_loss, d_ws, as_stream(stream)),
+                         "psc_admm_residual launch");
+}
+
+psc_status psc_dense3x3_bwd_weight(const float* d_x, const float* d_g, int32_t n, int32_t cin, int32_t h,
+                                   int32_t w, int32_t cout, float* d_dw, float* d_db, void* stream) {
+    if (n < 0 || n > 65535 || cin < 1 || cout < 1 || cout > 65535 || h < 1 || w < 1 || h > 32768 || w > 32768)
+        return fail(PSC_ERR_ARG, "bad shape n=%d cin=%d cout=%d h=%d w=%d", n, cin, cout, h, w);
+    const int64_t plane = int64_t(h) * w;
+    if (int64_t(n) * cin * plane > kMaxElems || int64_t(n) * cout * plane > kMaxElems ||
+        int64_t(cout) * cin * 9 > kMaxElems || int64_t(cout) * cin > 0x7fffffff)
+        return fail(PSC_ERR_ARG, "a tensor holds more than 2^31-1 elements");
+    if (!d_dw) return fail(PSC_ERR_ARG, "d_dw must be non-NULL");
+    if (n > 0 && (!d_x || !d_g)) return fail(PSC_ERR_ARG, "d_x and d_g must be non-NULL");
+    return device_status(psc::launch_dense_wgrad(d_x, d_g, n, cin, h, w, cout, d_dw, d_db, as_stream(stream)),
+                         "psc_dense3x3_bwd_weight launch");
+}
+
+psc_status psc_admm_primal(int64_t n_weights, float* d_w, const float* d_dw, const float* d_a, const float* d_d,
+                           int32_t cout, float* d_b, const float* d_db, float lr, float rho, float* d_v,
+                           void* stream) {
+    if (n_weights < 0 || n_weights > kMaxElems) return fail(PSC_ERR_ARG, "n_weights outside 0..2^31-1");
+    if (cout < 0) return fail(PSC_ERR_ARG, "cout < 0");
+    if (!std::isfinite(lr) || !std::isfinite(rho) || rho < 0.f) return fail(PSC_ERR_ARG, "lr and rho must be finite, rho >= 0");
+    if (n_weights > 0 && (!d_w || !d_dw || !d_a || !d_d || !d_v))
+        return fail(PSC_ERR_ARG, "d_w, d_dw, d_a, d_d and d_v must be non-NULL");
+    if (d_b && cout > 0 && !d_db) return fail(PSC_ERR_ARG, "d_db must be non-NULL with d_b");
+    return device_status(psc::launch_admm_primal(d_w, d_dw, d_a, d_d, n_weights, d_b, d_db, cout, lr, rho, d_v,
+                                                 as_stream(stream)),
+                         "psc_admm_primal launch");
+}
+
+psc_status psc_admm_dual(const psc_layer* L, const float* d_v, const uint8_t* d_pat, const uint8_t* d_keep,
+                         float* d_a, float* d_d, void* stream) {
+    if (psc_status s = check_layer(L, false)) return s;
+    if (L->wdtype != PSC_F32) return fail(PSC_ERR_UNSUPPORTED, "the ADMM steps run in fp32");
+    if (!d_v || !d_pat || !d_keep || !d_a || !d_d) return fail(PSC_ERR_ARG, "every pointer must be non-NULL");
+    const psc::PatTable t = table_of(L);
+    return device_status(psc::launch_admm_dual(t, d_v, d_pat, d_keep, int64_t(L->cout) * L->cin, d_a, d_d,
+                                               as_stream(stream)),
+                         "psc_admm_dual launch");
 }
 
 psc_status psc_dense3x3_fwd(int32_t dtype, const void* d_x, int32_t n, int32_t cin, int32_t h,

@@ -225,3 +225,46 @@ def random_masks(seed: int, m: int, centre: bool = True) -> np.ndarray:
     codes = [c for c in range(512) if bin(c).count("1") == 4 and (not centre or (c >> 4) & 1)]
     idx = rng.choice(len(codes), size=m, replace=False)
     return np.array([codes[i] for i in idx], dtype=np.uint16)
+
+
+# ---------------------------------------------------------------- ADMM pruning
+@dataclasses.dataclass(frozen=True)
+class AdmmWorkload:
+    """One layer pruned by data-free ADMM (Algorithm 1) on batches of T
+    synthetic inputs: the layer's pre-trained weights and bias are He-init
+    and N(0, 0.1) draws; each iteration k draws a new batch."""
+    name: str
+    seed_base: int
+    batch: int                 # T
+    layer: ConvLayer
+    m: int
+    x_dist: str                # "pixels": U{0..255} / 255; "relu": |N(0, 1)|
+    lr: float = 1e-3
+
+    def weights(self) -> np.ndarray:
+        return he_weights(1000 * self.seed_base, self.layer.cout, self.layer.cin)
+
+    def bias(self) -> np.ndarray:
+        return bias_vector(1000 * self.seed_base + 2, self.layer.cout)
+
+    def batch_input(self, k: int) -> np.ndarray:
+        """Batch of iteration k (from 1): images with U{0..255} pixels scaled
+        to [0, 1] for a first layer, or non-negative N(0,1) magnitudes (the
+        value range of a ReLU output) for a later one."""
+        shape = (self.batch, self.layer.cin, self.layer.h, self.layer.w)
+        seed = 1000 * self.seed_base + 100 + k
+        if self.x_dist == "pixels":
+            return (pixel_activations(seed, shape) / np.float32(255.0)).astype(np.float32)
+        return np.abs(normal_activations(seed, shape))
+
+
+def admm_workloads() -> List[AdmmWorkload]:
+    """VGG-16's first layer (3->64 at 224x224, every kernel kept: pattern
+    pruning only) on synthetic images, and a 64->64 layer at 32x32 with half
+    of its kernels dropped (patterns + connectivity), both at T = 32."""
+    return [
+        AdmmWorkload("admm_vgg16_conv1_T32", 7, 32, ConvLayer("conv1", 3, 64, 224, 224, 3 * 64, relu=True), 8,
+                     "pixels"),
+        AdmmWorkload("admm_64c_32x32_T32", 8, 32,
+                     ConvLayer("conv", 64, 64, 32, 32, keep_after_drop(64 * 64, 50), relu=True), 8, "relu"),
+    ]
