@@ -18,9 +18,13 @@ time of MIOpen's dense convolution of the same masked weights (torch
 conv2d) with the speedup over it; and the oracle's fp32-accumulating conv
 loop timed on the host cores, on all threads and on one.
 
+It also times the retraining kernels of each workload (dx through the
+transposed packing and the masked weight gradient) and one iteration of the
+data-free ADMM pruning of a layer (Algorithm 1) on the two ADMM workloads.
+
 Prints ONE JSON line: the headline workload's nonzero-MAC GFLOP/s and
-ms/step, its conv kernels' roofline, the CPU baseline, and a "configs"
-object with the per-workload results.
+ms/step, its conv kernels' roofline, the CPU baseline, a "configs" object
+with the per-workload results and an "admm" object.
 """
 import argparse
 import hashlib
@@ -66,6 +70,10 @@ def parse():
                          "timed at start-up), all, none, or layer names separated by commas")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 256 MiB device-to-device copy (reference for HBM counters)")
+    ap.add_argument("--no-backward", dest="backward", action="store_false",
+                    help="skip the retraining kernels (dx through the transposed packing, masked dW)")
+    ap.add_argument("--no-admm", dest="admm", action="store_false",
+                    help="skip the ADMM pruning iteration timings")
     ap.add_argument("--profile-only", action="store_true",
                     help="only the headline workload's warm-up and timed eager steps (for profiler runs)")
     return ap.parse_args()
@@ -300,6 +308,95 @@ def cpu_baseline(net, budget_s=8.0):
             "value_1thread": round(flops1 / tt / 1e9, 3)}
 
 
+def measure_backward(net):
+    """Retraining kernels (Sec. 3.3) on every stride-1 layer of a prepared
+    workload: dx through the transposed packing (the tuned forward kernels)
+    and the masked weight gradient; flops 8*N*H*W*keep each, as the
+    forward."""
+    import torch
+    from paper_2003_06513_amd import binding as B
+    rows, tot = [], {"dx": [0.0, 0.0], "dw": [0.0, 0.0]}
+    for li, L in enumerate(net.layers):
+        lay = L["lay"]
+        if lay.stride != 1:
+            continue
+        pt = B.prepare_transposed(L["prep"], L["w"])
+        dy = torch.randn((net.wl.batch, lay.cout, lay.h, lay.w), device="cuda").to(net.tdt)
+        dx = torch.empty((net.wl.batch, lay.cin, lay.h, lay.w), dtype=net.tdt, device="cuda")
+        dv = torch.empty(4 * lay.keep, dtype=torch.float32, device="cuda")
+        db = torch.empty(lay.cout, dtype=torch.float32, device="cuda")
+        ws = B.conv3x3_bwd_weight_workspace(L["prep"].layer, L["prep"].layer.dtype, net.wl.batch, lay.h, lay.w)
+        torch.cuda.synchronize()
+        t_dx = time_launches(lambda: B.conv3x3_fwd(pt.layer, pt.packed, dy, dx))[0]
+        t_dw = time_launches(lambda: B.conv3x3_bwd_weight(L["prep"].layer, L["prep"].packed, L["x"], dy, dv, db,
+                                                          ws=ws))[0]
+        fl = 8.0 * net.wl.batch * lay.h * lay.w * lay.keep
+        tot["dx"][0] += fl
+        tot["dx"][1] += t_dx
+        tot["dw"][0] += fl
+        tot["dw"][1] += t_dw
+        rows.append(dict(layer=lay.name, dx_ms=round(t_dx, 5), dw_ms=round(t_dw, 5),
+                         dx_gflops=round(fl / (t_dx * 1e-3) / 1e9, 1), dw_gflops=round(fl / (t_dw * 1e-3) / 1e9, 1)))
+    out = {"layers": rows}
+    for k, (fl, ms) in tot.items():
+        if ms > 0:
+            out[k + "_ms_per_step"] = round(ms, 4)
+            out[k + "_tflops"] = round(fl / (ms * 1e-3) / 1e12, 3)
+            out[k + "_roofline_frac"] = round(fl / (ms * 1e-3) / 1e12 / PEAK_VALU_TFLOPS, 4)
+    return out
+
+
+def measure_admm(wl, iters=10):
+    """One ADMM iteration of one layer (Algorithm 1): the pre-trained target,
+    the current layer, the loss gradient, the dense weight gradient, the SGD
+    step, the projection (project + select) and the dual step, on a new
+    synthetic batch per iteration (batches drawn and uploaded beforehand)."""
+    import torch
+    from paper_2003_06513_amd import binding as B
+    w0 = torch.from_numpy(wl.weights()).cuda()
+    b0 = torch.from_numpy(wl.bias()).cuda()
+    masks = B.select_library(wl.weights(), wl.m)
+    st = B.AdmmLayer(w0, b0, masks, wl.layer.keep, lr=wl.lr)
+    xs = [torch.from_numpy(wl.batch_input(k)).cuda() for k in range(1, 3)]
+    shape = (wl.batch, wl.layer.cout, wl.layer.h, wl.layer.w)
+    tgt = torch.empty(shape, dtype=torch.float32, device="cuda")
+    scale = 1.0 / tgt.numel()
+
+    def one(k):
+        x = xs[k % 2]
+        st.target(x, out=tgt)
+        st.iteration(x, tgt, B.admm_rho(k + 1), scale)
+    for k in range(3):
+        one(k)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for k in range(iters):
+        one(k)
+    e.record()
+    torch.cuda.synchronize()
+    ms_iter = s.elapsed_time(e) / iters
+    x = xs[0]
+    z = st._bufs["z"]
+    dense_fl = 18.0 * wl.batch * wl.layer.h * wl.layer.w * wl.layer.cin * wl.layer.cout
+    parts = {
+        "dense_fwd": time_launches(lambda: B.dense3x3_fwd(x, st.w, z, bias=st.b), warm=3, samples=10, reps=2)[0],
+        "residual": time_launches(lambda: B.admm_residual(z, tgt, scale, st._bufs["g"], st.loss, st.ws_res),
+                                  warm=3, samples=10, reps=2)[0],
+        "dense_wgrad": time_launches(lambda: B.dense3x3_bwd_weight(x, st._bufs["g"], st.dw, st.db,
+                                                                   ws=st._bufs.get("wgrad_ws")),
+                                     warm=3, samples=10, reps=2)[0],
+    }
+    return {"batch": wl.batch, "layer": "%d->%d %dx%d" % (wl.layer.cin, wl.layer.cout, wl.layer.h, wl.layer.w),
+            "keep": wl.layer.keep, "m": wl.m, "ms_per_iteration": round(ms_iter, 4),
+            "loss_after": float(st.loss.item()),
+            "ms": {k: round(v, 4) for k, v in parts.items()},
+            "dense_fwd_tflops": round(dense_fl / (parts["dense_fwd"] * 1e-3) / 1e12, 3),
+            "dense_wgrad_tflops": round(dense_fl / (parts["dense_wgrad"] * 1e-3) / 1e12, 3),
+            "dense_fwd_roofline_frac": round(dense_fl / (parts["dense_fwd"] * 1e-3) / 1e12 / PEAK_VALU_TFLOPS, 4),
+            "dense_wgrad_roofline_frac": round(dense_fl / (parts["dense_wgrad"] * 1e-3) / 1e12 / PEAK_VALU_TFLOPS, 4)}
+
+
 def conv_sources_digest():
     """sha256 over the conv kernel sources (a committed counter summary is
     valid only for the kernels it measured)."""
@@ -361,6 +458,8 @@ def measure(wl, args, headline):
         sparse_ms = sum(r["ms"] for r in rows)
         res["miopen_ms_per_step"] = round(dense_ms, 4)
         res["speedup_vs_miopen"] = round(dense_ms / sparse_ms, 3)
+    if args.backward:
+        res["backward"] = measure_backward(net)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(net)
     roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_VALU_TFLOPS, "unit": "TFLOP/s",
@@ -440,7 +539,9 @@ def main():
         line["cpu_baseline"] = hr["cpu_baseline"]
     line["configs"] = {}
     for name, res in configs.items():
-        c = {k: v for k, v in res.items() if k not in ("layer_detail", "cpu_baseline")}
+        c = {k: v for k, v in res.items() if k not in ("layer_detail", "cpu_baseline", "backward")}
+        if "backward" in res:
+            c["backward"] = {k: v for k, v in res["backward"].items() if k != "layers"}
         c["roofline"] = {k: roofs[name][k] for k in ("achieved", "peak", "frac", "traffic")}
         if "cpu_baseline" in res:
             c["cpu_gflops_all_cores"] = res["cpu_baseline"]["value"]
@@ -450,6 +551,12 @@ def main():
                                + (("miopen_ms", "speedup_vs_miopen") if "miopen_ms" in r else ())}
                               for r in res["layer_detail"]]
         line["configs"][name] = c
+    if args.admm:
+        from synthetic import inputs
+        line["admm"] = {}
+        for wl in inputs.admm_workloads():
+            print("[bench] %s" % wl.name, file=sys.stderr, flush=True)
+            line["admm"][wl.name] = measure_admm(wl)
     print(json.dumps(line), flush=True)
     if args.details:
         with open(args.details, "w") as f:

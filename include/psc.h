@@ -234,11 +234,16 @@ psc_status psc_transpose_prep(const psc_layer *layer, const void *d_w, const uin
  *   d_dbias[f] = sum over images and pixels of dy[n, f].
  * Outputs are fp32 (fp32 accumulation for both activation dtypes), written
  * in full; d_dvalues [keep*4] must be 16-byte aligned, d_dbias is [cout] in
- * the original filter order.  Stride 1, zero padding 1. */
+ * the original filter order.  Stride 1, zero padding 1.  The batch and the
+ * image may be split over several waves per kernel; their sums meet in the
+ * caller's workspace (psc_conv3x3_bwd_weight_workspace bytes, may be 0) and
+ * are added in a fixed order, so results are reproducible bit for bit. */
+psc_status psc_conv3x3_bwd_weight_workspace(const psc_layer *layer, int32_t act_dtype, int32_t n,
+                                            int32_t h, int32_t w, size_t *bytes);
 psc_status psc_conv3x3_bwd_weight(const psc_layer *layer, const psc_packed *packed,
                                   int32_t act_dtype, const void *d_x, const void *d_dy,
                                   int32_t n, int32_t h, int32_t w, float *d_dvalues,
-                                  float *d_dbias, void *stream);
+                                  float *d_dbias, void *d_ws, size_t ws_bytes, void *stream);
 
 /* ---- Data-free ADMM pattern pruning of one layer (Sec. 4.3, Eq. 4-7;
  * Algorithm 1).  With input X (synthetic data), pre-trained W0, b0 and
@@ -265,10 +270,13 @@ psc_status psc_admm_residual(const float *d_z, const float *d_target, int64_t nu
 /* The dense weight gradient of the 3x3 layer (stride 1, zero padding 1):
  *   d_dw[o][i][r][s] = sum over images and pixels of
  *                      g[n, o, h, w] * x[n, i, h + r - 1, w + s - 1]
- * and, if d_db is non-NULL, d_db[o] = sum of g[n, o, :, :]; fp32. */
+ * and, if d_db is non-NULL, d_db[o] = sum of g[n, o, :, :]; fp32.  Workspace
+ * as for psc_conv3x3_bwd_weight (psc_dense3x3_bwd_weight_workspace bytes). */
+psc_status psc_dense3x3_bwd_weight_workspace(int32_t n, int32_t cin, int32_t h, int32_t w,
+                                             int32_t cout, size_t *bytes);
 psc_status psc_dense3x3_bwd_weight(const float *d_x, const float *d_g, int32_t n, int32_t cin,
                                    int32_t h, int32_t w, int32_t cout, float *d_dw, float *d_db,
-                                   void *stream);
+                                   void *d_ws, size_t ws_bytes, void *stream);
 
 /* Eq. 4, one SGD step, in place: for each of the n_weights entries
  *   W = W - lr * (dW + rho * ((W - A) + D)),   V = W + D;

@@ -100,9 +100,11 @@ def lib() -> ctypes.CDLL:
                                ctypes.c_int),
         "psc_transpose_layer": ([LP, LP], ctypes.c_int),
         "psc_transpose_prep": ([LP, P, P, P, P, P, P, P], ctypes.c_int),
-        "psc_conv3x3_bwd_weight": ([LP, PP, i32, P, P, i32, i32, i32, P, P, P], ctypes.c_int),
+        "psc_conv3x3_bwd_weight_workspace": ([LP, i32, i32, i32, i32, ctypes.POINTER(sz)], ctypes.c_int),
+        "psc_conv3x3_bwd_weight": ([LP, PP, i32, P, P, i32, i32, i32, P, P, P, sz, P], ctypes.c_int),
         "psc_admm_residual": ([P, P, i64, ctypes.c_float, P, P, P, sz, P], ctypes.c_int),
-        "psc_dense3x3_bwd_weight": ([P, P, i32, i32, i32, i32, i32, P, P, P], ctypes.c_int),
+        "psc_dense3x3_bwd_weight_workspace": ([i32, i32, i32, i32, i32, ctypes.POINTER(sz)], ctypes.c_int),
+        "psc_dense3x3_bwd_weight": ([P, P, i32, i32, i32, i32, i32, P, P, P, sz, P], ctypes.c_int),
         "psc_admm_primal": ([i64, P, P, P, P, i32, P, P, ctypes.c_float, ctypes.c_float, P, P], ctypes.c_int),
         "psc_admm_dual": ([LP, P, P, P, P, P, P], ctypes.c_int),
         "psc_dense3x3_fwd": ([i32, P, i32, i32, i32, i32, P, i32, P, i32, P, P], ctypes.c_int),
@@ -340,14 +342,29 @@ def transpose_prep(layer: Layer, w, pat, keep_mask, w_t, pat_t, keep_t, stream=N
                                     _stream(stream)), "psc_transpose_prep")
 
 
-def conv3x3_bwd_weight(layer: Layer, packed: Packed, x, dy, dvalues, dbias=None, stream=None):
+def _ws_bytes(tensor):
+    return 0 if tensor is None else int(tensor.numel()) * tensor.element_size()
+
+
+def conv3x3_bwd_weight_workspace(layer: Layer, dtype: int, n: int, h: int, w: int, device="cuda"):
+    """A workspace tensor for psc_conv3x3_bwd_weight (None if it needs none)."""
+    b = ctypes.c_size_t(0)
+    _check(lib().psc_conv3x3_bwd_weight_workspace(layer.ref(), int(dtype), int(n), int(h), int(w), ctypes.byref(b)),
+           "psc_conv3x3_bwd_weight_workspace")
+    return None if b.value == 0 else _torch().empty(int(b.value), dtype=_torch().uint8, device=device)
+
+
+def conv3x3_bwd_weight(layer: Layer, packed: Packed, x, dy, dvalues, dbias=None, ws=None, stream=None):
     n, cin, h, w = (int(d) for d in x.shape)
     if cin != layer.cin or tuple(dy.shape) != (n, layer.cout, h, w) or dvalues.numel() != 4 * layer.keep:
         raise ValueError("x/dy/dvalues shapes do not match the layer")
+    if ws is None:
+        ws = conv3x3_bwd_weight_workspace(layer, dtype_code(x), n, h, w, x.device)
     cp = packed.c()
     _check(lib().psc_conv3x3_bwd_weight(layer.ref(), ctypes.byref(cp), dtype_code(x), _dev(x, "x"), _dev(dy, "dy"),
-                                        n, h, w, _dev(dvalues, "dvalues"), _dev(dbias, "dbias"), _stream(stream)),
-           "psc_conv3x3_bwd_weight")
+                                        n, h, w, _dev(dvalues, "dvalues"), _dev(dbias, "dbias"), _dev(ws, "ws"),
+                                        _ws_bytes(ws), _stream(stream)), "psc_conv3x3_bwd_weight")
+    return ws
 
 
 ADMM_RESIDUAL_WS_BYTES = 8192
@@ -370,13 +387,24 @@ def admm_residual(z, target, scale: float, g, loss, ws, stream=None):
                                    _stream(stream)), "psc_admm_residual")
 
 
-def dense3x3_bwd_weight(x, g, dw, db=None, stream=None):
+def dense3x3_bwd_weight_workspace(n: int, cin: int, h: int, w: int, cout: int, device="cuda"):
+    b = ctypes.c_size_t(0)
+    _check(lib().psc_dense3x3_bwd_weight_workspace(int(n), int(cin), int(h), int(w), int(cout), ctypes.byref(b)),
+           "psc_dense3x3_bwd_weight_workspace")
+    return None if b.value == 0 else _torch().empty(int(b.value), dtype=_torch().uint8, device=device)
+
+
+def dense3x3_bwd_weight(x, g, dw, db=None, ws=None, stream=None):
     n, cin, h, w = (int(d) for d in x.shape)
     cout = int(g.shape[1])
     if tuple(g.shape) != (n, cout, h, w) or tuple(dw.shape) != (cout, cin, 3, 3):
         raise ValueError("x/g/dw shapes do not match")
+    if ws is None:
+        ws = dense3x3_bwd_weight_workspace(n, cin, h, w, cout, x.device)
     _check(lib().psc_dense3x3_bwd_weight(_f32(x, "x"), _f32(g, "g"), n, cin, h, w, cout, _f32(dw, "dw"),
-                                         _f32(db, "db"), _stream(stream)), "psc_dense3x3_bwd_weight")
+                                         _f32(db, "db"), _dev(ws, "ws"), _ws_bytes(ws), _stream(stream)),
+           "psc_dense3x3_bwd_weight")
+    return ws
 
 
 def admm_primal(w, dw, a, d, b, db, lr: float, rho: float, v, stream=None):
@@ -443,7 +471,11 @@ class AdmmLayer:
         g = self._buf("g", (n, self.layer.cout, h, w))
         dense3x3_fwd(x, self.w, z, bias=self.b, relu=False, stream=stream)
         admm_residual(z, target, scale, g, self.loss, self.ws_res, stream)
-        dense3x3_bwd_weight(x, g, self.dw, self.db, stream)
+        ws = self._bufs.get("wgrad_ws")
+        need = dense3x3_bwd_weight_workspace(n, self.layer.cin, h, w, self.layer.cout, x.device) \
+            if "wgrad_shape" not in self._bufs or self._bufs["wgrad_shape"] != (n, h, w) else ws
+        self._bufs["wgrad_ws"], self._bufs["wgrad_shape"] = need, (n, h, w)
+        dense3x3_bwd_weight(x, g, self.dw, self.db, ws=need, stream=stream)
         admm_primal(self.w, self.dw, self.a, self.d, self.b, self.db, self.lr, rho, self.v, stream)
         project(self.layer, self.v, self.pat, self.energy, stream)
         if self.ws_sel is None:

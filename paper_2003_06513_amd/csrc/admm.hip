@@ -4,7 +4,7 @@
 //   Z = W X + b                    psc_dense3x3_fwd (the pre-trained target
 //                                  X' = relu(W0 X + b0) the same way)
 //   G, loss                        k_admm_residual: G = 2c (relu(Z) - X')[Z > 0]
-//   dW, db                         k_dense_wgrad: the dense weight gradient
+//   dW, db                         the dense weight gradient (wgrad.hip)
 //   W, b, V = W + D                k_admm_primal: the SGD step of Eq. 4
 //   pattern ids, keep mask         psc_project + psc_select on V (Eq. 6)
 //   A, D                           k_admm_dual: A = V on the kept pattern
@@ -52,63 +52,6 @@ __global__ __launch_bounds__(256) void k_sum_partials(const double* __restrict__
         __syncthreads();
     }
     if (threadIdx.x == 0) *out = c * part[0];
-}
-
-// One block per (filter o, input channel i): dW[o][i][r][s] = sum over
-// images and pixels of g[n, o, h, w] * x[n, i, h + r - 1, w + s - 1], and
-// db[o] (blocks with i = 0).  Threads cover max(1, 256 / W) rows of up to 256
-// columns per step; per-thread partial sums are added across the block in a
-// fixed order.
-__global__ __launch_bounds__(256) void k_dense_wgrad(const float* __restrict__ x, const float* __restrict__ g,
-                                                     int n, int cin, int H, int W, int cout,
-                                                     float* __restrict__ dw, float* __restrict__ db) {
-    __shared__ float part[4][10];
-    const int o = blockIdx.x / cin, ci = blockIdx.x - (blockIdx.x / cin) * cin;
-    const int rpi = W >= 256 ? 1 : 256 / W;
-    const int cw = W >= 256 ? 256 : W;
-    const int lr = threadIdx.x / cw, lc = threadIdx.x - lr * cw;
-    const int plane = H * W;
-    float acc[10];
-#pragma unroll
-    for (int u = 0; u < 10; ++u) acc[u] = 0.f;
-    if (lr < rpi) {
-        for (int nn = 0; nn < n; ++nn) {
-            const float* xc = x + (int64_t(nn) * cin + ci) * plane;
-            const float* gc = g + (int64_t(nn) * cout + o) * plane;
-            for (int i0 = 0; i0 < H; i0 += rpi) {
-                const int i = i0 + lr;
-                if (i >= H) continue;
-                for (int j = lc; j < W; j += cw) {
-                    const float gv = gc[i * W + j];
-#pragma unroll
-                    for (int r = 0; r < 3; ++r) {
-                        const int ii = i + r - 1;
-                        const bool rok = ii >= 0 && ii < H;
-#pragma unroll
-                        for (int s = 0; s < 3; ++s) {
-                            const int jj = j + s - 1;
-                            const float xv = (rok && jj >= 0 && jj < W) ? xc[ii * W + jj] : 0.f;
-                            acc[3 * r + s] = fmaf(gv, xv, acc[3 * r + s]);
-                        }
-                    }
-                    acc[9] += gv;
-                }
-            }
-        }
-    }
-#pragma unroll
-    for (int u = 0; u < 10; ++u) {
-        float v = acc[u];
-        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-        if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6][u] = v;
-    }
-    __syncthreads();
-    if (threadIdx.x < 10) {
-        const int u = threadIdx.x;
-        const float v = (part[0][u] + part[1][u]) + (part[2][u] + part[3][u]);
-        if (u < 9) dw[(int64_t(o) * cin + ci) * 9 + u] = v;
-        else if (ci == 0 && db) db[o] = v;
-    }
 }
 
 // The SGD step of Eq. 4 on W (gradient dW + rho (W - A + D)) and on b, and
@@ -161,13 +104,6 @@ hipError_t launch_admm_residual(const float* z, const float* t, int64_t numel, f
     hipLaunchKernelGGL(k_admm_residual, dim3(unsigned(nb)), dim3(256), 0, stream, z, t, numel, 2.0f * scale, g,
                        partial);
     hipLaunchKernelGGL(k_sum_partials, dim3(1), dim3(256), 0, stream, partial, nb, double(scale), loss);
-    return hipGetLastError();
-}
-
-hipError_t launch_dense_wgrad(const float* x, const float* g, int n, int cin, int h, int w, int cout, float* dw,
-                              float* db, hipStream_t stream) {
-    hipLaunchKernelGGL(k_dense_wgrad, dim3(unsigned(int64_t(cout) * cin)), dim3(256), 0, stream, x, g, n, cin, h, w,
-                       cout, dw, db);
     return hipGetLastError();
 }
 

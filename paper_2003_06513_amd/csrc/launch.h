@@ -78,8 +78,9 @@ void describe_conv(const PatTable& tab, const ConvArgs& a, int algo, ConvForm& o
 hipError_t launch_transpose_prep(int dtype, int cout, int cin, const void* w, const uint8_t* pat,
                                  const uint8_t* keep, void* wt, uint8_t* pat_t, uint8_t* keep_t,
                                  hipStream_t stream);
+size_t wgrad_workspace_bytes(int n, int cin, int cout, int h, int w, int64_t nk, bool dense);
 hipError_t launch_bwd_weight(const PatTable& tab, const PackedView& pk, int dtype, int n, int cin, int h, int w,
-                             int cout, int64_t keep, const void* x, const void* dy, float* dv, float* db,
+                             int cout, int64_t keep, const void* x, const void* dy, float* dv, float* db, void* ws,
                              hipStream_t stream);
 
 // Sec. 4.3 Eq. 4-7: the data-free ADMM pruning of one layer (fp32).
@@ -87,7 +88,7 @@ size_t admm_residual_workspace_bytes();
 hipError_t launch_admm_residual(const float* z, const float* t, int64_t numel, float scale, float* g,
                                 double* loss, void* ws, hipStream_t stream);
 hipError_t launch_dense_wgrad(const float* x, const float* g, int n, int cin, int h, int w, int cout, float* dw,
-                              float* db, hipStream_t stream);
+                              float* db, void* ws, hipStream_t stream);
 hipError_t launch_admm_primal(float* w, const float* dw, const float* a, const float* d, int64_t nw, float* b,
                               const float* db, int cout, float lr, float rho, float* v, hipStream_t stream);
 hipError_t launch_admm_dual(const PatTable& tab, const float* v, const uint8_t* pat, const uint8_t* keep, int64_t nk,

@@ -404,11 +404,22 @@ psc_status psc_transpose_prep(const psc_layer* L, const void* d_w, const uint8_t
                          "psc_transpose_prep launch");
 }
 
+psc_status psc_conv3x3_bwd_weight_workspace(const psc_layer* L, int32_t act_dtype, int32_t n, int32_t h, int32_t w,
+                                            size_t* bytes) {
+    if (psc_status s = check_conv_shape(L, act_dtype, n, h, w, 0, 0, 1)) return s;
+    if (!bytes) return fail(PSC_ERR_ARG, "bytes is NULL");
+    *bytes = psc::wgrad_workspace_bytes(n, L->cin, L->cout, h, w, L->keep, false);
+    return ok();
+}
+
 psc_status psc_conv3x3_bwd_weight(const psc_layer* L, const psc_packed* pk, int32_t act_dtype, const void* d_x,
                                   const void* d_dy, int32_t n, int32_t h, int32_t w, float* d_dvalues,
-                                  float* d_dbias, void* stream) {
+                                  float* d_dbias, void* d_ws, size_t ws_bytes, void* stream) {
     if (psc_status s = check_conv_shape(L, act_dtype, n, h, w, 0, 0, 1)) return s;
     if (psc_status s = check_packed(L, pk)) return s;
+    const size_t need = psc::wgrad_workspace_bytes(n, L->cin, L->cout, h, w, L->keep, false);
+    if (need && (!d_ws || ws_bytes < need))
+        return fail(PSC_ERR_WORKSPACE, "bwd weight needs %zu workspace bytes, got %zu", need, ws_bytes);
     if (n == 0) return ok();
     if (!d_x || !d_dy) return fail(PSC_ERR_ARG, "d_x and d_dy must be non-NULL");
     if (L->keep > 0 && !d_dvalues) return fail(PSC_ERR_ARG, "d_dvalues must be non-NULL when keep > 0");
@@ -416,7 +427,7 @@ psc_status psc_conv3x3_bwd_weight(const psc_layer* L, const psc_packed* pk, int3
     const psc::PatTable t = table_of(L);
     const psc::PackedView v{pk->filter_perm, pk->filter_ptr, pk->seg_ptr, pk->cin_idx, pk->pat_id, pk->values};
     return device_status(psc::launch_bwd_weight(t, v, act_dtype, n, L->cin, h, w, L->cout, L->keep, d_x, d_dy,
-                                                d_dvalues, d_dbias, as_stream(stream)),
+                                                d_dvalues, d_dbias, d_ws, as_stream(stream)),
                          "psc_conv3x3_bwd_weight launch");
 }
 
@@ -434,17 +445,35 @@ psc_status psc_admm_residual(const float* d_z, const float* d_target, int64_t nu
                          "psc_admm_residual launch");
 }
 
-psc_status psc_dense3x3_bwd_weight(const float* d_x, const float* d_g, int32_t n, int32_t cin, int32_t h,
-                                   int32_t w, int32_t cout, float* d_dw, float* d_db, void* stream) {
+static psc_status check_dense_wgrad_shape(int32_t n, int32_t cin, int32_t h, int32_t w, int32_t cout) {
     if (n < 0 || n > 65535 || cin < 1 || cout < 1 || cout > 65535 || h < 1 || w < 1 || h > 32768 || w > 32768)
         return fail(PSC_ERR_ARG, "bad shape n=%d cin=%d cout=%d h=%d w=%d", n, cin, cout, h, w);
     const int64_t plane = int64_t(h) * w;
     if (int64_t(n) * cin * plane > kMaxElems || int64_t(n) * cout * plane > kMaxElems ||
-        int64_t(cout) * cin * 9 > kMaxElems || int64_t(cout) * cin > 0x7fffffff)
+        int64_t(cout) * cin * 9 > kMaxElems)
         return fail(PSC_ERR_ARG, "a tensor holds more than 2^31-1 elements");
+    return PSC_OK;
+}
+
+psc_status psc_dense3x3_bwd_weight_workspace(int32_t n, int32_t cin, int32_t h, int32_t w, int32_t cout,
+                                             size_t* bytes) {
+    if (psc_status s = check_dense_wgrad_shape(n, cin, h, w, cout)) return s;
+    if (!bytes) return fail(PSC_ERR_ARG, "bytes is NULL");
+    *bytes = psc::wgrad_workspace_bytes(n, cin, cout, h, w, int64_t(cout) * cin, true);
+    return ok();
+}
+
+psc_status psc_dense3x3_bwd_weight(const float* d_x, const float* d_g, int32_t n, int32_t cin, int32_t h,
+                                   int32_t w, int32_t cout, float* d_dw, float* d_db, void* d_ws, size_t ws_bytes,
+                                   void* stream) {
+    if (psc_status s = check_dense_wgrad_shape(n, cin, h, w, cout)) return s;
     if (!d_dw) return fail(PSC_ERR_ARG, "d_dw must be non-NULL");
     if (n > 0 && (!d_x || !d_g)) return fail(PSC_ERR_ARG, "d_x and d_g must be non-NULL");
-    return device_status(psc::launch_dense_wgrad(d_x, d_g, n, cin, h, w, cout, d_dw, d_db, as_stream(stream)),
+    const size_t need = psc::wgrad_workspace_bytes(n, cin, cout, h, w, int64_t(cout) * cin, true);
+    if (need && (!d_ws || ws_bytes < need))
+        return fail(PSC_ERR_WORKSPACE, "dense bwd weight needs %zu workspace bytes, got %zu", need, ws_bytes);
+    if (n == 0) return ok();
+    return device_status(psc::launch_dense_wgrad(d_x, d_g, n, cin, h, w, cout, d_dw, d_db, d_ws, as_stream(stream)),
                          "psc_dense3x3_bwd_weight launch");
 }
 

@@ -183,5 +183,5 @@ def test_bwd_weight_validates(L):
         setattr(pk, n_, 0x10000)
     import ctypes
     rc = L.psc_conv3x3_bwd_weight(lay.ref(), ctypes.byref(pk), B.PSC_F32, FAKE, FAKE, 1, 4, 4,
-                                  ctypes.c_void_p(0x10004), None, None)
+                                  ctypes.c_void_p(0x10004), None, FAKE, 1 << 30, None)
     assert rc == B.PSC_ERR_ARG and "16-byte" in B.last_error()
