@@ -190,7 +190,9 @@ psc_status psc_conv3x3_fwd_pool2(const psc_layer *layer, const psc_packed *packe
  *   y[n,f,i,j] = sigma(b[f] + sum over kept (ci, p) of f of
  *                sum_{(r,s) in p} v * x[n, ci, stride*i + r - 1, stride*j + s - 1])
  * with out-of-image taps reading zero.  stride 1 is psc_conv3x3_fwd_algo.
- * Stride 2 runs on the one-output-per-lane kernel for either algo.  Other
+ * Stride 2 with algo 0 runs the tuned stride-2 kernel for even widths of at
+ * most 126 columns (the one-output-per-lane kernel otherwise, and always
+ * with algo 1).  Other
  * conventions and errors as in psc_conv3x3_fwd_algo; a stride other than 1
  * or 2 returns PSC_ERR_ARG. */
 psc_status psc_conv3x3_fwd_strided(const psc_layer *layer, const psc_packed *packed,
@@ -299,7 +301,8 @@ psc_status psc_admm_dual(const psc_layer *layer, const float *d_v, const uint8_t
 typedef struct psc_conv_config {
     int32_t kernel;            /* 0: tuned kernel, one output column per lane
                                   1: tuned kernel, 4 output columns per lane
-                                  2: one-output-per-lane kernel */
+                                  2: one-output-per-lane kernel
+                                  3: stride-2 kernel, one output column per lane */
     int32_t staged;            /* 0: input rows loaded straight into registers,
                                   1: staged through LDS, one run per wave,
                                   2: staged through LDS, several runs per wave */

@@ -15,6 +15,36 @@ struct PatTable {
     uint16_t mask[kMaxPatterns];
 };
 
+// The 56 masks made of the centre and 3 of its 8 neighbours, ascending: the
+// shapes the pattern heuristic of Sec. 4.2 can produce, for which the conv
+// kernels have loops compiled with their taps fixed.
+struct Centre3Table {
+    uint16_t code[56];
+    constexpr Centre3Table() : code{} {
+        int n = 0;
+        for (int c = 0; c < 512; ++c) {
+            int pc = 0;
+            for (int b = 0; b < 9; ++b) pc += (c >> b) & 1;
+            if (((c >> 4) & 1) && pc == 4) code[n++] = uint16_t(c);
+        }
+    }
+};
+constexpr Centre3Table kCentre3{};
+
+// Position of the JJ-th set bit of MASK (ascending), -1 if none.
+template <int MASK, int JJ>
+struct NthBit {
+    static constexpr int value() {
+        int seen = 0;
+        for (int q = 0; q < 9; ++q)
+            if ((MASK >> q) & 1) {
+                if (seen == JJ) return q;
+                ++seen;
+            }
+        return -1;
+    }
+};
+
 // Storage <-> fp32 conversions.  fp16 is IEEE binary16; widening is exact,
 // narrowing rounds to nearest even (the hardware default mode).
 template <int DT> struct Elt;

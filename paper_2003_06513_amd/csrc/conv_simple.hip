@@ -9,6 +9,8 @@ namespace psc {
 hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const ConvArgs& a,
                               hipStream_t stream);
 bool describe_conv_stream(const PatTable& tab, const ConvArgs& a, ConvForm& out);
+hipError_t launch_conv_stride2(const PatTable& tab, const PackedView& pk, const ConvArgs& a, hipStream_t stream);
+bool describe_conv_stride2(const PatTable& tab, const ConvArgs& a, ConvForm& out);
 
 namespace {
 
@@ -169,8 +171,13 @@ hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs
     if (algo == 0 && a.stride == 1) {
         const hipError_t e = launch_conv_stream(tab, pk, a, stream);
         if (e != hipErrorNotSupported) return e;
-        // inputs beyond the 2 GiB one buffer descriptor covers, pooled
-        // outputs of haloed column tiles and strided layers take the
+        // inputs beyond the 2 GiB one buffer descriptor covers and pooled
+        // outputs of haloed column tiles take the one-output-per-lane kernel
+    }
+    if (algo == 0 && a.stride == 2) {
+        const hipError_t e = launch_conv_stride2(tab, pk, a, stream);
+        if (e != hipErrorNotSupported) return e;
+        // odd widths and more than 63 output columns take the
         // one-output-per-lane kernel
     }
     return a.dtype == DT_F16 ? conv_simple<DT_F16>(tab, pk, a, stream)
@@ -179,6 +186,7 @@ hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs
 
 void describe_conv(const PatTable& tab, const ConvArgs& a, int algo, ConvForm& out) {
     if (algo == 0 && a.stride == 1 && describe_conv_stream(tab, a, out)) return;
+    if (algo == 0 && a.stride == 2 && describe_conv_stride2(tab, a, out)) return;
     const int outs = a.pool ? (a.h / 2) * (a.w / 2) : ((a.h - 1) / a.stride + 1) * ((a.w - 1) / a.stride + 1);
     const int64_t lanes = int64_t(a.n) * outs;
     out = ConvForm{2, 0, 1, 1, 1, 1, 1, 1, int((lanes + 255) / 256) * a.cout, 256};

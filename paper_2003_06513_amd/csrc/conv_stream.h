@@ -54,20 +54,6 @@ __device__ psc_f32x4 psc_sbuf_f32x4(psc_i32x4, int32_t, int32_t) __asm("llvm.amd
 namespace psc {
 namespace cs {
 
-// The 56 masks made of the centre and 3 of its 8 neighbours, ascending.
-struct Centre3Table {
-    uint16_t code[56];
-    constexpr Centre3Table() : code{} {
-        int n = 0;
-        for (int c = 0; c < 512; ++c) {
-            int pc = 0;
-            for (int b = 0; b < 9; ++b) pc += (c >> b) & 1;
-            if (((c >> 4) & 1) && pc == 4) code[n++] = uint16_t(c);
-        }
-    }
-};
-constexpr Centre3Table kCentre3{};
-
 constexpr int kMaxSplit = 8;
 
 typedef psc_i32x4 int32x4;
@@ -240,20 +226,6 @@ __device__ __forceinline__ void kernel_taps(float (&a)[R], const float (&x)[R + 
         tap_q<Q3, R, WS>(a, x, w[3]);
     }
 }
-
-// Position of the JJ-th set bit of MASK (ascending).
-template <int MASK, int JJ>
-struct NthBit {
-    static constexpr int value() {
-        int seen = 0;
-        for (int q = 0; q < 9; ++q)
-            if ((MASK >> q) & 1) {
-                if (seen == JJ) return q;
-                ++seen;
-            }
-        return -1;
-    }
-};
 
 // ------------------------------------------------------------------ runs
 struct RunCtx;

@@ -22,11 +22,25 @@ PSC_EXTERN_R(DT_F16, 8)
 #undef PSC_EXTERN_R
 extern template hipError_t cs::launch_wide<2>(const PackedView&, const ConvArgs&, const Geo&, hipStream_t);
 
-// Launch configuration.  Rows per lane R minimise the lane-rows issued
-// (ceil(units / S) * R, larger R on ties; even R when pooling; R = 8 only
-// with one segment per wave); a workgroup holds 4 filters, or
-// fewer filters split into KS shares (KS doubles up to 8) while the grid
-// holds under 4 waves per SIMD.  Returns false when the tuned kernels do not
+// Grids of at least this many waves are throughput-bound (16 waves per SIMD).
+constexpr int64_t kManyWaves = 16384;
+// Filters are split into more shares while the grid holds fewer waves.
+constexpr int64_t kSplitWaves = 4096;
+
+// Note on R = 8 with several segments per wave: launches of the direct form
+// with R = 8 and 3 or 7 full-row segments per wave (the batch-256 CIFAR
+// layers 128@16 and 256@8) once faulted the device.  Every load of x and
+// the metadata in that form is range-checked by its buffer descriptor and
+// every store index was checked on the host for those launches, so the cause
+// is not known; the launcher never picks R = 8 when a wave holds more than
+// one segment.
+//
+// Launch configuration.  Rows per lane R minimise the lane-rows loaded
+// (ceil(units / S) * (R + 2)) in throughput-bound grids, the lane-rows
+// issued (ceil(units / S) * R) otherwise, larger R on ties; even R when
+// pooling; R = 8 only with one segment per wave.  A workgroup holds 4
+// filters, or fewer filters split into KS shares (KS doubles up to 8) while
+// the grid holds under 4 waves per SIMD.  Returns false when the tuned kernels do not
 // take the call: x beyond the 2 GiB a buffer descriptor addresses here, or a
 // pooled output of haloed column tiles.  Host only.
 bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
@@ -105,17 +119,22 @@ bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
         g.Wt = Wt;
         g.CT = ct;
     }
-    // rows per lane
+    // rows per lane.  A grid of many waves (throughput-bound) is limited by
+    // the rows a lane loads, R + 2 per R output rows, so its cost counts
+    // loaded rows; a small grid (batch 1) is limited by the per-kernel
+    // latency of its waves, so its cost counts output rows.
     const int cand[4] = {8, 7, 4, 2};
     int R = 8;
     int64_t best = -1;
-    // 8 rows per lane only with one segment per wave (several segments at
-    // R = 8 are kept off: see the note on the launch configuration)
+    const int64_t units4 = int64_t(a.n) * ((a.h + 3) / 4) * g.CT;
+    const bool many_waves = (units4 + g.S - 1) / g.S * a.cout >= kManyWaves;
+    // 8 rows per lane only with one segment per wave (see the note on R = 8
+    // above)
     for (int rr : cand) {
         if (a.pool && (rr & 1)) continue;               // pooled rows pair up inside a lane
         if (rr == 8 && g.S > 1) continue;
         const int64_t units = int64_t(a.n) * ((a.h + rr - 1) / rr) * g.CT;
-        const int64_t cost = (units + g.S - 1) / g.S * rr;
+        const int64_t cost = (units + g.S - 1) / g.S * (many_waves ? rr + 2 : rr);
         if (best < 0 || cost < best) {
             best = cost;
             R = rr;
@@ -125,7 +144,7 @@ bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
     g.U = a.n * g.RB * g.CT;
     const int sgroups = (g.U + g.S - 1) / g.S;
     g.KS = 1;
-    while (g.KS < kMaxSplit && int64_t(sgroups) * a.cout * g.KS < 4096 && a.cin >= 16 * g.KS) g.KS *= 2;
+    while (g.KS < kMaxSplit && int64_t(sgroups) * a.cout * g.KS < kSplitWaves && a.cin >= 16 * g.KS) g.KS *= 2;
     g.FW = g.KS >= 4 ? 1 : 4 / g.KS;
     if (g.FW > a.cout) g.FW = a.cout;
     const int fgroups = (a.cout + g.FW - 1) / g.FW;
@@ -163,7 +182,7 @@ bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
         // one full-row segment per wave and a grid of about one round of
         // waves (batch 1 at W >= 32) is bound by the per-kernel latency,
         // which the direct loads keep shorter
-        const int64_t waves = int64_t(g.nblocks) * g.FW * g.KS;
+        const int64_t waves = int64_t(sgroups) * a.cout * 4;   // at 4 shares per filter
         const bool throughput = g.S >= 2 || waves >= 2 * 6 * 1024;
         g.lds = fits && throughput ? 1 : 0;
         if (g.lds && nruns_max > 1) g.lds = 2;             // several runs per wave: the general form

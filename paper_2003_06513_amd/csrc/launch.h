@@ -67,7 +67,7 @@ hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs
 
 // The launch configuration launch_conv would use (host only, no device work).
 struct ConvForm {
-    int kernel;             // 0 k_conv_stream, 1 k_conv_wide, 2 k_conv_simple
+    int kernel;             // 0 k_conv_stream, 1 k_conv_wide, 2 k_conv_simple, 3 k_conv_stride2
     int staged;             // 0 direct loads, 1 rows staged through LDS, 2 staged, several runs per wave
     int rows_per_lane, cols_per_lane, segments_per_wave, column_tiles;
     int shares, filters_per_block, blocks, threads_per_block;

@@ -177,6 +177,12 @@ def form_cases():
                                 found[key] = (work, (key, n, cin, cout, hw, hw, dt, pool, 1, 0))
     out = [v[1] for v in found.values()]
     for dt in (B.PSC_F32, B.PSC_F16):
+        # the tuned stride-2 kernel: whole filters and split filters, ragged
+        # output bands, several bands per wave
+        for n, cin, cout, h, w in ((2, 9, 7, 14, 12), (1, 64, 8, 16, 16), (3, 5, 6, 13, 6), (1, 24, 5, 9, 126)):
+            L = B.Layer(cout, cin, list(FORM_MASKS), cin * cout // 2, dt)
+            cfg = B.conv3x3_config(L, dt, n, h, w, False, 2, 0)
+            out.append((("stride2", cfg["kernel"], cfg["shares"] > 1), n, cin, cout, h, w, dt, False, 2, 0))
         out.append((("simple-stride2",), 2, 9, 7, 13, 11, dt, False, 2, 0))
         out.append((("simple-algo1",), 2, 9, 7, 13, 11, dt, False, 1, 1))
         out.append((("simple-algo1-pool",), 2, 9, 7, 12, 10, dt, True, 1, 1))

@@ -68,7 +68,9 @@ def test_form_search_reaches_every_form():
     assert any(k[0] == 1 and k[3] for k in keys) and any(k[0] == 1 and k[4] for k in keys)
     assert any(k[2] for k in keys)                                                         # column tiles
     assert {c[0][0] for c in cases if not isinstance(c[0][0], int)} == \
-        {"simple-stride2", "simple-algo1", "simple-algo1-pool"}
+        {"stride2", "simple-stride2", "simple-algo1", "simple-algo1-pool"}
+    s2 = [c[0] for c in cases if c[0][0] == "stride2"]
+    assert all(k[1] == 3 for k in s2) and any(k[2] for k in s2) and any(not k[2] for k in s2)
 
 
 def test_config_query_validates():
@@ -78,5 +80,6 @@ def test_config_query_validates():
                  (B.PSC_F32, 1, 8, 8, False, 1, 2), (B.PSC_F32, -1, 8, 8, False, 1, 0)]:
         with pytest.raises(B.PscError):
             B.conv3x3_config(L, *args)
-    c = B.conv3x3_config(L, B.PSC_F32, 2, 16, 16, False, 2, 0)
-    assert c["kernel"] == 2
+    assert B.conv3x3_config(L, B.PSC_F32, 2, 16, 16, False, 2, 0)["kernel"] == 3      # tuned stride 2
+    assert B.conv3x3_config(L, B.PSC_F32, 2, 16, 15, False, 2, 0)["kernel"] == 2      # odd width
+    assert B.conv3x3_config(L, B.PSC_F32, 2, 16, 16, False, 2, 1)["kernel"] == 2      # algo 1

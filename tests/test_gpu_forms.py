@@ -40,9 +40,13 @@ def test_form_parity_guard_rerun(case):
     masks = B.select_library(wt, 6)
     keep = inputs.keep_after_drop(cout * cin, 50)
     prep, packed = prepared_case(wt, masks, keep)
+    got = B.conv3x3_config(prep.layer, dtc, n, h, w, pool, stride, algo)
     if isinstance(key[0], int):
-        got = B.conv3x3_config(prep.layer, dtc, n, h, w, pool, stride, algo)
         assert (got["kernel"], got["staged"], got["rows_per_lane"]) == (key[0], key[1], key[5])
+    elif key[0] == "stride2":
+        assert got["kernel"] == key[1] == 3
+    else:
+        assert got["kernel"] == 2
     x = inputs.normal_activations(seed + 1, (n, cin, h, w), dtype)
     bias = inputs.bias_vector(seed + 2, cout, dtype) if seed % 2 else None
     relu = bool(seed % 3)
