@@ -244,7 +244,7 @@ def layer_table(net, miopen):
         row = dict(layer=lay.name, cin=lay.cin, cout=lay.cout, h=lay.h, w=lay.w, stride=lay.stride, keep=lay.keep,
                    fused_pool=bool(L["fused"]), ms=round(med, 5), p10=round(p10, 5), p90=round(p90, 5),
                    mean_ms=round(mean, 5), nz_gflops=round(nz / (med * 1e-3) / 1e9, 1),
-                   kernel=["stream", "wide", "simple", "stride2"][L["cfg"]["kernel"]] + ("-staged" if L["cfg"]["staged"] else ""),
+                   kernel=["stream", "wide", "simple", "stride2", "rows"][L["cfg"]["kernel"]] + ("-staged" if L["cfg"]["staged"] else ""),
                    R=L["cfg"]["rows_per_lane"], KS=L["cfg"]["shares"])
         if miopen:
             wd = torch.empty(L["w"].shape, dtype=net.tdt, device="cuda")

@@ -165,8 +165,13 @@ psc_status psc_conv3x3_fwd(const psc_layer *layer, const psc_packed *packed,
                            int32_t relu, void *d_y, void *stream);
 
 /* Same as psc_conv3x3_fwd with an explicit kernel choice: algo 0 = the
- * default tuned kernel, 1 = the simple one-output-per-lane kernel (kept as a
- * second implementation for testing). */
+ * default tuned kernels (chosen from the shape), 1 = the simple
+ * one-output-per-lane kernel (kept as a second implementation for testing),
+ * 2 = the one-row-per-lane kernel, which algo 0 picks for batches that fill
+ * a wave with whole images on planes of at most 16 columns, 3 = the
+ * column-per-lane tuned kernels (algo 0 without that choice).  Algo 2 needs
+ * stride 1, no pool, h <= 63 and w in {4, 7, 8, 14, 16, 28} (fp16: w even,
+ * or 7), else PSC_ERR_UNSUPPORTED. */
 psc_status psc_conv3x3_fwd_algo(const psc_layer *layer, const psc_packed *packed,
                                 int32_t act_dtype, const void *d_x, int32_t n,
                                 int32_t h, int32_t w, const void *d_bias,
@@ -302,13 +307,14 @@ typedef struct psc_conv_config {
     int32_t kernel;            /* 0: tuned kernel, one output column per lane
                                   1: tuned kernel, 4 output columns per lane
                                   2: one-output-per-lane kernel
-                                  3: stride-2 kernel, one output column per lane */
+                                  3: stride-2 kernel, one output column per lane
+                                  4: one output row per lane (all w columns) */
     int32_t staged;            /* 0: input rows loaded straight into registers,
                                   1: staged through LDS, one run per wave,
                                   2: staged through LDS, several runs per wave */
     int32_t rows_per_lane;     /* output rows per lane */
     int32_t cols_per_lane;     /* output columns per lane */
-    int32_t segments_per_wave; /* row bands (or column tiles) per wave */
+    int32_t segments_per_wave; /* row bands (or column tiles, or images) per wave */
     int32_t column_tiles;      /* column tiles per image row (1: full rows) */
     int32_t shares;            /* waves that split one filter's kernels */
     int32_t filters_per_block;

@@ -1,0 +1,427 @@
+// Pattern-sparse 3x3 convolution, stride 1, zero padding 1 (Sec. 4.1 Eq. 1
+// with the compiler optimisations of Sec. 3.4) for planes of at most 28
+// columns: ONE OUTPUT ROW PER LANE.
+//
+// The column-per-lane kernels (conv_stream.h) load, for every kernel, R+2
+// single elements per lane (one per input row of its column) for 4R FMAs.
+// On small planes at large batch that load path is the bound.  Here a lane
+// owns a whole output row of one image -- W accumulators -- and per kernel
+// loads its own input row with 16-byte loads; the rows above and below come
+// from the neighbouring lanes by DPP inside the FMA (v_fmac_f32_dpp
+// wave_shr:1 / wave_shl:1), and the left and right neighbours of a column are
+// other registers of the same lane.  So each loaded element feeds up to 12
+// FMAs (load redundancy elimination at the register level), and a kernel
+// costs 1..7 load instructions instead of R+2.
+//
+// Lane layout: a wave holds S = 64 / (H+1) images; image s occupies lanes
+// s(H+1) .. s(H+1)+H-1 (row r in lane s(H+1)+r) and lane s(H+1)+H holds zero:
+// the padding row below image s and above image s+1.  Padding columns cost
+// nothing: the FMAs that would read them are left out at compile time.
+//
+// As in the other kernels, one wave walks one reordered filter's compressed
+// storage (filter kernel reorder, compressed weight storage): pattern segment
+// by pattern segment, each through a loop compiled for its centre+3 shape,
+// with channel index and weights wave-uniform in SGPRs (scalar buffer loads).
+// The next kernel's row loads while the current kernel's FMAs run.  Small
+// grids split each filter over KS waves whose partial sums are added through
+// LDS in share order (deterministic).
+#pragma once
+
+#include "conv_stream.h"
+
+namespace psc {
+namespace rw {
+
+constexpr int kMaxShares = 8;
+
+struct RGeo {
+    int n, cin, H, W, cout, m;
+    int S;          // images per wave
+    int seg_len;    // lanes per image: H rows + 1 zero lane
+    int groups;     // image groups: ceil(n / S)
+    int FW, KS;     // filters and shares per filter in a workgroup
+    int groups_x;   // filter groups (fastest varying logical block index)
+    int nblocks;
+    int x_bytes;    // bytes of x (the buffer range), below 2^31
+    int keep;
+    int relu;
+    int8_t shape[kMaxPatterns];  // centre+3 shape index of each library pattern, -1 = other mask
+    uint16_t mask[kMaxPatterns];
+};
+
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Raw words of one lane's input row.  fp16 rows of odd width start at a
+// 2-byte boundary: the lane loads the 16-byte window from the 4-byte boundary
+// at or below the row start and shifts it by the 2 bytes if needed.
+template <int DT, int W>
+struct RowWords {
+    static constexpr int ESZ = DT == DT_F32 ? 4 : 2;
+    static constexpr bool ODD = DT == DT_F16 && (W & 1);
+    static constexpr int BYTES = ODD ? 16 : W * ESZ;
+    static constexpr int NW = BYTES / 4;
+    static_assert(BYTES % 4 == 0, "rows are loaded in whole dwords");
+    static_assert(!ODD || W <= 7, "the shifted window holds 7 halves");
+    uint32_t d[NW];
+    uint32_t sh;   // ODD: 0 or 16, the bit shift of the row start in the window
+};
+
+// Load the words at byte offset vo + soff (a buffer load returns zero for any
+// offset past the range of x: padding lanes pass 2^31).
+template <int DT, int W>
+__device__ __forceinline__ void load_words(__amdgpu_buffer_rsrc_t xr, uint32_t vo, int soff, int x_bytes,
+                                           bool valid, RowWords<DT, W>& rw) {
+    using RWd = RowWords<DT, W>;
+    if constexpr (RWd::ODD) {
+        const uint32_t t = vo + uint32_t(soff);
+        const uint32_t at = t & ~3u;
+        rw.sh = (t & 2u) << 3;
+        const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(xr, int(at), 0, 0);
+        rw.d[0] = v.x, rw.d[1] = v.y, rw.d[2] = v.z, rw.d[3] = v.w;
+        // the window of a row that starts on a 4-byte boundary reaches 2
+        // bytes past the row; for the last row of x those lie past the range,
+        // so its 7th half is loaded on its own
+        if (valid && int64_t(at) + 16 > int64_t(x_bytes)) {
+            const uint32_t h = __builtin_amdgcn_raw_buffer_load_b16(xr, int(at + 12), 0, 0);
+            rw.d[3] = (rw.d[3] & 0xffff0000u) | h;
+        }
+    } else {
+#pragma unroll
+        for (int o = 0; o < RWd::BYTES; o += 16) {
+            const int left = RWd::BYTES - o;
+            if (left >= 16) {
+                const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(xr, int(vo + o), soff, 0);
+                rw.d[o / 4] = v.x, rw.d[o / 4 + 1] = v.y, rw.d[o / 4 + 2] = v.z, rw.d[o / 4 + 3] = v.w;
+            } else if (left == 12) {
+                const u32x3 v = __builtin_amdgcn_raw_buffer_load_b96(xr, int(vo + o), soff, 0);
+                rw.d[o / 4] = v.x, rw.d[o / 4 + 1] = v.y, rw.d[o / 4 + 2] = v.z;
+            } else if (left == 8) {
+                const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(xr, int(vo + o), soff, 0);
+                rw.d[o / 4] = v.x, rw.d[o / 4 + 1] = v.y;
+            } else {
+                rw.d[o / 4] = __builtin_amdgcn_raw_buffer_load_b32(xr, int(vo + o), soff, 0);
+            }
+        }
+    }
+}
+
+// The W input values of the row as fp32 (fp16 widened exactly).
+template <int DT, int W>
+__device__ __forceinline__ void unpack_row(const RowWords<DT, W>& rw, float (&x)[W]) {
+    if constexpr (DT == DT_F32) {
+#pragma unroll
+        for (int j = 0; j < W; ++j) x[j] = __builtin_bit_cast(float, rw.d[j]);
+    } else {
+        uint32_t s[RowWords<DT, W>::NW];
+        if constexpr (RowWords<DT, W>::ODD) {
+#pragma unroll
+            for (int i = 0; i + 1 < RowWords<DT, W>::NW; ++i) s[i] = __builtin_amdgcn_alignbit(rw.d[i + 1], rw.d[i], rw.sh);
+            s[RowWords<DT, W>::NW - 1] = rw.d[RowWords<DT, W>::NW - 1] >> rw.sh;
+        } else {
+#pragma unroll
+            for (int i = 0; i < RowWords<DT, W>::NW; ++i) s[i] = rw.d[i];
+        }
+#pragma unroll
+        for (int j = 0; j < W; ++j)
+            x[j] = float(__builtin_bit_cast(_Float16, uint16_t(s[j / 2] >> (16 * (j & 1)))));
+    }
+}
+
+// After the row values are final: an asm the compiler sees as writing them
+// (so no VALU write of a row value can follow), then the two wait states a
+// DPP read needs after a VALU write of its source.
+template <int W>
+__device__ __forceinline__ void settle_row(float (&x)[W]) {
+#pragma unroll
+    for (int j = 0; j < W; j += 4) {
+        if constexpr (W % 4 == 0) {
+            asm volatile("" : "+v"(x[j]), "+v"(x[j + 1]), "+v"(x[j + 2]), "+v"(x[j + 3]));
+        } else {
+            if (j + 3 < W) asm volatile("" : "+v"(x[j]), "+v"(x[j + 1]), "+v"(x[j + 2]), "+v"(x[j + 3]));
+            else
+                for (int t = j; t < W; ++t) asm volatile("" : "+v"(x[t]));
+        }
+    }
+    asm volatile("s_nop 1");
+}
+
+// The tap at kernel position Q = 3 ky + kx: acc[c] += w * x(row r + ky - 1,
+// column c + kx - 1).  Row r - 1 is the lane to the left (wave_shr), row r + 1
+// the lane to the right (wave_shl); lanes without a neighbour read zero
+// (bound_ctrl).  Columns outside the row are skipped.
+template <int Q, int W>
+__device__ __forceinline__ void tap_row(float (&acc)[W], const float (&x)[W], float w) {
+    constexpr int ky = Q / 3, kx = Q % 3;
+    constexpr int c0 = kx == 0 ? 1 : 0, c1 = kx == 2 ? W - 1 : W;
+#pragma unroll
+    for (int c = c0; c < c1; ++c) {
+        if constexpr (ky == 1) {
+            acc[c] = __builtin_fmaf(w, x[c + kx - 1], acc[c]);
+        } else if constexpr (ky == 0) {
+            asm volatile("v_fmac_f32_dpp %0, %1, %2 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+                         : "+v"(acc[c])
+                         : "v"(x[c + kx - 1]), "v"(w));
+        } else {
+            asm volatile("v_fmac_f32_dpp %0, %1, %2 wave_shl:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+                         : "+v"(acc[c])
+                         : "v"(x[c + kx - 1]), "v"(w));
+        }
+    }
+}
+
+template <int W>
+__device__ __forceinline__ void tap_row_dyn(int q, float (&acc)[W], const float (&x)[W], float w) {
+    switch (q) {
+        case 0: tap_row<0, W>(acc, x, w); break;
+        case 1: tap_row<1, W>(acc, x, w); break;
+        case 2: tap_row<2, W>(acc, x, w); break;
+        case 3: tap_row<3, W>(acc, x, w); break;
+        case 4: tap_row<4, W>(acc, x, w); break;
+        case 5: tap_row<5, W>(acc, x, w); break;
+        case 6: tap_row<6, W>(acc, x, w); break;
+        case 7: tap_row<7, W>(acc, x, w); break;
+        default: tap_row<8, W>(acc, x, w); break;
+    }
+}
+
+struct RowCtx {
+    cs::Meta m;
+    __amdgpu_buffer_rsrc_t xr;   // x, bounded to its size
+    int chan_bytes;              // bytes of one input channel plane
+    int x_bytes;
+    uint32_t vo;                 // byte offset of this lane's row in channel 0 (2^31: padding lane)
+    bool valid;
+};
+
+template <int DT, int W>
+__device__ __forceinline__ void row_of(const RowCtx& c, int ci, RowWords<DT, W>& rw) {
+    // wave-uniform: an SGPR operand.  A malformed channel index reads zeros
+    // or other data of x, never memory outside it (range-checked loads).
+    const int soff = __builtin_amdgcn_readfirstlane(ci * c.chan_bytes);
+    load_words<DT, W>(c.xr, c.vo, soff, c.x_bytes, c.valid, rw);
+}
+
+// Kernels [k, e) of one pattern segment share (e > k), two per trip: the row
+// of one loads while the other's FMAs run; metadata is read two kernels
+// ahead; the single loop exit keeps the accumulators in place.
+template <int DT, int W, class TapFn>
+__device__ __forceinline__ void run_rows(const RowCtx& c, int k, int e, float (&acc)[W], TapFn taps) {
+    const int last = e - 1;
+    float wA[4], wB[4];
+    cs::meta_w<DT>(c.m, k, wA);
+    int kk = k + 1 <= last ? k + 1 : last;
+    int ciB = cs::meta_ci(c.m, kk);
+    cs::meta_w<DT>(c.m, kk, wB);
+    RowWords<DT, W> rA, rB;
+    row_of<DT, W>(c, cs::meta_ci(c.m, k), rA);
+    while (k + 1 < e) {
+        row_of<DT, W>(c, ciB, rB);                               // row of kernel k+1
+        kk = k + 2 <= last ? k + 2 : last;
+        const int ciA2 = cs::meta_ci(c.m, kk);
+        float wA2[4];
+        cs::meta_w<DT>(c.m, kk, wA2);
+        kk = k + 3 <= last ? k + 3 : last;
+        const int ciB2 = cs::meta_ci(c.m, kk);
+        float wB2[4];
+        cs::meta_w<DT>(c.m, kk, wB2);
+        {
+            float x[W];
+            unpack_row<DT, W>(rA, x);
+            settle_row<W>(x);
+            taps(acc, x, wA);                                    // kernel k
+        }
+        row_of<DT, W>(c, ciA2, rA);                              // row of kernel k+2
+        {
+            float x[W];
+            unpack_row<DT, W>(rB, x);
+            settle_row<W>(x);
+            taps(acc, x, wB);                                    // kernel k+1
+        }
+        k += 2;
+        wA[0] = wA2[0], wA[1] = wA2[1], wA[2] = wA2[2], wA[3] = wA2[3];
+        wB[0] = wB2[0], wB[1] = wB2[1], wB[2] = wB2[2], wB[3] = wB2[3];
+        ciB = ciB2;
+    }
+    if (k < e) {
+        float x[W];
+        unpack_row<DT, W>(rA, x);
+        settle_row<W>(x);
+        taps(acc, x, wA);
+    }
+}
+
+template <int DT, int W, int MASK>
+__device__ __forceinline__ void run_shape_rows(const RowCtx& c, int k, int e, float (&acc)[W]) {
+    constexpr int Q0 = NthBit<MASK, 0>::value(), Q1 = NthBit<MASK, 1>::value();
+    constexpr int Q2 = NthBit<MASK, 2>::value(), Q3 = NthBit<MASK, 3>::value();
+    run_rows<DT, W>(c, k, e, acc, [](float (&a)[W], const float (&x)[W], const float (&w)[4]) {
+        // the same-row taps first: they put FMAs between the settle and the
+        // DPP reads
+        if constexpr (Q0 / 3 == 1) tap_row<Q0, W>(a, x, w[0]);
+        if constexpr (Q1 / 3 == 1) tap_row<Q1, W>(a, x, w[1]);
+        if constexpr (Q2 / 3 == 1) tap_row<Q2, W>(a, x, w[2]);
+        if constexpr (Q3 / 3 == 1) tap_row<Q3, W>(a, x, w[3]);
+        if constexpr (Q0 / 3 != 1) tap_row<Q0, W>(a, x, w[0]);
+        if constexpr (Q1 / 3 != 1) tap_row<Q1, W>(a, x, w[1]);
+        if constexpr (Q2 / 3 != 1) tap_row<Q2, W>(a, x, w[2]);
+        if constexpr (Q3 / 3 != 1) tap_row<Q3, W>(a, x, w[3]);
+    });
+}
+
+// Any 4-of-9 mask: each tap is chosen per kernel by a uniform branch.
+template <int DT, int W>
+__device__ __forceinline__ void run_generic_rows(unsigned mask, const RowCtx& c, int k, int e, float (&acc)[W]) {
+    int q0 = 4, q1 = 4, q2 = 4, q3 = 4, seen = 0;
+#pragma unroll
+    for (int q = 0; q < 9; ++q) {
+        if ((mask >> q) & 1u) {
+            if (seen == 0) q0 = q;
+            else if (seen == 1) q1 = q;
+            else if (seen == 2) q2 = q;
+            else if (seen == 3) q3 = q;
+            ++seen;
+        }
+    }
+    run_rows<DT, W>(c, k, e, acc, [=](float (&a)[W], const float (&x)[W], const float (&w)[4]) {
+        tap_row_dyn<W>(q0, a, x, w[0]);
+        tap_row_dyn<W>(q1, a, x, w[1]);
+        tap_row_dyn<W>(q2, a, x, w[2]);
+        tap_row_dyn<W>(q3, a, x, w[3]);
+    });
+}
+
+#define PSC_ROWS_CASE(I) \
+    case I: run_shape_rows<DT, W, kCentre3.code[I]>(c, k, e, acc); return;
+#define PSC_ROWS_CASE8(I)                                                                           \
+    PSC_ROWS_CASE(I) PSC_ROWS_CASE(I + 1) PSC_ROWS_CASE(I + 2) PSC_ROWS_CASE(I + 3)                 \
+    PSC_ROWS_CASE(I + 4) PSC_ROWS_CASE(I + 5) PSC_ROWS_CASE(I + 6) PSC_ROWS_CASE(I + 7)
+
+template <int DT, int W>
+__device__ __forceinline__ void run_pattern_rows(int shape, unsigned mask, const RowCtx& c, int k, int e,
+                                                 float (&acc)[W]) {
+    switch (shape) {
+        PSC_ROWS_CASE8(0)
+        PSC_ROWS_CASE8(8)
+        PSC_ROWS_CASE8(16)
+        PSC_ROWS_CASE8(24)
+        PSC_ROWS_CASE8(32)
+        PSC_ROWS_CASE8(40)
+        PSC_ROWS_CASE8(48)
+        default: run_generic_rows<DT, W>(mask, c, k, e, acc); return;
+    }
+}
+#undef PSC_ROWS_CASE8
+#undef PSC_ROWS_CASE
+
+template <int DT, int W>
+__global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __restrict__ x,
+                                                   const int32_t* __restrict__ perm,
+                                                   const int32_t* __restrict__ seg_ptr,
+                                                   const int32_t* __restrict__ cin_idx,
+                                                   const typename Elt<DT>::T* __restrict__ vals,
+                                                   const typename Elt<DT>::T* __restrict__ bias,
+                                                   typename Elt<DT>::T* __restrict__ y, RGeo g) {
+    using E = Elt<DT>;
+    constexpr int ESZ = int(sizeof(typename E::T));
+    extern __shared__ float psc_rows_red[];   // KS > 1: [KS][W][64] partial sums
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+    const int gf = wave / g.KS, sp = wave - gf * g.KS;   // filter slot, share
+
+    // XCD-aware block order: the hardware deals consecutive blocks out to the
+    // 8 XCDs in turn; remap so that one XCD runs consecutive logical blocks,
+    // which share an image group (its rows stay in that XCD's L2) and differ
+    // in their filter group.
+    const int b = blockIdx.x;
+    int lb = b;
+    if (g.nblocks >= 8) {
+        const int per = g.nblocks / 8, rem = g.nblocks % 8;
+        const int xcd = b % 8, slot = b / 8;
+        lb = (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + slot;
+    }
+    const int fg = lb % g.groups_x, grp = lb / g.groups_x;
+    const int i = fg * g.FW + gf;                        // reordered filter of this wave
+    const bool has_filter = i < g.cout;
+
+    // ---- lane geometry: image s of the group, row r (r == H: the zero lane)
+    const int s = lane / g.seg_len, r = lane - s * g.seg_len;
+    const int img = grp * g.S + s;
+    const bool valid = s < g.S && img < g.n && r < g.H;
+    const int plane = g.H * g.W;
+
+    float acc[W];
+#pragma unroll
+    for (int c = 0; c < W; ++c) acc[c] = 0.f;
+
+    if (has_filter) {
+        const int* segp = seg_ptr + i * (g.m + 1);
+        const int f0 = segp[0], f1 = segp[g.m];
+        // share sp: the sp-th of KS equal contiguous ranges of the filter's kernels
+        const int len = f1 - f0;
+        const int s0 = f0 + len * sp / g.KS, s1 = f0 + len * (sp + 1) / g.KS;
+        RowCtx ctx;
+        ctx.m = cs::Meta{cs::scalar_rsrc(cin_idx, g.keep * 4), cs::scalar_rsrc(vals, g.keep * 4 * ESZ)};
+        ctx.xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<typename E::T*>(x), int16_t(0), g.x_bytes, 0x00020000);
+        ctx.chan_bytes = __builtin_amdgcn_readfirstlane(plane * ESZ);
+        ctx.x_bytes = g.x_bytes;
+        ctx.vo = valid ? uint32_t((img * g.cin * g.H + r) * g.W) * uint32_t(ESZ) : 0x80000000u;
+        ctx.valid = valid;
+        for (int p = 0; p < g.m; ++p) {
+            int k0 = segp[p], k1 = segp[p + 1];
+            k0 = k0 < s0 ? s0 : k0;
+            k1 = k1 > s1 ? s1 : k1;                     // malformed pointers stay in the share
+            if (k0 < k1) run_pattern_rows<DT, W>(g.shape[p], g.mask[p], ctx, k0, k1, acc);
+        }
+    }
+
+    // ---- add the KS partial sums of each filter in share order
+    if (g.KS > 1) {
+        float (*red)[W][64] = reinterpret_cast<float (*)[W][64]>(psc_rows_red);
+        for (int slot = 0; slot < g.FW; ++slot) {
+            if (slot == gf) {
+#pragma unroll
+                for (int c = 0; c < W; ++c) red[sp][c][lane] = acc[c];
+            }
+            __syncthreads();
+            if (slot == gf) {
+#pragma unroll
+                for (int c = 0; c < W; ++c) {
+                    float v = 0.f;
+                    for (int t = 0; t < g.KS; ++t) v += red[t][c][lane];
+                    acc[c] = v;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    if (!has_filter || !valid) return;
+    const int f = perm[i];
+    const float bv = bias ? E::load(bias, f) : 0.f;
+    typename E::T* yp = y + (int64_t(img) * g.cout + f) * plane + r * g.W;
+#pragma unroll
+    for (int c = 0; c < W; ++c) {
+        // the KS waves of a filter hold the same sums; share t stores columns t, t+KS, ...
+        if ((c % g.KS) == sp) {
+            float v = acc[c] + bv;
+            if (g.relu) v = v > 0.f ? v : 0.f;
+            yp[c] = E::from_f(v);
+        }
+    }
+}
+
+template <int DT, int W>
+hipError_t launch_rows(const PackedView& pk, const ConvArgs& a, const RGeo& g, hipStream_t stream) {
+    using T = typename Elt<DT>::T;
+    const int waves = g.FW * g.KS;
+    const size_t smem = g.KS > 1 ? size_t(g.KS) * W * 64 * sizeof(float) : 0;
+    hipLaunchKernelGGL((k_conv_rows<DT, W>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)), smem, stream,
+                       static_cast<const T*>(a.x), pk.filter_perm, pk.seg_ptr, pk.cin_idx,
+                       static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), static_cast<T*>(a.y), g);
+    return hipGetLastError();
+}
+
+}  // namespace rw
+}  // namespace psc

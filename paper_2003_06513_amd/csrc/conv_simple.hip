@@ -11,6 +11,9 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
 bool describe_conv_stream(const PatTable& tab, const ConvArgs& a, ConvForm& out);
 hipError_t launch_conv_stride2(const PatTable& tab, const PackedView& pk, const ConvArgs& a, hipStream_t stream);
 bool describe_conv_stride2(const PatTable& tab, const ConvArgs& a, ConvForm& out);
+hipError_t launch_conv_rows(const PatTable& tab, const PackedView& pk, const ConvArgs& a, hipStream_t stream);
+bool describe_conv_rows(const PatTable& tab, const ConvArgs& a, ConvForm& out);
+bool prefer_conv_rows(const PatTable& tab, const ConvArgs& a);
 
 namespace {
 
@@ -168,6 +171,11 @@ hipError_t conv_simple(const PatTable& tab, const PackedView& pk, const ConvArgs
 
 hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs& a, int algo,
                        hipStream_t stream) {
+    // algo 2: the one-row-per-lane kernel (the caller has checked that it
+    // takes the call)
+    if (algo == 2 || (algo == 0 && prefer_conv_rows(tab, a))) return launch_conv_rows(tab, pk, a, stream);
+    // algo 3: the column-per-lane tuned kernels, whatever the shape
+    if (algo == 3) algo = 0;
     if (algo == 0 && a.stride == 1) {
         const hipError_t e = launch_conv_stream(tab, pk, a, stream);
         if (e != hipErrorNotSupported) return e;
@@ -184,7 +192,14 @@ hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs
                              : conv_simple<DT_F32>(tab, pk, a, stream);
 }
 
+bool conv_rows_takes(const PatTable& tab, const ConvArgs& a) {
+    ConvForm f;
+    return describe_conv_rows(tab, a, f);
+}
+
 void describe_conv(const PatTable& tab, const ConvArgs& a, int algo, ConvForm& out) {
+    if ((algo == 2 || (algo == 0 && prefer_conv_rows(tab, a))) && describe_conv_rows(tab, a, out)) return;
+    if (algo == 3) algo = 0;
     if (algo == 0 && a.stride == 1 && describe_conv_stream(tab, a, out)) return;
     if (algo == 0 && a.stride == 2 && describe_conv_stride2(tab, a, out)) return;
     const int outs = a.pool ? (a.h / 2) * (a.w / 2) : ((a.h - 1) / a.stride + 1) * ((a.w - 1) / a.stride + 1);

@@ -67,12 +67,14 @@ hipError_t launch_conv(const PatTable& tab, const PackedView& pk, const ConvArgs
 
 // The launch configuration launch_conv would use (host only, no device work).
 struct ConvForm {
-    int kernel;             // 0 k_conv_stream, 1 k_conv_wide, 2 k_conv_simple, 3 k_conv_stride2
+    int kernel;             // 0 k_conv_stream, 1 k_conv_wide, 2 k_conv_simple, 3 k_conv_stride2, 4 k_conv_rows
     int staged;             // 0 direct loads, 1 rows staged through LDS, 2 staged, several runs per wave
     int rows_per_lane, cols_per_lane, segments_per_wave, column_tiles;
     int shares, filters_per_block, blocks, threads_per_block;
 };
 void describe_conv(const PatTable& tab, const ConvArgs& a, int algo, ConvForm& out);
+// Whether the one-row-per-lane kernel (algo 2) takes the call (host only).
+bool conv_rows_takes(const PatTable& tab, const ConvArgs& a);
 // Sec. 3.3 retraining: the transposed, rotated layer (for dx) and the masked
 // weight gradient.
 hipError_t launch_transpose_prep(int dtype, int cout, int cin, const void* w, const uint8_t* pat,

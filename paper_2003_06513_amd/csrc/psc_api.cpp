@@ -292,7 +292,7 @@ static psc_status check_conv_shape(const psc_layer* L, int32_t act_dtype, int32_
     if (n < 0 || n > 65535) return fail(PSC_ERR_ARG, "n=%d outside 0..65535", n);
     if (h < 1 || w < 1 || h > 32768 || w > 32768)
         return fail(PSC_ERR_ARG, "h=%d, w=%d outside 1..32768", h, w);
-    if (algo < 0 || algo > 1) return fail(PSC_ERR_ARG, "algo=%d is not 0 or 1", algo);
+    if (algo < 0 || algo > 3) return fail(PSC_ERR_ARG, "algo=%d is not 0, 1, 2 or 3", algo);
     if (pool && ((h & 1) || (w & 1))) return fail(PSC_ERR_ARG, "h=%d, w=%d must be even for the 2x2 pool", h, w);
     if (stride != 1 && stride != 2) return fail(PSC_ERR_ARG, "stride=%d is not 1 or 2", stride);
     const int64_t plane = int64_t(h) * w;
@@ -301,6 +301,14 @@ static psc_status check_conv_shape(const psc_layer* L, int32_t act_dtype, int32_
     if (xe > kMaxElems || ye > kMaxElems)
         return fail(PSC_ERR_ARG, "x or y holds more than 2^31-1 elements");
     if (pool && stride != 1) return fail(PSC_ERR_ARG, "the fused 2x2 pool needs stride 1");
+    if (algo == 2) {
+        const psc::ConvArgs a{act_dtype, n, L->cin, h, w, L->cout, L->keep, nullptr, nullptr, 0, nullptr, pool, stride};
+        if (!psc::conv_rows_takes(table_of(L), a))
+            return fail(PSC_ERR_UNSUPPORTED,
+                        "algo 2 (one row per lane) needs stride 1, no pool, h <= 63 and w in {4, 7, 8, 14, 16, 28} "
+                        "(fp16: w even or 7); got h=%d, w=%d, stride=%d, pool=%d",
+                        h, w, stride, pool);
+    }
     return PSC_OK;
 }
 

@@ -158,7 +158,8 @@ def form_cases():
     form, column tiles or full rows, split filters, pooled epilogue, rows per
     lane, dtype -- the smallest shape (n, cin, cout, h, w) of a fixed grid
     that takes it, found with the host-side configuration query; plus the
-    stride-2 and algo-1 simple kernel.  Returns a sorted list of
+    stride-2 kernel, the one-row-per-lane kernel (algo 2) and the algo-1
+    simple kernel.  Returns a sorted list of
     (key, n, cin, cout, h, w, dtype_code, pool, stride, algo)."""
     found = {}
     for n in (1, 2, 3, 4, 8):
@@ -183,6 +184,19 @@ def form_cases():
             L = B.Layer(cout, cin, list(FORM_MASKS), cin * cout // 2, dt)
             cfg = B.conv3x3_config(L, dt, n, h, w, False, 2, 0)
             out.append((("stride2", cfg["kernel"], cfg["shares"] > 1), n, cin, cout, h, w, dt, False, 2, 0))
+        # the one-row-per-lane kernel (algo 2) at every compiled width: ragged
+        # image groups, a partial wave, split filters, rows unequal to columns,
+        # and (fp16, width 7, odd cin and n) the last row of x read through a
+        # window that reaches past the end of x
+        rows_shapes = ((13, 5, 6, 4, 4), (1, 40, 5, 4, 4), (9, 7, 5, 7, 7), (5, 3, 4, 7, 7), (3, 33, 6, 7, 7),
+                       (8, 16, 9, 8, 8), (4, 24, 4, 5, 8), (5, 6, 7, 14, 14), (2, 48, 3, 13, 14),
+                       (4, 10, 6, 16, 16), (1, 64, 4, 11, 16), (3, 9, 5, 28, 28), (1, 40, 3, 20, 28))
+        for n, cin, cout, h, w in rows_shapes:
+            if dt == B.PSC_F16 and (w & 1) and w != 7:
+                continue
+            L = B.Layer(cout, cin, list(FORM_MASKS), cin * cout // 2, dt)
+            cfg = B.conv3x3_config(L, dt, n, h, w, False, 1, 2)
+            out.append((("rows", cfg["kernel"], w, cfg["shares"] > 1), n, cin, cout, h, w, dt, False, 1, 2))
         out.append((("simple-stride2",), 2, 9, 7, 13, 11, dt, False, 2, 0))
         out.append((("simple-algo1",), 2, 9, 7, 13, 11, dt, False, 1, 1))
         out.append((("simple-algo1-pool",), 2, 9, 7, 12, 10, dt, True, 1, 1))

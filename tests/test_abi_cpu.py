@@ -136,6 +136,10 @@ def test_conv_validation(L):
                                  ctypes.c_void_p(0x20000), None) == B.PSC_ERR_ARG
     assert L.psc_conv3x3_fwd_algo(lay.ref(), ctypes.byref(cp), B.PSC_F32, FAKE, 1, 4, 4, None, 0,
                                   ctypes.c_void_p(0x20000), 5, None) == B.PSC_ERR_ARG
+    # the one-row-per-lane kernel has no variant for 5 columns
+    rc, msg = _status(L.psc_conv3x3_fwd_algo(lay.ref(), ctypes.byref(cp), B.PSC_F32, FAKE, 1, 4, 5, None, 0,
+                                             ctypes.c_void_p(0x20000), 2, None))
+    assert rc == B.PSC_ERR_UNSUPPORTED and "algo 2" in msg
     # output overlapping the input
     rc, msg = _status(L.psc_conv3x3_fwd(lay.ref(), ctypes.byref(cp), B.PSC_F32, FAKE, 1, 4, 4, None, 0,
                                         ctypes.c_void_p(FAKE.value + 8), None))

@@ -68,7 +68,14 @@ def test_form_search_reaches_every_form():
     assert any(k[0] == 1 and k[3] for k in keys) and any(k[0] == 1 and k[4] for k in keys)
     assert any(k[2] for k in keys)                                                         # column tiles
     assert {c[0][0] for c in cases if not isinstance(c[0][0], int)} == \
-        {"stride2", "simple-stride2", "simple-algo1", "simple-algo1-pool"}
+        {"stride2", "rows", "simple-stride2", "simple-algo1", "simple-algo1-pool"}
+    rows = [c for c in cases if c[0][0] == "rows"]
+    assert all(c[0][1] == 4 for c in rows)
+    for dt in (B.PSC_F32, B.PSC_F16):
+        assert {c[5] for c in rows if c[6] == dt} == {4, 7, 8, 14, 16, 28}
+        assert any(c[0][3] for c in rows if c[6] == dt) and any(not c[0][3] for c in rows if c[6] == dt)
+    # the automatic choice takes the rows kernel for whole-wave batches on small planes
+    assert any(isinstance(c[0][0], int) and c[0][0] == 4 for c in cases)
     s2 = [c[0] for c in cases if c[0][0] == "stride2"]
     assert all(k[1] == 3 for k in s2) and any(k[2] for k in s2) and any(not k[2] for k in s2)
 
@@ -77,9 +84,16 @@ def test_config_query_validates():
     L = B.Layer(8, 4, [23, 282], 10, B.PSC_F32)
     for args in [(B.PSC_F16, 1, 8, 8, False, 1, 0), (B.PSC_F32, 1, 8, 8, False, 3, 0),
                  (B.PSC_F32, 1, 7, 8, True, 1, 0), (B.PSC_F32, 1, 8, 8, True, 2, 0),
-                 (B.PSC_F32, 1, 8, 8, False, 1, 2), (B.PSC_F32, -1, 8, 8, False, 1, 0)]:
+                 (B.PSC_F32, 1, 8, 8, False, 1, 4), (B.PSC_F32, 1, 8, 9, False, 1, 2),
+                 (B.PSC_F32, 1, 8, 8, True, 1, 2), (B.PSC_F32, 1, 8, 8, False, 2, 2),
+                 (B.PSC_F32, 1, 64, 8, False, 1, 2), (B.PSC_F32, -1, 8, 8, False, 1, 0)]:
         with pytest.raises(B.PscError):
             B.conv3x3_config(L, *args)
     assert B.conv3x3_config(L, B.PSC_F32, 2, 16, 16, False, 2, 0)["kernel"] == 3      # tuned stride 2
     assert B.conv3x3_config(L, B.PSC_F32, 2, 16, 15, False, 2, 0)["kernel"] == 2      # odd width
     assert B.conv3x3_config(L, B.PSC_F32, 2, 16, 16, False, 2, 1)["kernel"] == 2      # algo 1
+    assert B.conv3x3_config(L, B.PSC_F32, 1, 8, 8, False, 1, 2)["kernel"] == 4        # algo 2: one row per lane
+    assert B.conv3x3_config(L, B.PSC_F32, 7, 8, 8, False, 1, 0)["kernel"] == 4        # a whole wave of images
+    assert B.conv3x3_config(L, B.PSC_F32, 6, 8, 8, False, 1, 0)["kernel"] == 0        # less than a wave
+    assert B.conv3x3_config(L, B.PSC_F32, 7, 8, 8, False, 1, 3)["kernel"] == 0        # algo 3: column per lane
+    assert B.conv3x3_config(L, B.PSC_F32, 64, 28, 28, False, 1, 0)["kernel"] == 0     # wider than 16
