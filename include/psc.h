@@ -170,8 +170,9 @@ psc_status psc_conv3x3_fwd(const psc_layer *layer, const psc_packed *packed,
  * 2 = the one-row-per-lane kernel, which algo 0 picks for batches that fill
  * a wave with whole images on planes of at most 16 columns, 3 = the
  * column-per-lane tuned kernels (algo 0 without that choice).  Algo 2 needs
- * stride 1, no pool, h <= 63 and w in {4, 7, 8, 14, 16, 28} (fp16: w even,
- * or 7), else PSC_ERR_UNSUPPORTED. */
+ * no pool, at most 63 output rows and w in {4, 7, 8, 14, 16, 28} (fp16: w
+ * even, or 7); with stride 2 (psc_conv3x3_fwd_strided) w in {8, 16, 32};
+ * else PSC_ERR_UNSUPPORTED. */
 psc_status psc_conv3x3_fwd_algo(const psc_layer *layer, const psc_packed *packed,
                                 int32_t act_dtype, const void *d_x, int32_t n,
                                 int32_t h, int32_t w, const void *d_bias,
@@ -195,9 +196,9 @@ psc_status psc_conv3x3_fwd_pool2(const psc_layer *layer, const psc_packed *packe
  *   y[n,f,i,j] = sigma(b[f] + sum over kept (ci, p) of f of
  *                sum_{(r,s) in p} v * x[n, ci, stride*i + r - 1, stride*j + s - 1])
  * with out-of-image taps reading zero.  stride 1 is psc_conv3x3_fwd_algo.
- * Stride 2 with algo 0 runs the tuned stride-2 kernel for even widths of at
- * most 126 columns (the one-output-per-lane kernel otherwise, and always
- * with algo 1).  Other
+ * Stride 2 with algo 0 or 3 runs the tuned stride-2 kernel for even widths
+ * of at most 126 columns (the one-output-per-lane kernel otherwise, and
+ * always with algo 1); algo 2 the one-row-per-lane kernel.  Other
  * conventions and errors as in psc_conv3x3_fwd_algo; a stride other than 1
  * or 2 returns PSC_ERR_ARG. */
 psc_status psc_conv3x3_fwd_strided(const psc_layer *layer, const psc_packed *packed,

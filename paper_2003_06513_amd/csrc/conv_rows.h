@@ -18,6 +18,11 @@
 // the padding row below image s and above image s+1.  Padding columns cost
 // nothing: the FMAs that would read them are left out at compile time.
 //
+// Stride 2 (ST = 2; the stage-entry convolutions): a lane owns output row i,
+// OW = W/2 columns; it loads input rows 2i and 2i+1 (W values each) and takes
+// row 2i-1 -- the odd row of the lane to the left -- by DPP.  Output column c
+// reads input columns 2c-1, 2c and 2c+1, all registers of the lane.
+//
 // As in the other kernels, one wave walks one reordered filter's compressed
 // storage (filter kernel reorder, compressed weight storage): pattern segment
 // by pattern segment, each through a loop compiled for its centre+3 shape,
@@ -36,8 +41,9 @@ constexpr int kMaxShares = 8;
 
 struct RGeo {
     int n, cin, H, W, cout, m;
+    int ST, OH, OW; // stride, output rows and columns
     int S;          // images per wave
-    int seg_len;    // lanes per image: H rows + 1 zero lane
+    int seg_len;    // lanes per image: OH rows + 1 zero lane
     int groups;     // image groups: ceil(n / S)
     int FW, KS;     // filters and shares per filter in a workgroup
     int groups_x;   // filter groups (fastest varying logical block index)
@@ -53,27 +59,51 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// Raw words of one lane's input row.  fp16 rows of odd width start at a
-// 2-byte boundary: the lane loads the 16-byte window from the 4-byte boundary
-// at or below the row start and shifts it by the 2 bytes if needed.
-template <int DT, int W>
+// Raw words of one lane's input row(s): stride 1, the row; stride 2, the even
+// row then the odd row.  fp16 rows of odd width start at a 2-byte boundary:
+// the lane loads the 16-byte window from the 4-byte boundary at or below the
+// row start and shifts it by the 2 bytes if needed.
+template <int DT, int W, int ST>
 struct RowWords {
     static constexpr int ESZ = DT == DT_F32 ? 4 : 2;
     static constexpr bool ODD = DT == DT_F16 && (W & 1);
-    static constexpr int BYTES = ODD ? 16 : W * ESZ;
-    static constexpr int NW = BYTES / 4;
+    static constexpr int BYTES = ODD ? 16 : W * ESZ;   // per row
+    static constexpr int NW = BYTES / 4;               // words per row
     static_assert(BYTES % 4 == 0, "rows are loaded in whole dwords");
     static_assert(!ODD || W <= 7, "the shifted window holds 7 halves");
-    uint32_t d[NW];
+    static_assert(ST == 1 || (!ODD && W % 2 == 0), "stride-2 rows have an even width");
+    uint32_t d[ST * NW];
     uint32_t sh;   // ODD: 0 or 16, the bit shift of the row start in the window
 };
 
-// Load the words at byte offset vo + soff (a buffer load returns zero for any
-// offset past the range of x: padding lanes pass 2^31).
-template <int DT, int W>
-__device__ __forceinline__ void load_words(__amdgpu_buffer_rsrc_t xr, uint32_t vo, int soff, int x_bytes,
-                                           bool valid, RowWords<DT, W>& rw) {
-    using RWd = RowWords<DT, W>;
+// Whole-row loads of BYTES bytes at byte offset vo + soff into d[0..BYTES/4).
+template <int BYTES>
+__device__ __forceinline__ void load_row_words(__amdgpu_buffer_rsrc_t xr, uint32_t vo, int soff, uint32_t* d) {
+#pragma unroll
+    for (int o = 0; o < BYTES; o += 16) {
+        const int left = BYTES - o;
+        if (left >= 16) {
+            const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(xr, int(vo + o), soff, 0);
+            d[o / 4] = v.x, d[o / 4 + 1] = v.y, d[o / 4 + 2] = v.z, d[o / 4 + 3] = v.w;
+        } else if (left == 12) {
+            const u32x3 v = __builtin_amdgcn_raw_buffer_load_b96(xr, int(vo + o), soff, 0);
+            d[o / 4] = v.x, d[o / 4 + 1] = v.y, d[o / 4 + 2] = v.z;
+        } else if (left == 8) {
+            const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(xr, int(vo + o), soff, 0);
+            d[o / 4] = v.x, d[o / 4 + 1] = v.y;
+        } else {
+            d[o / 4] = __builtin_amdgcn_raw_buffer_load_b32(xr, int(vo + o), soff, 0);
+        }
+    }
+}
+
+// Load the words at byte offset vo + soff (and, stride 2, the odd row at
+// vo2 + soff).  A buffer load returns zero for any offset past the range of
+// x: padding lanes and rows pass 2^31.
+template <int DT, int W, int ST>
+__device__ __forceinline__ void load_words(__amdgpu_buffer_rsrc_t xr, uint32_t vo, uint32_t vo2, int soff,
+                                           int x_bytes, bool valid, RowWords<DT, W, ST>& rw) {
+    using RWd = RowWords<DT, W, ST>;
     if constexpr (RWd::ODD) {
         const uint32_t t = vo + uint32_t(soff);
         const uint32_t at = t & ~3u;
@@ -88,40 +118,34 @@ __device__ __forceinline__ void load_words(__amdgpu_buffer_rsrc_t xr, uint32_t v
             rw.d[3] = (rw.d[3] & 0xffff0000u) | h;
         }
     } else {
-#pragma unroll
-        for (int o = 0; o < RWd::BYTES; o += 16) {
-            const int left = RWd::BYTES - o;
-            if (left >= 16) {
-                const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(xr, int(vo + o), soff, 0);
-                rw.d[o / 4] = v.x, rw.d[o / 4 + 1] = v.y, rw.d[o / 4 + 2] = v.z, rw.d[o / 4 + 3] = v.w;
-            } else if (left == 12) {
-                const u32x3 v = __builtin_amdgcn_raw_buffer_load_b96(xr, int(vo + o), soff, 0);
-                rw.d[o / 4] = v.x, rw.d[o / 4 + 1] = v.y, rw.d[o / 4 + 2] = v.z;
-            } else if (left == 8) {
-                const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(xr, int(vo + o), soff, 0);
-                rw.d[o / 4] = v.x, rw.d[o / 4 + 1] = v.y;
-            } else {
-                rw.d[o / 4] = __builtin_amdgcn_raw_buffer_load_b32(xr, int(vo + o), soff, 0);
-            }
-        }
+        load_row_words<RWd::BYTES>(xr, vo, soff, rw.d);
+        if constexpr (ST == 2) load_row_words<RWd::BYTES>(xr, vo2, soff, rw.d + RWd::NW);
     }
 }
 
-// The W input values of the row as fp32 (fp16 widened exactly).
+// The input values as fp32 (fp16 widened exactly): e, the row (stride 2:
+// the even row); o, stride 2 only, the odd row.
+template <int W, int ST>
+struct RowVals {
+    float e[W];
+    float o[ST == 2 ? W : 1];
+};
+
 template <int DT, int W>
-__device__ __forceinline__ void unpack_row(const RowWords<DT, W>& rw, float (&x)[W]) {
+__device__ __forceinline__ void unpack_words(const uint32_t* d, uint32_t sh, float (&x)[W]) {
+    constexpr int NW = RowWords<DT, W, 1>::NW;
     if constexpr (DT == DT_F32) {
 #pragma unroll
-        for (int j = 0; j < W; ++j) x[j] = __builtin_bit_cast(float, rw.d[j]);
+        for (int j = 0; j < W; ++j) x[j] = __builtin_bit_cast(float, d[j]);
     } else {
-        uint32_t s[RowWords<DT, W>::NW];
-        if constexpr (RowWords<DT, W>::ODD) {
+        uint32_t s[NW];
+        if constexpr (RowWords<DT, W, 1>::ODD) {
 #pragma unroll
-            for (int i = 0; i + 1 < RowWords<DT, W>::NW; ++i) s[i] = __builtin_amdgcn_alignbit(rw.d[i + 1], rw.d[i], rw.sh);
-            s[RowWords<DT, W>::NW - 1] = rw.d[RowWords<DT, W>::NW - 1] >> rw.sh;
+            for (int i = 0; i + 1 < NW; ++i) s[i] = __builtin_amdgcn_alignbit(d[i + 1], d[i], sh);
+            s[NW - 1] = d[NW - 1] >> sh;
         } else {
 #pragma unroll
-            for (int i = 0; i < RowWords<DT, W>::NW; ++i) s[i] = rw.d[i];
+            for (int i = 0; i < NW; ++i) s[i] = d[i];
         }
 #pragma unroll
         for (int j = 0; j < W; ++j)
@@ -129,60 +153,82 @@ __device__ __forceinline__ void unpack_row(const RowWords<DT, W>& rw, float (&x)
     }
 }
 
-// After the row values are final: an asm the compiler sees as writing them
-// (so no VALU write of a row value can follow), then the two wait states a
+// After the values are final: an asm the compiler sees as writing the DPP
+// source row (so no VALU write of it can follow), then the two wait states a
 // DPP read needs after a VALU write of its source.
 template <int W>
 __device__ __forceinline__ void settle_row(float (&x)[W]) {
 #pragma unroll
     for (int j = 0; j < W; j += 4) {
-        if constexpr (W % 4 == 0) {
-            asm volatile("" : "+v"(x[j]), "+v"(x[j + 1]), "+v"(x[j + 2]), "+v"(x[j + 3]));
-        } else {
-            if (j + 3 < W) asm volatile("" : "+v"(x[j]), "+v"(x[j + 1]), "+v"(x[j + 2]), "+v"(x[j + 3]));
-            else
-                for (int t = j; t < W; ++t) asm volatile("" : "+v"(x[t]));
-        }
+        if (j + 3 < W) asm volatile("" : "+v"(x[j]), "+v"(x[j + 1]), "+v"(x[j + 2]), "+v"(x[j + 3]));
+        else
+            for (int t = j; t < W; ++t) asm volatile("" : "+v"(x[t]));
     }
     asm volatile("s_nop 1");
 }
 
-// The tap at kernel position Q = 3 ky + kx: acc[c] += w * x(row r + ky - 1,
-// column c + kx - 1).  Row r - 1 is the lane to the left (wave_shr), row r + 1
-// the lane to the right (wave_shl); lanes without a neighbour read zero
-// (bound_ctrl).  Columns outside the row are skipped.
-template <int Q, int W>
-__device__ __forceinline__ void tap_row(float (&acc)[W], const float (&x)[W], float w) {
-    constexpr int ky = Q / 3, kx = Q % 3;
-    constexpr int c0 = kx == 0 ? 1 : 0, c1 = kx == 2 ? W - 1 : W;
-#pragma unroll
-    for (int c = c0; c < c1; ++c) {
-        if constexpr (ky == 1) {
-            acc[c] = __builtin_fmaf(w, x[c + kx - 1], acc[c]);
-        } else if constexpr (ky == 0) {
-            asm volatile("v_fmac_f32_dpp %0, %1, %2 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
-                         : "+v"(acc[c])
-                         : "v"(x[c + kx - 1]), "v"(w));
-        } else {
-            asm volatile("v_fmac_f32_dpp %0, %1, %2 wave_shl:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
-                         : "+v"(acc[c])
-                         : "v"(x[c + kx - 1]), "v"(w));
-        }
+template <int DT, int W, int ST>
+__device__ __forceinline__ void unpack_vals(const RowWords<DT, W, ST>& rw, RowVals<W, ST>& v) {
+    unpack_words<DT, W>(rw.d, rw.sh, v.e);
+    if constexpr (ST == 2) {
+        unpack_words<DT, W>(rw.d + RowWords<DT, W, ST>::NW, 0u, v.o);
+        settle_row<W>(v.o);
+    } else {
+        settle_row<W>(v.e);
     }
 }
 
-template <int W>
-__device__ __forceinline__ void tap_row_dyn(int q, float (&acc)[W], const float (&x)[W], float w) {
+// The tap at kernel position Q = 3 ky + kx, stride 1: acc[c] += w * x(row
+// r + ky - 1, column c + kx - 1).  Row r - 1 is the lane to the left
+// (wave_shr), row r + 1 the lane to the right (wave_shl); lanes without a
+// neighbour read zero (bound_ctrl).  Columns outside the row are skipped.
+// Stride 2: acc[c] += w * x(row 2i + ky - 1, column 2c + kx - 1) with row
+// 2i - 1 the odd row of the lane to the left, 2i the even and 2i + 1 the odd
+// row of the lane.
+#define PSC_DPP_SHR "v_fmac_f32_dpp %0, %1, %2 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+#define PSC_DPP_SHL "v_fmac_f32_dpp %0, %1, %2 wave_shl:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+template <int Q, int W, int ST>
+__device__ __forceinline__ void tap_row(float (&acc)[W / ST], const RowVals<W, ST>& x, float w) {
+    constexpr int ky = Q / 3, kx = Q % 3;
+    if constexpr (ST == 1) {
+        constexpr int c0 = kx == 0 ? 1 : 0, c1 = kx == 2 ? W - 1 : W;
+#pragma unroll
+        for (int c = c0; c < c1; ++c) {
+            if constexpr (ky == 1)
+                acc[c] = __builtin_fmaf(w, x.e[c + kx - 1], acc[c]);
+            else if constexpr (ky == 0)
+                asm volatile(PSC_DPP_SHR : "+v"(acc[c]) : "v"(x.e[c + kx - 1]), "v"(w));
+            else
+                asm volatile(PSC_DPP_SHL : "+v"(acc[c]) : "v"(x.e[c + kx - 1]), "v"(w));
+        }
+    } else {
+        constexpr int c0 = kx == 0 ? 1 : 0;
+#pragma unroll
+        for (int c = c0; c < W / 2; ++c) {
+            if constexpr (ky == 0)
+                asm volatile(PSC_DPP_SHR : "+v"(acc[c]) : "v"(x.o[2 * c + kx - 1]), "v"(w));
+            else if constexpr (ky == 1)
+                acc[c] = __builtin_fmaf(w, x.e[2 * c + kx - 1], acc[c]);
+            else
+                acc[c] = __builtin_fmaf(w, x.o[2 * c + kx - 1], acc[c]);
+        }
+    }
+}
+#undef PSC_DPP_SHL
+#undef PSC_DPP_SHR
+
+template <int W, int ST>
+__device__ __forceinline__ void tap_row_dyn(int q, float (&acc)[W / ST], const RowVals<W, ST>& x, float w) {
     switch (q) {
-        case 0: tap_row<0, W>(acc, x, w); break;
-        case 1: tap_row<1, W>(acc, x, w); break;
-        case 2: tap_row<2, W>(acc, x, w); break;
-        case 3: tap_row<3, W>(acc, x, w); break;
-        case 4: tap_row<4, W>(acc, x, w); break;
-        case 5: tap_row<5, W>(acc, x, w); break;
-        case 6: tap_row<6, W>(acc, x, w); break;
-        case 7: tap_row<7, W>(acc, x, w); break;
-        default: tap_row<8, W>(acc, x, w); break;
+        case 0: tap_row<0, W, ST>(acc, x, w); break;
+        case 1: tap_row<1, W, ST>(acc, x, w); break;
+        case 2: tap_row<2, W, ST>(acc, x, w); break;
+        case 3: tap_row<3, W, ST>(acc, x, w); break;
+        case 4: tap_row<4, W, ST>(acc, x, w); break;
+        case 5: tap_row<5, W, ST>(acc, x, w); break;
+        case 6: tap_row<6, W, ST>(acc, x, w); break;
+        case 7: tap_row<7, W, ST>(acc, x, w); break;
+        default: tap_row<8, W, ST>(acc, x, w); break;
     }
 }
 
@@ -191,33 +237,34 @@ struct RowCtx {
     __amdgpu_buffer_rsrc_t xr;   // x, bounded to its size
     int chan_bytes;              // bytes of one input channel plane
     int x_bytes;
-    uint32_t vo;                 // byte offset of this lane's row in channel 0 (2^31: padding lane)
+    uint32_t vo;                 // byte offset of this lane's (even) row in channel 0 (2^31: padding)
+    uint32_t vo2;                // stride 2: the odd row (2^31: padding)
     bool valid;
 };
 
-template <int DT, int W>
-__device__ __forceinline__ void row_of(const RowCtx& c, int ci, RowWords<DT, W>& rw) {
+template <int DT, int W, int ST>
+__device__ __forceinline__ void row_of(const RowCtx& c, int ci, RowWords<DT, W, ST>& rw) {
     // wave-uniform: an SGPR operand.  A malformed channel index reads zeros
     // or other data of x, never memory outside it (range-checked loads).
     const int soff = __builtin_amdgcn_readfirstlane(ci * c.chan_bytes);
-    load_words<DT, W>(c.xr, c.vo, soff, c.x_bytes, c.valid, rw);
+    load_words<DT, W, ST>(c.xr, c.vo, c.vo2, soff, c.x_bytes, c.valid, rw);
 }
 
 // Kernels [k, e) of one pattern segment share (e > k), two per trip: the row
 // of one loads while the other's FMAs run; metadata is read two kernels
 // ahead; the single loop exit keeps the accumulators in place.
-template <int DT, int W, class TapFn>
-__device__ __forceinline__ void run_rows(const RowCtx& c, int k, int e, float (&acc)[W], TapFn taps) {
+template <int DT, int W, int ST, class TapFn>
+__device__ __forceinline__ void run_rows(const RowCtx& c, int k, int e, float (&acc)[W / ST], TapFn taps) {
     const int last = e - 1;
     float wA[4], wB[4];
     cs::meta_w<DT>(c.m, k, wA);
     int kk = k + 1 <= last ? k + 1 : last;
     int ciB = cs::meta_ci(c.m, kk);
     cs::meta_w<DT>(c.m, kk, wB);
-    RowWords<DT, W> rA, rB;
-    row_of<DT, W>(c, cs::meta_ci(c.m, k), rA);
+    RowWords<DT, W, ST> rA, rB;
+    row_of<DT, W, ST>(c, cs::meta_ci(c.m, k), rA);
     while (k + 1 < e) {
-        row_of<DT, W>(c, ciB, rB);                               // row of kernel k+1
+        row_of<DT, W, ST>(c, ciB, rB);                           // row of kernel k+1
         kk = k + 2 <= last ? k + 2 : last;
         const int ciA2 = cs::meta_ci(c.m, kk);
         float wA2[4];
@@ -227,16 +274,14 @@ __device__ __forceinline__ void run_rows(const RowCtx& c, int k, int e, float (&
         float wB2[4];
         cs::meta_w<DT>(c.m, kk, wB2);
         {
-            float x[W];
-            unpack_row<DT, W>(rA, x);
-            settle_row<W>(x);
+            RowVals<W, ST> x;
+            unpack_vals<DT, W, ST>(rA, x);
             taps(acc, x, wA);                                    // kernel k
         }
-        row_of<DT, W>(c, ciA2, rA);                              // row of kernel k+2
+        row_of<DT, W, ST>(c, ciA2, rA);                          // row of kernel k+2
         {
-            float x[W];
-            unpack_row<DT, W>(rB, x);
-            settle_row<W>(x);
+            RowVals<W, ST> x;
+            unpack_vals<DT, W, ST>(rB, x);
             taps(acc, x, wB);                                    // kernel k+1
         }
         k += 2;
@@ -245,34 +290,35 @@ __device__ __forceinline__ void run_rows(const RowCtx& c, int k, int e, float (&
         ciB = ciB2;
     }
     if (k < e) {
-        float x[W];
-        unpack_row<DT, W>(rA, x);
-        settle_row<W>(x);
+        RowVals<W, ST> x;
+        unpack_vals<DT, W, ST>(rA, x);
         taps(acc, x, wA);
     }
 }
 
-template <int DT, int W, int MASK>
-__device__ __forceinline__ void run_shape_rows(const RowCtx& c, int k, int e, float (&acc)[W]) {
+template <int DT, int W, int ST, int MASK>
+__device__ __forceinline__ void run_shape_rows(const RowCtx& c, int k, int e, float (&acc)[W / ST]) {
     constexpr int Q0 = NthBit<MASK, 0>::value(), Q1 = NthBit<MASK, 1>::value();
     constexpr int Q2 = NthBit<MASK, 2>::value(), Q3 = NthBit<MASK, 3>::value();
-    run_rows<DT, W>(c, k, e, acc, [](float (&a)[W], const float (&x)[W], const float (&w)[4]) {
-        // the same-row taps first: they put FMAs between the settle and the
-        // DPP reads
-        if constexpr (Q0 / 3 == 1) tap_row<Q0, W>(a, x, w[0]);
-        if constexpr (Q1 / 3 == 1) tap_row<Q1, W>(a, x, w[1]);
-        if constexpr (Q2 / 3 == 1) tap_row<Q2, W>(a, x, w[2]);
-        if constexpr (Q3 / 3 == 1) tap_row<Q3, W>(a, x, w[3]);
-        if constexpr (Q0 / 3 != 1) tap_row<Q0, W>(a, x, w[0]);
-        if constexpr (Q1 / 3 != 1) tap_row<Q1, W>(a, x, w[1]);
-        if constexpr (Q2 / 3 != 1) tap_row<Q2, W>(a, x, w[2]);
-        if constexpr (Q3 / 3 != 1) tap_row<Q3, W>(a, x, w[3]);
+    // the taps that read the DPP source row through DPP go last: the others
+    // put FMAs between the settle and the DPP reads
+    constexpr int DR = 0;   // ky of the taps read by DPP (the row above)
+    run_rows<DT, W, ST>(c, k, e, acc, [](float (&a)[W / ST], const RowVals<W, ST>& x, const float (&w)[4]) {
+        if constexpr (Q0 / 3 != DR && (ST == 2 || Q0 / 3 == 1)) tap_row<Q0, W, ST>(a, x, w[0]);
+        if constexpr (Q1 / 3 != DR && (ST == 2 || Q1 / 3 == 1)) tap_row<Q1, W, ST>(a, x, w[1]);
+        if constexpr (Q2 / 3 != DR && (ST == 2 || Q2 / 3 == 1)) tap_row<Q2, W, ST>(a, x, w[2]);
+        if constexpr (Q3 / 3 != DR && (ST == 2 || Q3 / 3 == 1)) tap_row<Q3, W, ST>(a, x, w[3]);
+        if constexpr (!(Q0 / 3 != DR && (ST == 2 || Q0 / 3 == 1))) tap_row<Q0, W, ST>(a, x, w[0]);
+        if constexpr (!(Q1 / 3 != DR && (ST == 2 || Q1 / 3 == 1))) tap_row<Q1, W, ST>(a, x, w[1]);
+        if constexpr (!(Q2 / 3 != DR && (ST == 2 || Q2 / 3 == 1))) tap_row<Q2, W, ST>(a, x, w[2]);
+        if constexpr (!(Q3 / 3 != DR && (ST == 2 || Q3 / 3 == 1))) tap_row<Q3, W, ST>(a, x, w[3]);
     });
 }
 
 // Any 4-of-9 mask: each tap is chosen per kernel by a uniform branch.
-template <int DT, int W>
-__device__ __forceinline__ void run_generic_rows(unsigned mask, const RowCtx& c, int k, int e, float (&acc)[W]) {
+template <int DT, int W, int ST>
+__device__ __forceinline__ void run_generic_rows(unsigned mask, const RowCtx& c, int k, int e,
+                                                 float (&acc)[W / ST]) {
     int q0 = 4, q1 = 4, q2 = 4, q3 = 4, seen = 0;
 #pragma unroll
     for (int q = 0; q < 9; ++q) {
@@ -284,23 +330,23 @@ __device__ __forceinline__ void run_generic_rows(unsigned mask, const RowCtx& c,
             ++seen;
         }
     }
-    run_rows<DT, W>(c, k, e, acc, [=](float (&a)[W], const float (&x)[W], const float (&w)[4]) {
-        tap_row_dyn<W>(q0, a, x, w[0]);
-        tap_row_dyn<W>(q1, a, x, w[1]);
-        tap_row_dyn<W>(q2, a, x, w[2]);
-        tap_row_dyn<W>(q3, a, x, w[3]);
+    run_rows<DT, W, ST>(c, k, e, acc, [=](float (&a)[W / ST], const RowVals<W, ST>& x, const float (&w)[4]) {
+        tap_row_dyn<W, ST>(q0, a, x, w[0]);
+        tap_row_dyn<W, ST>(q1, a, x, w[1]);
+        tap_row_dyn<W, ST>(q2, a, x, w[2]);
+        tap_row_dyn<W, ST>(q3, a, x, w[3]);
     });
 }
 
 #define PSC_ROWS_CASE(I) \
-    case I: run_shape_rows<DT, W, kCentre3.code[I]>(c, k, e, acc); return;
+    case I: run_shape_rows<DT, W, ST, kCentre3.code[I]>(c, k, e, acc); return;
 #define PSC_ROWS_CASE8(I)                                                                           \
     PSC_ROWS_CASE(I) PSC_ROWS_CASE(I + 1) PSC_ROWS_CASE(I + 2) PSC_ROWS_CASE(I + 3)                 \
     PSC_ROWS_CASE(I + 4) PSC_ROWS_CASE(I + 5) PSC_ROWS_CASE(I + 6) PSC_ROWS_CASE(I + 7)
 
-template <int DT, int W>
+template <int DT, int W, int ST>
 __device__ __forceinline__ void run_pattern_rows(int shape, unsigned mask, const RowCtx& c, int k, int e,
-                                                 float (&acc)[W]) {
+                                                 float (&acc)[W / ST]) {
     switch (shape) {
         PSC_ROWS_CASE8(0)
         PSC_ROWS_CASE8(8)
@@ -309,13 +355,13 @@ __device__ __forceinline__ void run_pattern_rows(int shape, unsigned mask, const
         PSC_ROWS_CASE8(32)
         PSC_ROWS_CASE8(40)
         PSC_ROWS_CASE8(48)
-        default: run_generic_rows<DT, W>(mask, c, k, e, acc); return;
+        default: run_generic_rows<DT, W, ST>(mask, c, k, e, acc); return;
     }
 }
 #undef PSC_ROWS_CASE8
 #undef PSC_ROWS_CASE
 
-template <int DT, int W>
+template <int DT, int W, int ST>
 __global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __restrict__ x,
                                                    const int32_t* __restrict__ perm,
                                                    const int32_t* __restrict__ seg_ptr,
@@ -325,7 +371,8 @@ __global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __
                                                    typename Elt<DT>::T* __restrict__ y, RGeo g) {
     using E = Elt<DT>;
     constexpr int ESZ = int(sizeof(typename E::T));
-    extern __shared__ float psc_rows_red[];   // KS > 1: [KS][W][64] partial sums
+    constexpr int OW = W / ST;                // output columns (stride 2: W even)
+    extern __shared__ float psc_rows_red[];   // KS > 1: [KS][OW][64] partial sums
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
@@ -346,15 +393,15 @@ __global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __
     const int i = fg * g.FW + gf;                        // reordered filter of this wave
     const bool has_filter = i < g.cout;
 
-    // ---- lane geometry: image s of the group, row r (r == H: the zero lane)
+    // ---- lane geometry: image s of the group, output row r (r == OH: the zero lane)
     const int s = lane / g.seg_len, r = lane - s * g.seg_len;
     const int img = grp * g.S + s;
-    const bool valid = s < g.S && img < g.n && r < g.H;
+    const bool valid = s < g.S && img < g.n && r < g.OH;
     const int plane = g.H * g.W;
 
-    float acc[W];
+    float acc[OW];
 #pragma unroll
-    for (int c = 0; c < W; ++c) acc[c] = 0.f;
+    for (int c = 0; c < OW; ++c) acc[c] = 0.f;
 
     if (has_filter) {
         const int* segp = seg_ptr + i * (g.m + 1);
@@ -367,28 +414,31 @@ __global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __
         ctx.xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<typename E::T*>(x), int16_t(0), g.x_bytes, 0x00020000);
         ctx.chan_bytes = __builtin_amdgcn_readfirstlane(plane * ESZ);
         ctx.x_bytes = g.x_bytes;
-        ctx.vo = valid ? uint32_t((img * g.cin * g.H + r) * g.W) * uint32_t(ESZ) : 0x80000000u;
+        // input row ST*r of channel 0 of the lane's image (stride 2: and row
+        // 2r+1, zero past the last row)
+        ctx.vo = valid ? uint32_t((img * g.cin * g.H + ST * r) * g.W) * uint32_t(ESZ) : 0x80000000u;
+        ctx.vo2 = valid && ST == 2 && 2 * r + 1 < g.H ? ctx.vo + uint32_t(g.W * ESZ) : 0x80000000u;
         ctx.valid = valid;
         for (int p = 0; p < g.m; ++p) {
             int k0 = segp[p], k1 = segp[p + 1];
             k0 = k0 < s0 ? s0 : k0;
             k1 = k1 > s1 ? s1 : k1;                     // malformed pointers stay in the share
-            if (k0 < k1) run_pattern_rows<DT, W>(g.shape[p], g.mask[p], ctx, k0, k1, acc);
+            if (k0 < k1) run_pattern_rows<DT, W, ST>(g.shape[p], g.mask[p], ctx, k0, k1, acc);
         }
     }
 
     // ---- add the KS partial sums of each filter in share order
     if (g.KS > 1) {
-        float (*red)[W][64] = reinterpret_cast<float (*)[W][64]>(psc_rows_red);
+        float (*red)[OW][64] = reinterpret_cast<float (*)[OW][64]>(psc_rows_red);
         for (int slot = 0; slot < g.FW; ++slot) {
             if (slot == gf) {
 #pragma unroll
-                for (int c = 0; c < W; ++c) red[sp][c][lane] = acc[c];
+                for (int c = 0; c < OW; ++c) red[sp][c][lane] = acc[c];
             }
             __syncthreads();
             if (slot == gf) {
 #pragma unroll
-                for (int c = 0; c < W; ++c) {
+                for (int c = 0; c < OW; ++c) {
                     float v = 0.f;
                     for (int t = 0; t < g.KS; ++t) v += red[t][c][lane];
                     acc[c] = v;
@@ -400,9 +450,9 @@ __global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __
     if (!has_filter || !valid) return;
     const int f = perm[i];
     const float bv = bias ? E::load(bias, f) : 0.f;
-    typename E::T* yp = y + (int64_t(img) * g.cout + f) * plane + r * g.W;
+    typename E::T* yp = y + (int64_t(img) * g.cout + f) * (g.OH * OW) + r * OW;
 #pragma unroll
-    for (int c = 0; c < W; ++c) {
+    for (int c = 0; c < OW; ++c) {
         // the KS waves of a filter hold the same sums; share t stores columns t, t+KS, ...
         if ((c % g.KS) == sp) {
             float v = acc[c] + bv;
@@ -412,13 +462,13 @@ __global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __
     }
 }
 
-template <int DT, int W>
+template <int DT, int W, int ST>
 hipError_t launch_rows(const PackedView& pk, const ConvArgs& a, const RGeo& g, hipStream_t stream) {
     using T = typename Elt<DT>::T;
     const int waves = g.FW * g.KS;
-    const size_t smem = g.KS > 1 ? size_t(g.KS) * W * 64 * sizeof(float) : 0;
-    hipLaunchKernelGGL((k_conv_rows<DT, W>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)), smem, stream,
-                       static_cast<const T*>(a.x), pk.filter_perm, pk.seg_ptr, pk.cin_idx,
+    const size_t smem = g.KS > 1 ? size_t(g.KS) * (W / ST) * 64 * sizeof(float) : 0;
+    hipLaunchKernelGGL((k_conv_rows<DT, W, ST>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)), smem,
+                       stream, static_cast<const T*>(a.x), pk.filter_perm, pk.seg_ptr, pk.cin_idx,
                        static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), static_cast<T*>(a.y), g);
     return hipGetLastError();
 }

@@ -8,170 +8,215 @@
 // full output rows, each followed by one zero lane.  Output (i, j) reads
 // input rows 2i-1..2i+1 and columns 2j-1..2j+1, so for each kernel a lane
 // loads, for the 2R+1 input rows its R output rows need, columns 2j and
-// 2j+1 in one 8-byte (fp32) or 4-byte (fp16) load, and takes column 2j-1 --
-// the left lane's column 2(j-1)+1 -- by DPP.  The wave walks the filter's
-// storage one pattern segment after another, each through a loop compiled
-// with that centre+3 shape's taps fixed (other masks take a loop that
-// dispatches each tap); the channel index and weights are wave-uniform.
+// 2j+1 in one 8-byte (fp32) or 4-byte (fp16) buffer load at an offset fixed
+// per lane and row (the channel enters as a scalar offset; padding rows and
+// lanes point past the buffer range and read zero), and column 2j-1 -- the
+// left lane's column 2(j-1)+1 -- is read by DPP inside the FMA
+// (v_fmac_f32_dpp wave_shr:1).  The wave walks the filter's storage one
+// pattern segment after another, each through a loop compiled with that
+// centre+3 shape's taps fixed (other masks take a loop that dispatches each
+// tap); channel index and weights are wave-uniform (scalar buffer loads).
 // The next kernel's rows load while the current kernel's FMAs run.
-#include "common.h"
-#include "launch.h"
+#include "conv_stream.h"
 
 namespace psc {
 namespace {
 
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
 constexpr int kR2 = 4;                 // output rows per lane
 constexpr int kRows2 = 2 * kR2 + 1;    // input rows per lane and kernel
-constexpr int kDppShr = 0x138;         // wave_shr:1 -- lane i reads lane i-1
 
 struct Geo2 {
     int n, cin, H, W, cout, m, OH, OW;
     int S, seg_len, RB, units, slots;
     int KS, FW, groups_x, nblocks;
     int64_t keep;
+    int x_bytes;
     int relu;
     uint16_t mask[kMaxPatterns];
     int8_t shape[kMaxPatterns];   // centre+3 shape index of each library pattern, -1 = other mask
 };
 
-template <int DT> struct Pair;
-template <> struct Pair<DT_F32> {
-    __device__ __forceinline__ static void load(const float* p, float& e, float& o) {
-        const float2 v = *reinterpret_cast<const float2*>(p);
-        e = v.x;
-        o = v.y;
-    }
+// Raw words of a lane's column pair (2j, 2j+1) in each of its 2R+1 rows.
+template <int DT> struct Pairs {
+    uint32_t d[kRows2][DT == DT_F32 ? 2 : 1];
 };
-template <> struct Pair<DT_F16> {
-    __device__ __forceinline__ static void load(const uint16_t* p, float& e, float& o) {
-        const uint32_t v = *reinterpret_cast<const uint32_t*>(p);
-        e = float(__builtin_bit_cast(_Float16, uint16_t(v)));
-        o = float(__builtin_bit_cast(_Float16, uint16_t(v >> 16)));
-    }
-};
-
-template <int DT>
-__device__ __forceinline__ void load_rows2(const typename Elt<DT>::T* xc, const int (&ro)[kRows2], bool lane_ok,
-                                           float (&ev)[kRows2], float (&od)[kRows2]) {
-#pragma unroll
-    for (int r = 0; r < kRows2; ++r) {
-        float e = 0.f, o = 0.f;
-        if (lane_ok && ro[r] >= 0) Pair<DT>::load(xc + ro[r], e, o);
-        ev[r] = e;
-        od[r] = o;
-    }
-}
-
-// acc[i] += w * X[2i + DR] for the lane's R output rows.
-template <int DR>
-__device__ __forceinline__ void tap2(float (&acc)[kR2], const float (&X)[kRows2], float w) {
-#pragma unroll
-    for (int i = 0; i < kR2; ++i) acc[i] = fmaf(w, X[2 * i + DR], acc[i]);
-}
-
-// Tap at kernel position Q: column 0 reads the left lane's odd column (lf),
-// column 1 the lane's even column, column 2 its odd column.
-template <int Q>
-__device__ __forceinline__ void tap2_fix(float (&acc)[kR2], const float (&lf)[kRows2], const float (&ev)[kRows2],
-                                         const float (&od)[kRows2], float w) {
-    if constexpr (Q % 3 == 0) tap2<Q / 3>(acc, lf, w);
-    else if constexpr (Q % 3 == 1) tap2<Q / 3>(acc, ev, w);
-    else tap2<Q / 3>(acc, od, w);
-}
-
-__device__ __forceinline__ void tap2_dyn(int q, float (&acc)[kR2], const float (&lf)[kRows2],
-                                         const float (&ev)[kRows2], const float (&od)[kRows2], float w) {
-    switch (q) {
-        case 0: tap2<0>(acc, lf, w); break;
-        case 1: tap2<0>(acc, ev, w); break;
-        case 2: tap2<0>(acc, od, w); break;
-        case 3: tap2<1>(acc, lf, w); break;
-        case 4: tap2<1>(acc, ev, w); break;
-        case 5: tap2<1>(acc, od, w); break;
-        case 6: tap2<2>(acc, lf, w); break;
-        case 7: tap2<2>(acc, ev, w); break;
-        default: tap2<2>(acc, od, w); break;
-    }
-}
 
 struct Ctx2 {
-    int ro[kRows2];          // element offset of input column 2j of each row (-1: padding)
-    bool lane_ok;
-    int cin, plane;
+    cs::Meta m;
+    __amdgpu_buffer_rsrc_t xr;     // x, bounded to its size
+    int chan_bytes;                // bytes of one input channel plane
+    uint32_t vo[kRows2];           // byte offset of column 2j of each row, channel 0 (2^31: padding)
 };
 
 template <int DT>
-__device__ __forceinline__ void rows_of(const Ctx2& c, const typename Elt<DT>::T* xn, int ci, float (&ev)[kRows2],
-                                        float (&od)[kRows2]) {
-    const bool ok = unsigned(ci) < unsigned(c.cin);     // malformed channel indices read zeros
-    load_rows2<DT>(xn + int64_t(ok ? ci : 0) * c.plane, c.ro, c.lane_ok && ok, ev, od);
+__device__ __forceinline__ void load_pairs(const Ctx2& c, int ci, Pairs<DT>& p) {
+    // wave-uniform: an SGPR operand.  A malformed channel index reads zeros
+    // or other data of x, never memory outside it (range-checked loads).
+    const int soff = __builtin_amdgcn_readfirstlane(ci * c.chan_bytes);
+#pragma unroll
+    for (int r = 0; r < kRows2; ++r) {
+        if constexpr (DT == DT_F32) {
+            const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(c.xr, int(c.vo[r]), soff, 0);
+            p.d[r][0] = v.x;
+            p.d[r][1] = v.y;
+        } else {
+            p.d[r][0] = __builtin_amdgcn_raw_buffer_load_b32(c.xr, int(c.vo[r]), soff, 0);
+        }
+    }
 }
 
-// Kernels [k0, k1) of one pattern segment whose taps sit at positions Q0..Q3
-// (compile-time for the centre+3 shapes, QD = false; read from q[] for other
-// masks).  The rows of the next kernel load while this one's FMAs run.
-template <int DT, bool QD, int Q0, int Q1, int Q2, int Q3>
-__device__ __forceinline__ void run_seg2(const Ctx2& c, const typename Elt<DT>::T* xn,
-                                         const int32_t* __restrict__ cin_idx,
-                                         const typename Elt<DT>::T* __restrict__ vals, int k0, int k1,
-                                         const int (&q)[4], float (&acc)[kR2]) {
-    using E = Elt<DT>;
-    constexpr bool kLeft = Q0 % 3 == 0 || Q1 % 3 == 0 || Q2 % 3 == 0 || Q3 % 3 == 0;
-    const bool left = QD ? (q[0] % 3 == 0 || q[1] % 3 == 0 || q[2] % 3 == 0 || q[3] % 3 == 0) : kLeft;
-    float ev[kRows2], od[kRows2], ev2[kRows2], od2[kRows2];
-    rows_of<DT>(c, xn, cin_idx[k0], ev, od);
-    for (int k = k0; k < k1; ++k) {
-        if (k + 1 < k1) rows_of<DT>(c, xn, cin_idx[k + 1], ev2, od2);
-        float lf[kRows2];
-        if (left) {
+// The even and odd columns as fp32; then an asm the compiler sees as writing
+// them (no VALU write of them can follow) and the two wait states a DPP read
+// needs after a VALU write of its source.
+template <int DT>
+__device__ __forceinline__ void unpack_pairs(const Pairs<DT>& p, float (&ev)[kRows2], float (&od)[kRows2]) {
 #pragma unroll
-            for (int r = 0; r < kRows2; ++r)
-                lf[r] = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, od[r]),
-                                                                              kDppShr, 0xf, 0xf, true));
+    for (int r = 0; r < kRows2; ++r) {
+        if constexpr (DT == DT_F32) {
+            ev[r] = __builtin_bit_cast(float, p.d[r][0]);
+            od[r] = __builtin_bit_cast(float, p.d[r][1]);
         } else {
+            ev[r] = float(__builtin_bit_cast(_Float16, uint16_t(p.d[r][0])));
+            od[r] = float(__builtin_bit_cast(_Float16, uint16_t(p.d[r][0] >> 16)));
+        }
+    }
+    asm volatile("" : "+v"(od[0]), "+v"(od[1]), "+v"(od[2]), "+v"(od[3]), "+v"(od[4]));
+    asm volatile("" : "+v"(od[5]), "+v"(od[6]), "+v"(od[7]), "+v"(od[8]));
+    asm volatile("s_nop 1");
+}
+
+// The tap at kernel position Q = 3 ky + kx: acc[i] += w * x(row 2i + ky - 1,
+// column 2j + kx - 1) for the lane's R output rows.  Column 2j-1 is the odd
+// column of the lane to the left (DPP; a lane without one reads zero).
+template <int Q>
+__device__ __forceinline__ void tap2(float (&acc)[kR2], const float (&ev)[kRows2], const float (&od)[kRows2],
+                                     float w) {
+    constexpr int ky = Q / 3, kx = Q % 3;
 #pragma unroll
-            for (int r = 0; r < kRows2; ++r) lf[r] = 0.f;          // no column-0 tap reads it
+    for (int i = 0; i < kR2; ++i) {
+        if constexpr (kx == 0)
+            asm volatile("v_fmac_f32_dpp %0, %1, %2 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+                         : "+v"(acc[i])
+                         : "v"(od[2 * i + ky]), "v"(w));
+        else if constexpr (kx == 1)
+            acc[i] = __builtin_fmaf(w, ev[2 * i + ky], acc[i]);
+        else
+            acc[i] = __builtin_fmaf(w, od[2 * i + ky], acc[i]);
+    }
+}
+
+__device__ __forceinline__ void tap2_dyn(int q, float (&acc)[kR2], const float (&ev)[kRows2],
+                                         const float (&od)[kRows2], float w) {
+    switch (q) {
+        case 0: tap2<0>(acc, ev, od, w); break;
+        case 1: tap2<1>(acc, ev, od, w); break;
+        case 2: tap2<2>(acc, ev, od, w); break;
+        case 3: tap2<3>(acc, ev, od, w); break;
+        case 4: tap2<4>(acc, ev, od, w); break;
+        case 5: tap2<5>(acc, ev, od, w); break;
+        case 6: tap2<6>(acc, ev, od, w); break;
+        case 7: tap2<7>(acc, ev, od, w); break;
+        default: tap2<8>(acc, ev, od, w); break;
+    }
+}
+
+// Kernels [k, e) of one pattern segment share (e > k), two per trip: the
+// rows of one load while the other's FMAs run; metadata is read two kernels
+// ahead; the single loop exit keeps the accumulators in place.
+template <int DT, class TapFn>
+__device__ __forceinline__ void run2(const Ctx2& c, int k, int e, float (&acc)[kR2], TapFn taps) {
+    const int last = e - 1;
+    float wA[4], wB[4];
+    cs::meta_w<DT>(c.m, k, wA);
+    int kk = k + 1 <= last ? k + 1 : last;
+    int ciB = cs::meta_ci(c.m, kk);
+    cs::meta_w<DT>(c.m, kk, wB);
+    Pairs<DT> pA, pB;
+    load_pairs<DT>(c, cs::meta_ci(c.m, k), pA);
+    while (k + 1 < e) {
+        load_pairs<DT>(c, ciB, pB);                              // rows of kernel k+1
+        kk = k + 2 <= last ? k + 2 : last;
+        const int ciA2 = cs::meta_ci(c.m, kk);
+        float wA2[4];
+        cs::meta_w<DT>(c.m, kk, wA2);
+        kk = k + 3 <= last ? k + 3 : last;
+        const int ciB2 = cs::meta_ci(c.m, kk);
+        float wB2[4];
+        cs::meta_w<DT>(c.m, kk, wB2);
+        {
+            float ev[kRows2], od[kRows2];
+            unpack_pairs<DT>(pA, ev, od);
+            taps(acc, ev, od, wA);                               // kernel k
         }
-        const float w0 = E::load(vals, int64_t(k) * 4), w1 = E::load(vals, int64_t(k) * 4 + 1);
-        const float w2 = E::load(vals, int64_t(k) * 4 + 2), w3 = E::load(vals, int64_t(k) * 4 + 3);
-        if constexpr (QD) {
-            tap2_dyn(q[0], acc, lf, ev, od, w0);
-            tap2_dyn(q[1], acc, lf, ev, od, w1);
-            tap2_dyn(q[2], acc, lf, ev, od, w2);
-            tap2_dyn(q[3], acc, lf, ev, od, w3);
-        } else {
-            tap2_fix<Q0>(acc, lf, ev, od, w0);
-            tap2_fix<Q1>(acc, lf, ev, od, w1);
-            tap2_fix<Q2>(acc, lf, ev, od, w2);
-            tap2_fix<Q3>(acc, lf, ev, od, w3);
+        load_pairs<DT>(c, ciA2, pA);                             // rows of kernel k+2
+        {
+            float ev[kRows2], od[kRows2];
+            unpack_pairs<DT>(pB, ev, od);
+            taps(acc, ev, od, wB);                               // kernel k+1
         }
-        if (k + 1 < k1) {
-#pragma unroll
-            for (int r = 0; r < kRows2; ++r) {
-                ev[r] = ev2[r];
-                od[r] = od2[r];
-            }
-        }
+        k += 2;
+        wA[0] = wA2[0], wA[1] = wA2[1], wA[2] = wA2[2], wA[3] = wA2[3];
+        wB[0] = wB2[0], wB[1] = wB2[1], wB[2] = wB2[2], wB[3] = wB2[3];
+        ciB = ciB2;
+    }
+    if (k < e) {
+        float ev[kRows2], od[kRows2];
+        unpack_pairs<DT>(pA, ev, od);
+        taps(acc, ev, od, wA);
     }
 }
 
 template <int DT, int MASK>
-__device__ __forceinline__ void run_shape2(const Ctx2& c, const typename Elt<DT>::T* xn, const int32_t* cin_idx,
-                                           const typename Elt<DT>::T* vals, int k0, int k1, const int (&q)[4],
-                                           float (&acc)[kR2]) {
-    run_seg2<DT, false, NthBit<MASK, 0>::value(), NthBit<MASK, 1>::value(), NthBit<MASK, 2>::value(),
-             NthBit<MASK, 3>::value()>(c, xn, cin_idx, vals, k0, k1, q, acc);
+__device__ __forceinline__ void run_shape2(const Ctx2& c, int k, int e, float (&acc)[kR2]) {
+    constexpr int Q0 = NthBit<MASK, 0>::value(), Q1 = NthBit<MASK, 1>::value();
+    constexpr int Q2 = NthBit<MASK, 2>::value(), Q3 = NthBit<MASK, 3>::value();
+    run2<DT>(c, k, e, acc, [](float (&a)[kR2], const float (&ev)[kRows2], const float (&od)[kRows2],
+                              const float (&w)[4]) {
+        // the own-column taps first: they put FMAs between the unpack and the DPP reads
+        if constexpr (Q0 % 3 != 0) tap2<Q0>(a, ev, od, w[0]);
+        if constexpr (Q1 % 3 != 0) tap2<Q1>(a, ev, od, w[1]);
+        if constexpr (Q2 % 3 != 0) tap2<Q2>(a, ev, od, w[2]);
+        if constexpr (Q3 % 3 != 0) tap2<Q3>(a, ev, od, w[3]);
+        if constexpr (Q0 % 3 == 0) tap2<Q0>(a, ev, od, w[0]);
+        if constexpr (Q1 % 3 == 0) tap2<Q1>(a, ev, od, w[1]);
+        if constexpr (Q2 % 3 == 0) tap2<Q2>(a, ev, od, w[2]);
+        if constexpr (Q3 % 3 == 0) tap2<Q3>(a, ev, od, w[3]);
+    });
+}
+
+// Any 4-of-9 mask: each tap is chosen per kernel by a uniform branch.
+template <int DT>
+__device__ __forceinline__ void run_generic2(unsigned mask, const Ctx2& c, int k, int e, float (&acc)[kR2]) {
+    int q0 = 4, q1 = 4, q2 = 4, q3 = 4, seen = 0;
+#pragma unroll
+    for (int q = 0; q < 9; ++q) {
+        if ((mask >> q) & 1u) {
+            if (seen == 0) q0 = q;
+            else if (seen == 1) q1 = q;
+            else if (seen == 2) q2 = q;
+            else if (seen == 3) q3 = q;
+            ++seen;
+        }
+    }
+    run2<DT>(c, k, e, acc, [=](float (&a)[kR2], const float (&ev)[kRows2], const float (&od)[kRows2],
+                               const float (&w)[4]) {
+        tap2_dyn(q0, a, ev, od, w[0]);
+        tap2_dyn(q1, a, ev, od, w[1]);
+        tap2_dyn(q2, a, ev, od, w[2]);
+        tap2_dyn(q3, a, ev, od, w[3]);
+    });
 }
 
 #define PSC_S2_CASE(I) \
-    case I: run_shape2<DT, kCentre3.code[I]>(c, xn, cin_idx, vals, k0, k1, q, acc); return;
+    case I: run_shape2<DT, kCentre3.code[I]>(c, k, e, acc); return;
 #define PSC_S2_CASE8(I)                                                                             \
     PSC_S2_CASE(I) PSC_S2_CASE(I + 1) PSC_S2_CASE(I + 2) PSC_S2_CASE(I + 3) PSC_S2_CASE(I + 4)      \
     PSC_S2_CASE(I + 5) PSC_S2_CASE(I + 6) PSC_S2_CASE(I + 7)
 template <int DT>
-__device__ __forceinline__ void run_pattern2(int shape, const Ctx2& c, const typename Elt<DT>::T* xn,
-                                             const int32_t* cin_idx, const typename Elt<DT>::T* vals, int k0,
-                                             int k1, const int (&q)[4], float (&acc)[kR2]) {
+__device__ __forceinline__ void run_pattern2(int shape, unsigned mask, const Ctx2& c, int k, int e,
+                                             float (&acc)[kR2]) {
     switch (shape) {
         PSC_S2_CASE8(0)
         PSC_S2_CASE8(8)
@@ -180,7 +225,7 @@ __device__ __forceinline__ void run_pattern2(int shape, const Ctx2& c, const typ
         PSC_S2_CASE8(32)
         PSC_S2_CASE8(40)
         PSC_S2_CASE8(48)
-        default: run_seg2<DT, true, 0, 0, 0, 0>(c, xn, cin_idx, vals, k0, k1, q, acc); return;
+        default: run_generic2<DT>(mask, c, k, e, acc); return;
     }
 }
 #undef PSC_S2_CASE8
@@ -222,13 +267,7 @@ __global__ __launch_bounds__(256) void k_conv_stride2(const typename Elt<DT>::T*
         i0 = (u - nimg * g.RB) * kR2;
     }
     const int plane = g.H * g.W;
-    // element offset (inside one channel plane) of input column 2j of each row
-    int ro[kRows2];
-#pragma unroll
-    for (int r = 0; r < kRows2; ++r) {
-        const int row = 2 * i0 - 1 + r;
-        ro[r] = (row >= 0 && row < g.H) ? row * g.W + 2 * j : -1;
-    }
+    constexpr int ESZ = int(sizeof(typename E::T));
     float acc[kR2];
 #pragma unroll
     for (int r = 0; r < kR2; ++r) acc[r] = 0.f;
@@ -238,26 +277,24 @@ __global__ __launch_bounds__(256) void k_conv_stride2(const typename Elt<DT>::T*
         const int f0 = segp[0], f1 = segp[g.m];
         const int len = f1 - f0;
         const int s0 = f0 + len * sp / g.KS, s1 = f0 + len * (sp + 1) / g.KS;
-        const typename E::T* xn = x + int64_t(nimg) * g.cin * plane;
         Ctx2 c;
+        c.m = cs::Meta{cs::scalar_rsrc(cin_idx, int(g.keep) * 4), cs::scalar_rsrc(vals, int(g.keep) * 4 * ESZ)};
+        c.xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<typename E::T*>(x), int16_t(0), g.x_bytes, 0x00020000);
+        c.chan_bytes = __builtin_amdgcn_readfirstlane(plane * ESZ);
+        // byte offset of input column 2j of each of the lane's rows in
+        // channel 0 of its image; past the buffer range for padding
 #pragma unroll
-        for (int r = 0; r < kRows2; ++r) c.ro[r] = ro[r];
-        c.lane_ok = lane_ok;
-        c.cin = g.cin;
-        c.plane = plane;
+        for (int r = 0; r < kRows2; ++r) {
+            const int row = 2 * i0 - 1 + r;
+            c.vo[r] = (lane_ok && row >= 0 && row < g.H)
+                          ? uint32_t(nimg * g.cin * plane + row * g.W + 2 * j) * uint32_t(ESZ)
+                          : 0x80000000u;
+        }
         for (int p = 0; p < g.m; ++p) {
             int k0 = segp[p], k1 = segp[p + 1];
             k0 = k0 < s0 ? s0 : k0;
             k1 = k1 > s1 ? s1 : k1;                               // malformed pointers stay in the share
-            if (k0 >= k1) continue;
-            int q[4] = {4, 4, 4, 4}, t = 0;
-            const unsigned mk = g.mask[p];
-            for (int qq = 0; qq < 9; ++qq)
-                if ((mk >> qq) & 1u) {
-                    if (t < 4) q[t] = qq;
-                    ++t;
-                }
-            run_pattern2<DT>(g.shape[p], c, xn, cin_idx, vals, k0, k1, q, acc);
+            if (k0 < k1) run_pattern2<DT>(g.shape[p], g.mask[p], c, k0, k1, acc);
         }
     }
     // add the KS partial sums of each filter in share order
@@ -297,11 +334,16 @@ __global__ __launch_bounds__(256) void k_conv_stride2(const typename Elt<DT>::T*
 }  // namespace
 
 // Launch configuration of the stride-2 kernel; false when it does not take
-// the call (odd width, more than 63 output columns, a pooled output).
+// the call (odd width, more than 63 output columns, a pooled output, x
+// beyond the 2 GiB a buffer descriptor addresses here).
 static bool plan_conv_stride2(const PatTable& tab, const ConvArgs& a, ConvForm* form, Geo2* out) {
     if (a.stride != 2 || a.pool || (a.w & 1)) return false;
     const int OH = (a.h - 1) / 2 + 1, OW = (a.w - 1) / 2 + 1;
     if (OW > 63) return false;
+    // buffer descriptors address at most 2 GiB (x) and the packed weights
+    const int esz = a.dtype == DT_F16 ? 2 : 4;
+    const int64_t x_bytes = int64_t(a.n) * a.cin * a.h * a.w * esz;
+    if (x_bytes >= (int64_t(1) << 31) || a.keep * 4 * esz > 0x7fffffff) return false;
     Geo2 g{};
     g.n = a.n;
     g.cin = a.cin;
@@ -312,6 +354,7 @@ static bool plan_conv_stride2(const PatTable& tab, const ConvArgs& a, ConvForm* 
     g.OH = OH;
     g.OW = OW;
     g.keep = a.keep;
+    g.x_bytes = int(x_bytes);
     g.relu = a.relu;
     for (int p = 0; p < kMaxPatterns; ++p) {
         g.mask[p] = p < tab.m ? tab.mask[p] : 0;

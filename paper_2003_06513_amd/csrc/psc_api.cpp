@@ -305,8 +305,9 @@ static psc_status check_conv_shape(const psc_layer* L, int32_t act_dtype, int32_
         const psc::ConvArgs a{act_dtype, n, L->cin, h, w, L->cout, L->keep, nullptr, nullptr, 0, nullptr, pool, stride};
         if (!psc::conv_rows_takes(table_of(L), a))
             return fail(PSC_ERR_UNSUPPORTED,
-                        "algo 2 (one row per lane) needs stride 1, no pool, h <= 63 and w in {4, 7, 8, 14, 16, 28} "
-                        "(fp16: w even or 7); got h=%d, w=%d, stride=%d, pool=%d",
+                        "algo 2 (one row per lane) needs no pool, at most 63 output rows and, with stride 1, "
+                        "w in {4, 7, 8, 14, 16, 28} (fp16: w even or 7), with stride 2, w in {8, 16, 32}; "
+                        "got h=%d, w=%d, stride=%d, pool=%d",
                         h, w, stride, pool);
     }
     return PSC_OK;

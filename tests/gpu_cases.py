@@ -197,6 +197,14 @@ def form_cases():
             L = B.Layer(cout, cin, list(FORM_MASKS), cin * cout // 2, dt)
             cfg = B.conv3x3_config(L, dt, n, h, w, False, 1, 2)
             out.append((("rows", cfg["kernel"], w, cfg["shares"] > 1), n, cin, cout, h, w, dt, False, 1, 2))
+        # its stride-2 form: every compiled width, odd and even heights (the
+        # last output row's odd input row past the image), ragged groups,
+        # split filters
+        for n, cin, cout, h, w in ((13, 5, 6, 8, 8), (2, 40, 5, 7, 8), (9, 7, 5, 16, 16), (1, 48, 4, 15, 16),
+                                   (4, 9, 5, 32, 32), (1, 40, 3, 31, 32)):
+            L = B.Layer(cout, cin, list(FORM_MASKS), cin * cout // 2, dt)
+            cfg = B.conv3x3_config(L, dt, n, h, w, False, 2, 2)
+            out.append((("rows2", cfg["kernel"], w, cfg["shares"] > 1), n, cin, cout, h, w, dt, False, 2, 2))
         out.append((("simple-stride2",), 2, 9, 7, 13, 11, dt, False, 2, 0))
         out.append((("simple-algo1",), 2, 9, 7, 13, 11, dt, False, 1, 1))
         out.append((("simple-algo1-pool",), 2, 9, 7, 12, 10, dt, True, 1, 1))

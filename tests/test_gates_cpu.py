@@ -68,12 +68,16 @@ def test_form_search_reaches_every_form():
     assert any(k[0] == 1 and k[3] for k in keys) and any(k[0] == 1 and k[4] for k in keys)
     assert any(k[2] for k in keys)                                                         # column tiles
     assert {c[0][0] for c in cases if not isinstance(c[0][0], int)} == \
-        {"stride2", "rows", "simple-stride2", "simple-algo1", "simple-algo1-pool"}
+        {"stride2", "rows", "rows2", "simple-stride2", "simple-algo1", "simple-algo1-pool"}
     rows = [c for c in cases if c[0][0] == "rows"]
     assert all(c[0][1] == 4 for c in rows)
     for dt in (B.PSC_F32, B.PSC_F16):
         assert {c[5] for c in rows if c[6] == dt} == {4, 7, 8, 14, 16, 28}
         assert any(c[0][3] for c in rows if c[6] == dt) and any(not c[0][3] for c in rows if c[6] == dt)
+    rows2 = [c for c in cases if c[0][0] == "rows2"]
+    for dt in (B.PSC_F32, B.PSC_F16):
+        assert {c[5] for c in rows2 if c[6] == dt} == {8, 16, 32}
+        assert any(c[0][3] for c in rows2 if c[6] == dt) and any(c[4] % 2 for c in rows2 if c[6] == dt)
     # the automatic choice takes the rows kernel for whole-wave batches on small planes
     assert any(isinstance(c[0][0], int) and c[0][0] == 4 for c in cases)
     s2 = [c[0] for c in cases if c[0][0] == "stride2"]
@@ -85,7 +89,7 @@ def test_config_query_validates():
     for args in [(B.PSC_F16, 1, 8, 8, False, 1, 0), (B.PSC_F32, 1, 8, 8, False, 3, 0),
                  (B.PSC_F32, 1, 7, 8, True, 1, 0), (B.PSC_F32, 1, 8, 8, True, 2, 0),
                  (B.PSC_F32, 1, 8, 8, False, 1, 4), (B.PSC_F32, 1, 8, 9, False, 1, 2),
-                 (B.PSC_F32, 1, 8, 8, True, 1, 2), (B.PSC_F32, 1, 8, 8, False, 2, 2),
+                 (B.PSC_F32, 1, 8, 8, True, 1, 2), (B.PSC_F32, 1, 8, 10, False, 2, 2),
                  (B.PSC_F32, 1, 64, 8, False, 1, 2), (B.PSC_F32, -1, 8, 8, False, 1, 0)]:
         with pytest.raises(B.PscError):
             B.conv3x3_config(L, *args)

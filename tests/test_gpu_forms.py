@@ -45,8 +45,8 @@ def test_form_parity_guard_rerun(case):
         assert (got["kernel"], got["staged"], got["rows_per_lane"]) == (key[0], key[1], key[5])
     elif key[0] == "stride2":
         assert got["kernel"] == key[1] == 3
-    elif key[0] == "rows":
-        assert got["kernel"] == key[1] == 4 and got["cols_per_lane"] == w
+    elif key[0] in ("rows", "rows2"):
+        assert got["kernel"] == key[1] == 4 and got["cols_per_lane"] == (w - 1) // stride + 1
     else:
         assert got["kernel"] == 2
     x = inputs.normal_activations(seed + 1, (n, cin, h, w), dtype)
