@@ -111,7 +111,11 @@ extern "C" {
 const char* psc_last_error(void) { return g_last_error.c_str(); }
 
 const char* psc_status_string(psc_status s) {
-    switch (s) {
+    // a C caller may pass any int: read the bits as one, not as the enum
+    // (whose value range ends at 7)
+    int32_t v;
+    std::memcpy(&v, &s, sizeof v);
+    switch (v) {
         case PSC_OK: return "PSC_OK";
         case PSC_ERR_ARG: return "PSC_ERR_ARG";
         case PSC_ERR_UNSUPPORTED: return "PSC_ERR_UNSUPPORTED";
