@@ -245,7 +245,8 @@ psc_status psc_transpose_prep(const psc_layer *layer, const void *d_w, const uin
  * the original filter order.  Stride 1, zero padding 1.  The batch and the
  * image may be split over several waves per kernel; their sums meet in the
  * caller's workspace (psc_conv3x3_bwd_weight_workspace bytes, may be 0) and
- * are added in a fixed order, so results are reproducible bit for bit. */
+ * are added in a fixed order, so results are reproducible bit for bit.
+ * x and dy of more than 2 GiB each return PSC_ERR_UNSUPPORTED. */
 psc_status psc_conv3x3_bwd_weight_workspace(const psc_layer *layer, int32_t act_dtype, int32_t n,
                                             int32_t h, int32_t w, size_t *bytes);
 psc_status psc_conv3x3_bwd_weight(const psc_layer *layer, const psc_packed *packed,
@@ -279,7 +280,8 @@ psc_status psc_admm_residual(const float *d_z, const float *d_target, int64_t nu
  *   d_dw[o][i][r][s] = sum over images and pixels of
  *                      g[n, o, h, w] * x[n, i, h + r - 1, w + s - 1]
  * and, if d_db is non-NULL, d_db[o] = sum of g[n, o, :, :]; fp32.  Workspace
- * as for psc_conv3x3_bwd_weight (psc_dense3x3_bwd_weight_workspace bytes). */
+ * as for psc_conv3x3_bwd_weight (psc_dense3x3_bwd_weight_workspace bytes);
+ * x and g of more than 2 GiB each return PSC_ERR_UNSUPPORTED. */
 psc_status psc_dense3x3_bwd_weight_workspace(int32_t n, int32_t cin, int32_t h, int32_t w,
                                              int32_t cout, size_t *bytes);
 psc_status psc_dense3x3_bwd_weight(const float *d_x, const float *d_g, int32_t n, int32_t cin,

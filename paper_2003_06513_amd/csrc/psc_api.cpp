@@ -434,6 +434,8 @@ psc_status psc_conv3x3_bwd_weight(const psc_layer* L, const psc_packed* pk, int3
     if (need && (!d_ws || ws_bytes < need))
         return fail(PSC_ERR_WORKSPACE, "bwd weight needs %zu workspace bytes, got %zu", need, ws_bytes);
     if (n == 0) return ok();
+    if (!psc::wgrad_fits(n, L->cin, L->cout, h, w, act_dtype))
+        return fail(PSC_ERR_UNSUPPORTED, "bwd weight: x and dy must each fit in 2 GiB");
     if (!d_x || !d_dy) return fail(PSC_ERR_ARG, "d_x and d_dy must be non-NULL");
     if (L->keep > 0 && !d_dvalues) return fail(PSC_ERR_ARG, "d_dvalues must be non-NULL when keep > 0");
     if (reinterpret_cast<uintptr_t>(d_dvalues) & 15u) return fail(PSC_ERR_ARG, "d_dvalues must be 16-byte aligned");
@@ -486,6 +488,8 @@ psc_status psc_dense3x3_bwd_weight(const float* d_x, const float* d_g, int32_t n
     if (need && (!d_ws || ws_bytes < need))
         return fail(PSC_ERR_WORKSPACE, "dense bwd weight needs %zu workspace bytes, got %zu", need, ws_bytes);
     if (n == 0) return ok();
+    if (!psc::wgrad_fits(n, cin, cout, h, w, PSC_F32))
+        return fail(PSC_ERR_UNSUPPORTED, "dense bwd weight: x and g must each fit in 2 GiB");
     return device_status(psc::launch_dense_wgrad(d_x, d_g, n, cin, h, w, cout, d_dw, d_db, d_ws, as_stream(stream)),
                          "psc_dense3x3_bwd_weight launch");
 }

@@ -9,21 +9,32 @@
 // dense gradient of the ADMM primal step (Sec. 4.3 Eq. 4: all 9 positions
 // of every (f, ci)).
 //
-// Layout of the work: one wave per kernel and share of the image.  As in the
-// forward kernels, a lane owns one column and R rows of an output band (a
-// wave holds S bands of full rows separated by a zero lane, or a column tile
-// with one halo lane on each side); per band it loads its R rows of dy and
-// the R+2 rows of x around them once, takes the left/right neighbour columns
-// of x from the adjacent lanes by DPP, and accumulates every tap's products
-// in a register of its own.  The bands of a share are walked in turn, and
-// the per-lane sums are added across the wave once at the end.  With several
-// shares per kernel the share sums go to a workspace and a second kernel
-// adds them in share order, so results do not depend on scheduling.
+// Layout of the work.  The kernels of one filter all read the same dy plane,
+// so a wave takes one filter and a chunk of up to KC of its kernels (KC
+// consecutive kernels of one pattern segment in storage order; dense: KC
+// consecutive input channels) and one share of the images: for every output
+// band of the share it loads the R rows of dy once and, for each kernel of
+// the chunk, the R+2 rows of x around them, so one dy load feeds KC kernels.
+// The lane layout is the forward's: a lane owns one column and R rows of a
+// band (a wave holds S bands of full rows separated by a zero lane, or a
+// column tile with one halo lane on each side).  Rows come through buffer
+// loads at offsets fixed per lane and row, the channel entering as a scalar
+// offset and padding reading zero; the left and right neighbour columns of x
+// are read by DPP inside the FMA.  The taps of a chunk are compiled for its
+// centre+3 shape (other masks dispatch each tap).  At the end of a chunk the
+// KC x 4 per-lane sums are added across the wave by a reduce-scatter (each
+// step halves the values a lane holds).  The chunks of a filter are dealt
+// round-robin to G waves; with several image shares the share sums go to a
+// workspace and a second kernel adds them in share order, so results do not
+// depend on scheduling.
 #include "common.h"
 #include "launch.h"
+#include "conv_rows.h"
 
 namespace psc {
 namespace {
+
+constexpr int kKC = 4;           // kernels per chunk
 
 struct WGeo {
     int n, cin, cout, H, W;
@@ -31,101 +42,149 @@ struct WGeo {
     int seg_len;    // lanes per segment
     int Wt;         // output columns per segment
     int cols_mode;  // 0: full-row segments with zero separators, 1: haloed column tiles
+    int rows;       // 1: one image row per lane (small planes at large batch; S images per wave)
     int RB, CT;     // row bands and column tiles per image
-    int units;      // n * RB * CT
+    int units;      // n * RB * CT (rows: n)
     int slots;      // waves' worth of units: ceil(units / S)
-    int KS;         // shares of the slots per kernel
+    int G;          // waves sharing one filter's chunks (round-robin)
+    int KS;         // image shares (ranges of slots)
     int64_t nk;     // kernels
     int dense;      // 1: kernel k is (k / cin, k % cin) with all 9 taps
     int m;
+    int x_bytes, dy_bytes;   // buffer ranges
     uint16_t mask[kMaxPatterns];
+    int8_t shape[kMaxPatterns];   // centre+3 shape index of each library pattern, -1 = other mask
 };
 
-constexpr int kDppShr = 0x138;   // wave_shr:1 -- lane i reads lane i-1
-constexpr int kDppShl = 0x130;   // wave_shl:1 -- lane i reads lane i+1
-
-__device__ __forceinline__ float dpp_shift(float v, int ctrl_is_shr) {
-    const int iv = __builtin_bit_cast(int, v);
-    const int r = ctrl_is_shr ? __builtin_amdgcn_update_dpp(0, iv, kDppShr, 0xf, 0xf, true)
-                              : __builtin_amdgcn_update_dpp(0, iv, kDppShl, 0xf, 0xf, true);
-    return __builtin_bit_cast(float, r);
-}
-
-// acc += sum_r dy[r] * xs[r + DR] for one tap (DR: row offset 0..2).
-template <int R, int DR>
-__device__ __forceinline__ void tap_rows(float& acc, const float (&dyr)[R], const float (&xs)[R + 2]) {
+#define PSC_W_SHR "v_fmac_f32_dpp %0, %1, %2 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+#define PSC_W_SHL "v_fmac_f32_dpp %0, %1, %2 wave_shl:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+// acc += sum_r x(column c + kx - 1, row r + ky) * dy[r]: column c - 1 is the
+// lane to the left (DPP wave_shr), c + 1 the lane to the right (wave_shl);
+// lanes without a neighbour read zero.
+template <int R, int Q>
+__device__ __forceinline__ void wtap(float& acc, const float (&x)[R + 2], const float (&dyr)[R]) {
+    constexpr int ky = Q / 3, kx = Q % 3;
 #pragma unroll
-    for (int r = 0; r < R; ++r) acc = fmaf(dyr[r], xs[r + DR], acc);
+    for (int r = 0; r < R; ++r) {
+        if constexpr (kx == 1)
+            acc = __builtin_fmaf(x[r + ky], dyr[r], acc);
+        else if constexpr (kx == 0)
+            asm volatile(PSC_W_SHR : "+v"(acc) : "v"(x[r + ky]), "v"(dyr[r]));
+        else
+            asm volatile(PSC_W_SHL : "+v"(acc) : "v"(x[r + ky]), "v"(dyr[r]));
+    }
 }
+#undef PSC_W_SHL
+#undef PSC_W_SHR
 
 template <int R>
-__device__ __forceinline__ void tap_dyn(int q, float& acc, const float (&dyr)[R], const float (&xl)[R + 2],
-                                        const float (&xc)[R + 2], const float (&xr)[R + 2]) {
+__device__ __forceinline__ void wtap_dyn(int q, float& acc, const float (&x)[R + 2], const float (&dyr)[R]) {
     switch (q) {
-        case 0: tap_rows<R, 0>(acc, dyr, xl); break;
-        case 1: tap_rows<R, 0>(acc, dyr, xc); break;
-        case 2: tap_rows<R, 0>(acc, dyr, xr); break;
-        case 3: tap_rows<R, 1>(acc, dyr, xl); break;
-        case 4: tap_rows<R, 1>(acc, dyr, xc); break;
-        case 5: tap_rows<R, 1>(acc, dyr, xr); break;
-        case 6: tap_rows<R, 2>(acc, dyr, xl); break;
-        case 7: tap_rows<R, 2>(acc, dyr, xc); break;
-        default: tap_rows<R, 2>(acc, dyr, xr); break;
+        case 0: wtap<R, 0>(acc, x, dyr); break;
+        case 1: wtap<R, 1>(acc, x, dyr); break;
+        case 2: wtap<R, 2>(acc, x, dyr); break;
+        case 3: wtap<R, 3>(acc, x, dyr); break;
+        case 4: wtap<R, 4>(acc, x, dyr); break;
+        case 5: wtap<R, 5>(acc, x, dyr); break;
+        case 6: wtap<R, 6>(acc, x, dyr); break;
+        case 7: wtap<R, 7>(acc, x, dyr); break;
+        default: wtap<R, 8>(acc, x, dyr); break;
     }
 }
 
-// NT = 4 (the kept positions of a pattern, dispatched per tap) or 9 (dense).
-template <int DT, int R, int NT>
-__global__ __launch_bounds__(256) void k_wgrad(const typename Elt<DT>::T* __restrict__ x,
-                                               const typename Elt<DT>::T* __restrict__ dy,
-                                               const int32_t* __restrict__ perm, const int32_t* __restrict__ fptr,
-                                               const int32_t* __restrict__ cin_idx,
-                                               const uint8_t* __restrict__ pat_id, WGeo g, float* __restrict__ out) {
-    using E = Elt<DT>;
-    const int lane = threadIdx.x & 63;
-    const int64_t wid = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
-    const int64_t k = wid / g.KS;
-    const int s = int(wid - k * g.KS);
-    if (k >= g.nk) return;                                   // whole waves leave together
-    int f, ci;
-    int q[NT];
-    if (g.dense) {
-        f = int(k / g.cin);
-        ci = int(k - int64_t(f) * g.cin);
+// R rows of one column through a buffer descriptor (offsets past its range
+// read zero), widened to fp32.
+template <int DT, int N>
+__device__ __forceinline__ void load_col(__amdgpu_buffer_rsrc_t rs, const uint32_t (&vo)[N], int soff,
+                                         float (&v)[N]) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) q[t] = t;
-    } else {
-        // the filter holding kernel k: the last i with fptr[i] <= k
-        int lo = 0, hi = g.cout - 1;
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (fptr[mid] <= k) lo = mid;
-            else hi = mid - 1;
+    for (int r = 0; r < N; ++r) {
+        if constexpr (DT == DT_F32)
+            v[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, int(vo[r]), soff, 0));
+        else
+            v[r] = float(__builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(rs, int(vo[r]), soff, 0)));
+    }
+}
+
+// Values the compiler sees as written by an asm (no VALU write of them can
+// follow), then the two wait states a DPP read needs after a VALU write of
+// its source.
+template <int N>
+__device__ __forceinline__ void settle(float (&v)[N]) {
+#pragma unroll
+    for (int j = 0; j < N; j += 2) {
+        if (j + 1 < N) asm volatile("" : "+v"(v[j]), "+v"(v[j + 1]));
+        else asm volatile("" : "+v"(v[j]));
+    }
+    asm volatile("s_nop 1");
+}
+
+// Sum of each of the V values over the 64 lanes of the wave.  Reduce-scatter
+// while more than one value is left: at each step the lanes whose bit d is
+// set keep the upper half of their values and hand the lower half to their
+// partner lane^d (which keeps the lower half), so every step halves the
+// values a lane holds; the last value is then summed over the remaining
+// lanes.  Returns the value index (0..V-1) lane holds at the end; every lane
+// with the same index holds the same sum.
+template <int V, int H, int D>
+__device__ __forceinline__ void reduce_scatter_step(float (&a)[V], int lane, int& idx) {
+    if constexpr (H >= 1) {
+        const bool up = (lane & D) != 0;
+#pragma unroll
+        for (int j = 0; j < H; ++j) {
+            const float send = up ? a[j] : a[j + H];
+            const float keep = up ? a[j + H] : a[j];
+            a[j] = keep + __shfl_xor(send, D);
         }
-        f = perm[lo];
-        ci = cin_idx[k];
-        const int p = pat_id[k];
-        const unsigned mk = p < g.m ? g.mask[p] : 0u;
-        int t = 0;
+        if (up) idx += H;
+        reduce_scatter_step<V, H / 2, D / 2>(a, lane, idx);
+    } else {
 #pragma unroll
-        for (int u = 0; u < NT; ++u) q[u] = 4;
-        for (int u = 0; u < 9; ++u)
-            if ((mk >> u) & 1u) {
-                if (t < NT) q[t] = u;
-                ++t;
-            }
-        if (unsigned(ci) >= unsigned(g.cin) || p >= g.m || t != NT) ci = -1;   // malformed storage: no terms
+        for (int d = D; d >= 1; d /= 2) a[0] += __shfl_xor(a[0], d);
+    }
+}
+
+template <int V>
+__device__ __forceinline__ int wave_reduce_scatter(float (&a)[V], int lane) {
+    static_assert((V & (V - 1)) == 0 && V >= 2 && V <= 64, "V is a power of two from 2 to 64");
+    int idx = 0;
+    reduce_scatter_step<V, V / 2, 32>(a, lane, idx);
+    return idx;
+}
+
+struct WCtx {
+    __amdgpu_buffer_rsrc_t xs, dys;
+    int chan_bytes;
+};
+
+// The chunk [k0, k0 + kc) of one filter: kernels of one pattern segment with
+// taps Q (masked, NT = 4; QD: the positions come from q[] at run time), or the
+// dense kernels (f, ci0 + j) with all 9 taps.  Sums over the bands of slots
+// [sl0, sl1) go to out[(k0 + j) * NT + t], written by the lanes that hold
+// them after the reduction.
+template <int DT, int R, int NT, bool QD, int Q0, int Q1, int Q2, int Q3>
+__device__ __forceinline__ void run_chunk(const WGeo& g, const WCtx& c, const int32_t* __restrict__ cin_idx,
+                                          int f, int k0, int kc, int ci0, const int (&q)[4], int sl0, int sl1,
+                                          int lane, float* __restrict__ out) {
+    constexpr int ESZ = DT == DT_F32 ? 4 : 2;
+    float acc[kKC][NT];
+#pragma unroll
+    for (int j = 0; j < kKC; ++j)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[j][t] = 0.f;
+    int ci[kKC];
+#pragma unroll
+    for (int j = 0; j < kKC; ++j) {
+        const int kj = k0 + (j < kc ? j : 0);
+        // malformed channel indices read zeros (a range-checked load past x)
+        const int cj = g.dense ? ci0 + (j < kc ? j : 0) : cin_idx[kj];
+        ci[j] = __builtin_amdgcn_readfirstlane(unsigned(cj) < unsigned(g.cin) ? cj : 0x7fffffff / c.chan_bytes);
     }
     const int seg = lane / g.seg_len, cidx = lane - seg * g.seg_len;
-    const int plane = g.H * g.W;
-    float acc[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) acc[t] = 0.f;
-    const int sl0 = int(int64_t(g.slots) * s / g.KS), sl1 = int(int64_t(g.slots) * (s + 1) / g.KS);
     for (int sl = sl0; sl < sl1; ++sl) {
         const int u = sl * g.S + seg;
         int ld_col = -1, out_col = -1, nimg = 0, h0 = 0;
-        if (seg < g.S && u < g.units && ci >= 0) {
+        if (seg < g.S && u < g.units) {
             nimg = u / (g.RB * g.CT);
             const int rb = (u / g.CT) % g.RB, ct = u % g.CT;
             h0 = rb * R;
@@ -137,49 +196,298 @@ __global__ __launch_bounds__(256) void k_wgrad(const typename Elt<DT>::T* __rest
                 if (cidx >= 1 && cidx <= g.Wt && col < g.W) out_col = col;
             }
         }
-        float dyr[R], xc[R + 2], xl[R + 2], xr[R + 2];
-        const typename E::T* yp = dy + (int64_t(nimg) * g.cout + f) * plane;
-        const typename E::T* xp = x + (int64_t(nimg) * g.cin + (ci < 0 ? 0 : ci)) * plane;
+        uint32_t vy[R], vx[R + 2];
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int row = h0 + r;
-            dyr[r] = (out_col >= 0 && row < g.H) ? E::load(yp, row * g.W + out_col) : 0.f;
+            vy[r] = (out_col >= 0 && row < g.H)
+                        ? uint32_t(((nimg * g.cout + f) * g.H + row) * g.W + out_col) * uint32_t(ESZ)
+                        : 0x80000000u;
         }
 #pragma unroll
         for (int r = 0; r < R + 2; ++r) {
             const int row = h0 - 1 + r;
-            xc[r] = (ld_col >= 0 && row >= 0 && row < g.H) ? E::load(xp, row * g.W + ld_col) : 0.f;
+            vx[r] = (ld_col >= 0 && row >= 0 && row < g.H)
+                        ? uint32_t((nimg * g.cin * g.H + row) * g.W + ld_col) * uint32_t(ESZ)
+                        : 0x80000000u;
         }
+        float dyr[R];
+        load_col<DT, R>(c.dys, vy, 0, dyr);
+        float xk[kKC][R + 2];
 #pragma unroll
-        for (int r = 0; r < R + 2; ++r) {
-            xl[r] = dpp_shift(xc[r], 1);
-            xr[r] = dpp_shift(xc[r], 0);
-        }
-        if constexpr (NT == 9) {
-            tap_rows<R, 0>(acc[0], dyr, xl);
-            tap_rows<R, 0>(acc[1], dyr, xc);
-            tap_rows<R, 0>(acc[2], dyr, xr);
-            tap_rows<R, 1>(acc[3], dyr, xl);
-            tap_rows<R, 1>(acc[4], dyr, xc);
-            tap_rows<R, 1>(acc[5], dyr, xr);
-            tap_rows<R, 2>(acc[6], dyr, xl);
-            tap_rows<R, 2>(acc[7], dyr, xc);
-            tap_rows<R, 2>(acc[8], dyr, xr);
-        } else {
+        for (int j = 0; j < kKC; ++j)
+            if (j < kc) load_col<DT, R + 2>(c.xs, vx, ci[j] * c.chan_bytes, xk[j]);
 #pragma unroll
-            for (int t = 0; t < NT; ++t) tap_dyn<R>(q[t], acc[t], dyr, xl, xc, xr);
+        for (int j = 0; j < kKC; ++j) {
+            if (j < kc) {
+                settle<R + 2>(xk[j]);
+                if constexpr (NT == 9) {
+                    wtap<R, 0>(acc[j][0], xk[j], dyr);
+                    wtap<R, 1>(acc[j][1], xk[j], dyr);
+                    wtap<R, 2>(acc[j][2], xk[j], dyr);
+                    wtap<R, 3>(acc[j][3], xk[j], dyr);
+                    wtap<R, 4>(acc[j][4], xk[j], dyr);
+                    wtap<R, 5>(acc[j][5], xk[j], dyr);
+                    wtap<R, 6>(acc[j][6], xk[j], dyr);
+                    wtap<R, 7>(acc[j][7], xk[j], dyr);
+                    wtap<R, 8>(acc[j][8], xk[j], dyr);
+                } else if constexpr (QD) {
+                    wtap_dyn<R>(q[0], acc[j][0], xk[j], dyr);
+                    wtap_dyn<R>(q[1], acc[j][1], xk[j], dyr);
+                    wtap_dyn<R>(q[2], acc[j][2], xk[j], dyr);
+                    wtap_dyn<R>(q[3], acc[j][3], xk[j], dyr);
+                } else {
+                    wtap<R, Q0>(acc[j][0], xk[j], dyr);
+                    wtap<R, Q1>(acc[j][1], xk[j], dyr);
+                    wtap<R, Q2>(acc[j][2], xk[j], dyr);
+                    wtap<R, Q3>(acc[j][3], xk[j], dyr);
+                }
+            }
         }
     }
+    if constexpr (NT == 4) {
+        float a[kKC * 4];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        float v = acc[t];
-        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-        acc[t] = v;
+        for (int j = 0; j < kKC; ++j)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) a[j * 4 + t] = acc[j][t];
+        const int v = wave_reduce_scatter<kKC * 4>(a, lane);
+        // lanes with the same index hold the same sum: the lowest one writes it
+        if ((lane & (64 / (kKC * 4) - 1)) == 0 && v / 4 < kc) out[int64_t(k0 + v / 4) * 4 + (v % 4)] = a[0];
+    } else {
+#pragma unroll
+        for (int j = 0; j < kKC; ++j)
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                float v = acc[j][t];
+                for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+                acc[j][t] = v;
+            }
+        if (lane == 0)
+#pragma unroll
+            for (int j = 0; j < kKC; ++j)
+                if (j < kc)
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) out[int64_t(k0 + j) * NT + t] = acc[j][t];
     }
-    if (lane == 0) {
-        float* o = out + (int64_t(s) * g.nk + k) * NT;
+}
+
+// ---- one image row per lane (small planes at large batch).  A wave holds S
+// images, H row lanes each and a zero lane after each image; per image group
+// a lane loads its dy row once (16-byte loads) and, for each kernel of the
+// chunk, its x row; the rows above and below come from the neighbouring
+// lanes by DPP inside the FMA, the left and right columns are other
+// registers of the lane.
+#define PSC_W_SHR "v_fmac_f32_dpp %0, %1, %2 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+#define PSC_W_SHL "v_fmac_f32_dpp %0, %1, %2 wave_shl:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+// acc += sum_c x(row r + ky - 1, column c + kx - 1) * dy[c] over the columns
+// inside the row.
+template <int W, int Q>
+__device__ __forceinline__ void wtap_row(float& acc, const float (&x)[W], const float (&dyv)[W]) {
+    constexpr int ky = Q / 3, kx = Q % 3;
+    constexpr int c0 = kx == 0 ? 1 : 0, c1 = kx == 2 ? W - 1 : W;
 #pragma unroll
-        for (int t = 0; t < NT; ++t) o[t] = acc[t];
+    for (int c = c0; c < c1; ++c) {
+        if constexpr (ky == 1)
+            acc = __builtin_fmaf(x[c + kx - 1], dyv[c], acc);
+        else if constexpr (ky == 0)
+            asm volatile(PSC_W_SHR : "+v"(acc) : "v"(x[c + kx - 1]), "v"(dyv[c]));
+        else
+            asm volatile(PSC_W_SHL : "+v"(acc) : "v"(x[c + kx - 1]), "v"(dyv[c]));
+    }
+}
+#undef PSC_W_SHL
+#undef PSC_W_SHR
+
+template <int W>
+__device__ __forceinline__ void wtap_row_dyn(int q, float& acc, const float (&x)[W], const float (&dyv)[W]) {
+    switch (q) {
+        case 0: wtap_row<W, 0>(acc, x, dyv); break;
+        case 1: wtap_row<W, 1>(acc, x, dyv); break;
+        case 2: wtap_row<W, 2>(acc, x, dyv); break;
+        case 3: wtap_row<W, 3>(acc, x, dyv); break;
+        case 4: wtap_row<W, 4>(acc, x, dyv); break;
+        case 5: wtap_row<W, 5>(acc, x, dyv); break;
+        case 6: wtap_row<W, 6>(acc, x, dyv); break;
+        case 7: wtap_row<W, 7>(acc, x, dyv); break;
+        default: wtap_row<W, 8>(acc, x, dyv); break;
+    }
+}
+
+template <int DT, int W, bool QD, int Q0, int Q1, int Q2, int Q3>
+__device__ __forceinline__ void run_chunk_rows(const WGeo& g, const WCtx& c, const int32_t* __restrict__ cin_idx,
+                                               int f, int k0, int kc, const int (&q)[4], int sl0, int sl1,
+                                               int lane, float* __restrict__ out) {
+    constexpr int ESZ = DT == DT_F32 ? 4 : 2;
+    float acc[kKC][4];
+#pragma unroll
+    for (int j = 0; j < kKC; ++j)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[j][t] = 0.f;
+    int soff[kKC];
+#pragma unroll
+    for (int j = 0; j < kKC; ++j) {
+        const int cj = cin_idx[k0 + (j < kc ? j : 0)];
+        // malformed channel indices read zeros (an offset past the range of x)
+        soff[j] = __builtin_amdgcn_readfirstlane(unsigned(cj) < unsigned(g.cin) ? cj * c.chan_bytes : 0x7fffffff);
+    }
+    const int seg = lane / g.seg_len, r = lane - seg * g.seg_len;
+    for (int sl = sl0; sl < sl1; ++sl) {
+        const int img = sl * g.S + seg;
+        const bool valid = seg < g.S && img < g.n && r < g.H;
+        const uint32_t vx = valid ? uint32_t((img * g.cin * g.H + r) * g.W) * uint32_t(ESZ) : 0x80000000u;
+        const uint32_t vy = valid ? uint32_t(((img * g.cout + f) * g.H + r) * g.W) * uint32_t(ESZ) : 0x80000000u;
+        rw::RowWords<DT, W, 1> wy, wx[kKC];
+        rw::load_words<DT, W, 1>(c.dys, vy, 0x80000000u, 0, g.dy_bytes, valid, wy);
+#pragma unroll
+        for (int j = 0; j < kKC; ++j)
+            if (j < kc) rw::load_words<DT, W, 1>(c.xs, vx, 0x80000000u, soff[j], g.x_bytes, valid, wx[j]);
+        rw::RowVals<W, 1> yv;
+        rw::unpack_vals<DT, W, 1>(wy, yv);
+#pragma unroll
+        for (int j = 0; j < kKC; ++j) {
+            if (j < kc) {
+                rw::RowVals<W, 1> xv;
+                rw::unpack_vals<DT, W, 1>(wx[j], xv);   // ends with the settle a DPP source needs
+                if constexpr (QD) {
+                    wtap_row_dyn<W>(q[0], acc[j][0], xv.e, yv.e);
+                    wtap_row_dyn<W>(q[1], acc[j][1], xv.e, yv.e);
+                    wtap_row_dyn<W>(q[2], acc[j][2], xv.e, yv.e);
+                    wtap_row_dyn<W>(q[3], acc[j][3], xv.e, yv.e);
+                } else {
+                    wtap_row<W, Q0>(acc[j][0], xv.e, yv.e);
+                    wtap_row<W, Q1>(acc[j][1], xv.e, yv.e);
+                    wtap_row<W, Q2>(acc[j][2], xv.e, yv.e);
+                    wtap_row<W, Q3>(acc[j][3], xv.e, yv.e);
+                }
+            }
+        }
+    }
+    float a[kKC * 4];
+#pragma unroll
+    for (int j = 0; j < kKC; ++j)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) a[j * 4 + t] = acc[j][t];
+    const int v = wave_reduce_scatter<kKC * 4>(a, lane);
+    if ((lane & (64 / (kKC * 4) - 1)) == 0 && v / 4 < kc) out[int64_t(k0 + v / 4) * 4 + (v % 4)] = a[0];
+}
+
+template <int DT, int W, int MASK>
+__device__ __forceinline__ void run_chunk_rows_shape(const WGeo& g, const WCtx& c, const int32_t* cin_idx, int f,
+                                                     int k0, int kc, const int (&q)[4], int sl0, int sl1, int lane,
+                                                     float* out) {
+    run_chunk_rows<DT, W, false, NthBit<MASK, 0>::value(), NthBit<MASK, 1>::value(), NthBit<MASK, 2>::value(),
+                   NthBit<MASK, 3>::value()>(g, c, cin_idx, f, k0, kc, q, sl0, sl1, lane, out);
+}
+
+#define PSC_WR_CASE(I) \
+    case I: run_chunk_rows_shape<DT, W, kCentre3.code[I]>(g, c, cin_idx, f, k0, kc, q, sl0, sl1, lane, out); return;
+#define PSC_WR_CASE8(I)                                                                             \
+    PSC_WR_CASE(I) PSC_WR_CASE(I + 1) PSC_WR_CASE(I + 2) PSC_WR_CASE(I + 3) PSC_WR_CASE(I + 4)      \
+    PSC_WR_CASE(I + 5) PSC_WR_CASE(I + 6) PSC_WR_CASE(I + 7)
+template <int DT, int W>
+__device__ __forceinline__ void run_chunk_rows_pattern(int shape, const WGeo& g, const WCtx& c,
+                                                       const int32_t* cin_idx, int f, int k0, int kc,
+                                                       const int (&q)[4], int sl0, int sl1, int lane, float* out) {
+    switch (shape) {
+        PSC_WR_CASE8(0)
+        PSC_WR_CASE8(8)
+        PSC_WR_CASE8(16)
+        PSC_WR_CASE8(24)
+        PSC_WR_CASE8(32)
+        PSC_WR_CASE8(40)
+        PSC_WR_CASE8(48)
+        default: run_chunk_rows<DT, W, true, 0, 0, 0, 0>(g, c, cin_idx, f, k0, kc, q, sl0, sl1, lane, out); return;
+    }
+}
+#undef PSC_WR_CASE8
+#undef PSC_WR_CASE
+
+template <int DT, int R, int MASK>
+__device__ __forceinline__ void run_chunk_shape(const WGeo& g, const WCtx& c, const int32_t* cin_idx, int f, int k0,
+                                                int kc, const int (&q)[4], int sl0, int sl1, int lane, float* out) {
+    run_chunk<DT, R, 4, false, NthBit<MASK, 0>::value(), NthBit<MASK, 1>::value(), NthBit<MASK, 2>::value(),
+              NthBit<MASK, 3>::value()>(g, c, cin_idx, f, k0, kc, 0, q, sl0, sl1, lane, out);
+}
+
+#define PSC_WG_CASE(I) \
+    case I: run_chunk_shape<DT, R, kCentre3.code[I]>(g, c, cin_idx, f, k0, kc, q, sl0, sl1, lane, out); return;
+#define PSC_WG_CASE8(I)                                                                             \
+    PSC_WG_CASE(I) PSC_WG_CASE(I + 1) PSC_WG_CASE(I + 2) PSC_WG_CASE(I + 3) PSC_WG_CASE(I + 4)      \
+    PSC_WG_CASE(I + 5) PSC_WG_CASE(I + 6) PSC_WG_CASE(I + 7)
+template <int DT, int R>
+__device__ __forceinline__ void run_chunk_pattern(int shape, const WGeo& g, const WCtx& c, const int32_t* cin_idx,
+                                                  int f, int k0, int kc, const int (&q)[4], int sl0, int sl1,
+                                                  int lane, float* out) {
+    switch (shape) {
+        PSC_WG_CASE8(0)
+        PSC_WG_CASE8(8)
+        PSC_WG_CASE8(16)
+        PSC_WG_CASE8(24)
+        PSC_WG_CASE8(32)
+        PSC_WG_CASE8(40)
+        PSC_WG_CASE8(48)
+        default: run_chunk<DT, R, 4, true, 0, 0, 0, 0>(g, c, cin_idx, f, k0, kc, 0, q, sl0, sl1, lane, out); return;
+    }
+}
+#undef PSC_WG_CASE8
+#undef PSC_WG_CASE
+
+// One wave per (filter, chunk group, image share); chunk j of the filter
+// (counted over its pattern segments in storage order) belongs to group
+// j % G.
+// W > 0: one image row per lane (masked gradients on planes of W columns).
+template <int DT, int R, int NT, int W = 0>
+__global__ __launch_bounds__(256) void k_wgrad(const typename Elt<DT>::T* __restrict__ x,
+                                               const typename Elt<DT>::T* __restrict__ dy,
+                                               const int32_t* __restrict__ perm, const int32_t* __restrict__ seg_ptr,
+                                               const int32_t* __restrict__ cin_idx, WGeo g, float* __restrict__ out) {
+    using E = Elt<DT>;
+    constexpr int ESZ = int(sizeof(typename E::T));
+    const int lane = threadIdx.x & 63;
+    const int64_t wid = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    const int64_t per_filter = int64_t(g.G) * g.KS;
+    const int i = __builtin_amdgcn_readfirstlane(int(wid / per_filter));
+    if (i >= g.cout) return;                                 // whole waves leave together
+    const int rem = int(wid - int64_t(i) * per_filter);
+    const int grp = rem / g.KS, s = rem - grp * g.KS;
+    const int sl0 = int(int64_t(g.slots) * s / g.KS), sl1 = int(int64_t(g.slots) * (s + 1) / g.KS);
+    WCtx c;
+    c.xs = __builtin_amdgcn_make_buffer_rsrc(const_cast<typename E::T*>(x), int16_t(0), g.x_bytes, 0x00020000);
+    c.dys = __builtin_amdgcn_make_buffer_rsrc(const_cast<typename E::T*>(dy), int16_t(0), g.dy_bytes, 0x00020000);
+    c.chan_bytes = g.H * g.W * ESZ;
+    float* o = out + int64_t(s) * g.nk * NT;
+    const int q0[4] = {4, 4, 4, 4};
+    if constexpr (NT == 9) {
+        const int f = i;
+        int j = 0;
+        for (int c0 = 0; c0 < g.cin; c0 += kKC, ++j) {
+            if (j % g.G != grp) continue;
+            const int kc = g.cin - c0 < kKC ? g.cin - c0 : kKC;
+            run_chunk<DT, R, 9, false, 0, 0, 0, 0>(g, c, nullptr, f, f * g.cin + c0, kc, c0, q0, sl0, sl1, lane, o);
+        }
+    } else {
+        const int f = perm[i];
+        const int* segp = seg_ptr + int64_t(i) * (g.m + 1);
+        int j = 0;
+        for (int p = 0; p < g.m; ++p) {
+            const int k1 = segp[p + 1];
+            int q[4] = {4, 4, 4, 4}, t = 0;
+            const unsigned mk = g.mask[p];
+            for (int u = 0; u < 9; ++u)
+                if ((mk >> u) & 1u) {
+                    if (t < 4) q[t] = u;
+                    ++t;
+                }
+            for (int k0 = segp[p]; k0 < k1; k0 += kKC, ++j) {
+                if (j % g.G != grp) continue;
+                const int kc = k1 - k0 < kKC ? k1 - k0 : kKC;
+                if constexpr (W > 0)
+                    run_chunk_rows_pattern<DT, W>(g.shape[p], g, c, cin_idx, f, k0, kc, q, sl0, sl1, lane, o);
+                else
+                    run_chunk_pattern<DT, R>(g.shape[p], g, c, cin_idx, f, k0, kc, q, sl0, sl1, lane, o);
+            }
+        }
     }
 }
 
@@ -211,10 +519,10 @@ __global__ __launch_bounds__(256) void k_bias_grad(const typename Elt<DT>::T* __
     if (threadIdx.x == 0) db[f] = (part[0] + part[1]) + (part[2] + part[3]);
 }
 
-constexpr int kTargetWaves = 32768;
+constexpr int64_t kTargetWaves = 16384;   // 16 waves per SIMD
 constexpr int kMaxShares = 64;
 
-WGeo plan(int n, int cin, int cout, int h, int w, int64_t nk, bool dense, const PatTable* tab) {
+WGeo plan(int n, int cin, int cout, int h, int w, int64_t nk, bool dense, const PatTable* tab, int dtype) {
     WGeo g{};
     g.n = n;
     g.cin = cin;
@@ -224,25 +532,72 @@ WGeo plan(int n, int cin, int cout, int h, int w, int64_t nk, bool dense, const 
     g.nk = nk;
     g.dense = dense ? 1 : 0;
     g.m = tab ? tab->m : 0;
-    for (int p = 0; p < kMaxPatterns; ++p) g.mask[p] = (tab && p < tab->m) ? tab->mask[p] : 0;
-    if (w <= 63) {
-        g.cols_mode = 0;
-        g.seg_len = w + 1;
-        g.S = 65 / (w + 1);
+    for (int p = 0; p < kMaxPatterns; ++p) {
+        g.mask[p] = (tab && p < tab->m) ? tab->mask[p] : 0;
+        g.shape[p] = -1;
+        if (tab && p < tab->m)
+            for (int t = 0; t < 56; ++t)
+                if (kCentre3.code[t] == tab->mask[p]) g.shape[p] = int8_t(t);
+    }
+    const int64_t esz = dtype == DT_F16 ? 2 : 4;
+    const int64_t xb = int64_t(n) * cin * h * w * esz, yb = int64_t(n) * cout * h * w * esz;
+    g.x_bytes = int(xb > 0x7fffffff ? 0x7fffffff : xb);
+    g.dy_bytes = int(yb > 0x7fffffff ? 0x7fffffff : yb);
+    // one image row per lane: masked gradients on compiled widths when the
+    // batch fills a wave with whole images
+    const bool wfit = w == 4 || w == 7 || w == 8 || w == 14 || w == 16;
+    if (!dense && wfit && h <= 63 && n >= 64 / (h + 1)) {
+        g.rows = 1;
+        g.seg_len = h + 1;
+        g.S = 64 / (h + 1);
         g.Wt = w;
         g.CT = 1;
+        g.RB = 1;
+        g.units = n;
+        g.slots = (n + g.S - 1) / g.S;
     } else {
-        g.cols_mode = 1;
-        g.Wt = 62;
-        g.seg_len = 64;
-        g.S = 1;
-        g.CT = (w + 61) / 62;
+        // full-row segments if they use the lanes at least as well as
+        // haloed column tiles (the forward's choice)
+        const int S_rows = w <= 63 ? 65 / (w + 1) : 0;
+        const int use_rows = S_rows * w;
+        int ct = (w + 61) / 62, use_cols = 0;
+        for (int t = ct; t <= w && t <= 64; ++t) {
+            const int wt = (w + t - 1) / t;
+            const int use = (64 / (wt + 2)) * w / t;
+            if (use > use_cols) {
+                use_cols = use;
+                ct = t;
+            }
+        }
+        if (S_rows > 0 && use_rows >= use_cols) {
+            g.cols_mode = 0;
+            g.seg_len = w + 1;
+            g.S = S_rows;
+            g.Wt = w;
+            g.CT = 1;
+        } else {
+            g.cols_mode = 1;
+            g.Wt = (w + ct - 1) / ct;
+            g.seg_len = g.Wt + 2;
+            g.S = 64 / g.seg_len;
+            g.CT = ct;
+        }
     }
-    const int R = h >= 8 ? 8 : 4;
-    g.RB = (h + R - 1) / R;
-    g.units = n * g.RB * g.CT;
-    g.slots = (g.units + g.S - 1) / g.S;
-    int64_t ks = nk > 0 ? (kTargetWaves + nk - 1) / nk : 1;
+    if (!g.rows) {
+        const int R = h >= 8 ? 8 : 4;
+        g.RB = (h + R - 1) / R;
+        g.units = n * g.RB * g.CT;
+        g.slots = (g.units + g.S - 1) / g.S;
+    }
+    // chunks of a filter: about its kernels / KC (the reordered filters run
+    // from the most kept kernels down); spread them over G waves first, then
+    // split the images into shares until the grid holds about kTargetWaves
+    const int64_t per = cout > 0 ? (dense ? cin : (nk + cout - 1) / cout) : 0;
+    const int64_t chunks = (per + kKC - 1) / kKC;
+    int64_t G = cout > 0 ? kTargetWaves / cout : 1;
+    if (G > chunks) G = chunks;
+    g.G = int(G < 1 ? 1 : G);
+    int64_t ks = cout > 0 ? kTargetWaves / (int64_t(cout) * g.G) : 1;
     if (ks > g.slots) ks = g.slots;
     if (ks > kMaxShares) ks = kMaxShares;
     g.KS = int(ks < 1 ? 1 : ks);
@@ -250,18 +605,38 @@ WGeo plan(int n, int cin, int cout, int h, int w, int64_t nk, bool dense, const 
 }
 
 template <int DT, int NT>
-hipError_t run(const WGeo& g, const void* x, const void* dy, const int32_t* perm, const int32_t* fptr,
-               const int32_t* cin_idx, const uint8_t* pat_id, float* out, void* ws, hipStream_t stream) {
+hipError_t run(const WGeo& g, const void* x, const void* dy, const int32_t* perm, const int32_t* seg_ptr,
+               const int32_t* cin_idx, float* out, void* ws, hipStream_t stream) {
     using T = typename Elt<DT>::T;
-    if (g.nk == 0) return hipSuccess;
+    if (g.nk == 0 || g.n == 0) return hipSuccess;
     float* dst = g.KS > 1 ? static_cast<float*>(ws) : out;
-    const dim3 grid(unsigned((g.nk * g.KS + 3) / 4));
-    if (g.H >= 8)
-        hipLaunchKernelGGL((k_wgrad<DT, 8, NT>), grid, dim3(256), 0, stream, static_cast<const T*>(x),
-                           static_cast<const T*>(dy), perm, fptr, cin_idx, pat_id, g, dst);
-    else
-        hipLaunchKernelGGL((k_wgrad<DT, 4, NT>), grid, dim3(256), 0, stream, static_cast<const T*>(x),
-                           static_cast<const T*>(dy), perm, fptr, cin_idx, pat_id, g, dst);
+    const int64_t waves = int64_t(g.cout) * g.G * g.KS;
+    const dim3 grid(unsigned((waves + 3) / 4));
+#define PSC_WROWS(WW)                                                                                    \
+    hipLaunchKernelGGL((k_wgrad<DT, 4, NT, WW>), grid, dim3(256), 0, stream, static_cast<const T*>(x),          \
+                       static_cast<const T*>(dy), perm, seg_ptr, cin_idx, g, dst)
+    bool done = false;
+    if constexpr (NT == 4) {
+        if (g.rows) {
+            switch (g.W) {
+                case 4: PSC_WROWS(4); break;
+                case 7: PSC_WROWS(7); break;
+                case 8: PSC_WROWS(8); break;
+                case 14: PSC_WROWS(14); break;
+                default: PSC_WROWS(16); break;
+            }
+            done = true;
+        }
+    }
+#undef PSC_WROWS
+    if (!done) {
+        if (g.H >= 8)
+            hipLaunchKernelGGL((k_wgrad<DT, 8, NT>), grid, dim3(256), 0, stream, static_cast<const T*>(x),
+                               static_cast<const T*>(dy), perm, seg_ptr, cin_idx, g, dst);
+        else
+            hipLaunchKernelGGL((k_wgrad<DT, 4, NT>), grid, dim3(256), 0, stream, static_cast<const T*>(x),
+                               static_cast<const T*>(dy), perm, seg_ptr, cin_idx, g, dst);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || g.KS == 1) return e;
     const int64_t n = g.nk * NT;
@@ -280,18 +655,24 @@ hipError_t bias_grad(const void* dy, int n, int cout, int plane, float* db, hipS
 
 }  // namespace
 
+// Buffer descriptors address at most 2 GiB of x and of dy.
+bool wgrad_fits(int n, int cin, int cout, int h, int w, int dtype) {
+    const int64_t esz = dtype == DT_F16 ? 2 : 4;
+    return int64_t(n) * cin * h * w * esz <= 0x7fffffff && int64_t(n) * cout * h * w * esz <= 0x7fffffff;
+}
+
 size_t wgrad_workspace_bytes(int n, int cin, int cout, int h, int w, int64_t nk, bool dense) {
-    const WGeo g = plan(n, cin, cout, h, w, nk, dense, nullptr);
-    return g.KS > 1 ? size_t(g.KS) * size_t(nk) * (dense ? 9 : 4) * sizeof(float) : 0;
+    const WGeo g = plan(n, cin, cout, h, w, nk, dense, nullptr, DT_F32);
+    return g.KS > 1 && n > 0 ? size_t(g.KS) * size_t(nk) * (dense ? 9 : 4) * sizeof(float) : 0;
 }
 
 hipError_t launch_bwd_weight(const PatTable& tab, const PackedView& pk, int dtype, int n, int cin, int h, int w,
                              int cout, int64_t keep, const void* x, const void* dy, float* dv, float* db, void* ws,
                              hipStream_t stream) {
-    const WGeo g = plan(n, cin, cout, h, w, keep, false, &tab);
+    const WGeo g = plan(n, cin, cout, h, w, keep, false, &tab, dtype);
     hipError_t e = dtype == DT_F16
-                       ? run<DT_F16, 4>(g, x, dy, pk.filter_perm, pk.filter_ptr, pk.cin_idx, pk.pat_id, dv, ws, stream)
-                       : run<DT_F32, 4>(g, x, dy, pk.filter_perm, pk.filter_ptr, pk.cin_idx, pk.pat_id, dv, ws, stream);
+                       ? run<DT_F16, 4>(g, x, dy, pk.filter_perm, pk.seg_ptr, pk.cin_idx, dv, ws, stream)
+                       : run<DT_F32, 4>(g, x, dy, pk.filter_perm, pk.seg_ptr, pk.cin_idx, dv, ws, stream);
     if (e != hipSuccess || !db) return e;
     return dtype == DT_F16 ? bias_grad<DT_F16>(dy, n, cout, h * w, db, stream)
                            : bias_grad<DT_F32>(dy, n, cout, h * w, db, stream);
@@ -299,8 +680,8 @@ hipError_t launch_bwd_weight(const PatTable& tab, const PackedView& pk, int dtyp
 
 hipError_t launch_dense_wgrad(const float* x, const float* g_, int n, int cin, int h, int w, int cout, float* dw,
                               float* db, void* ws, hipStream_t stream) {
-    const WGeo g = plan(n, cin, cout, h, w, int64_t(cout) * cin, true, nullptr);
-    hipError_t e = run<DT_F32, 9>(g, x, g_, nullptr, nullptr, nullptr, nullptr, dw, ws, stream);
+    const WGeo g = plan(n, cin, cout, h, w, int64_t(cout) * cin, true, nullptr, DT_F32);
+    hipError_t e = run<DT_F32, 9>(g, x, g_, nullptr, nullptr, nullptr, dw, ws, stream);
     if (e != hipSuccess || !db) return e;
     return bias_grad<DT_F32>(g_, n, cout, h * w, db, stream);
 }

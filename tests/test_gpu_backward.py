@@ -36,6 +36,12 @@ SHAPES = [
     # cin != cout, and full-size layers of the VGG-16 and ResNet-50 workloads
     (2, 5, 7, 9, 11), (1, 3, 8, 1, 1), (3, 8, 5, 6, 70), (2, 16, 24, 14, 14), (1, 24, 12, 28, 28),
     (2, 9, 6, 7, 130), (1, 512, 512, 28, 28), (32, 256, 256, 14, 14),
+    # whole waves of small images (one image row per lane in both passes):
+    # every compiled width, ragged image groups, rows unequal to columns, odd
+    # n, cin and cout (fp16 width 7: rows read through a shifted window, the
+    # last row of x and of dy at the end of its buffer)
+    (13, 5, 6, 4, 4), (9, 7, 5, 7, 7), (11, 3, 5, 7, 7), (8, 16, 9, 8, 8), (7, 4, 5, 5, 8),
+    (5, 6, 7, 14, 14), (4, 10, 6, 16, 16), (32, 64, 64, 7, 7),
 ]
 
 
