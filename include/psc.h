@@ -341,6 +341,13 @@ psc_status psc_dense3x3_fwd(int32_t dtype, const void *d_x, int32_t n, int32_t c
 psc_status psc_maxpool2x2(int32_t dtype, const void *d_x, int32_t n, int32_t c,
                           int32_t h, int32_t w, void *d_y, void *stream);
 
+/* Measurement probe, not part of the method: blocks x 256 lanes each run 8
+ * independent chains of iters fp32 FMAs (v_fmac_f32; packed fp32 is disabled
+ * in this build) and store one sum to d_out [blocks*256] (fp32, device).
+ * Timing it gives the vector-ALU FMA rate the conv kernels can reach:
+ * 2 * 8 * iters * blocks * 256 flops.  blocks in 1..2^20, iters >= 0. */
+psc_status psc_probe_fma(int32_t blocks, int32_t iters, float *d_out, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -94,6 +94,7 @@ def lib() -> ctypes.CDLL:
         "psc_unpack_dense": ([LP, PP, P, P], ctypes.c_int),
         "psc_conv3x3_fwd": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, P], ctypes.c_int),
         "psc_conv3x3_fwd_algo": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, P], ctypes.c_int),
+        "psc_probe_fma": ([i32, i32, P, P], ctypes.c_int),
         "psc_conv3x3_fwd_pool2": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, P], ctypes.c_int),
         "psc_conv3x3_fwd_strided": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, i32, P], ctypes.c_int),
         "psc_conv3x3_config": ([LP, i32, i32, i32, i32, i32, i32, i32, ctypes.POINTER(CConvConfig)],
@@ -319,6 +320,12 @@ def dense3x3_fwd(x, wd, y, bias=None, relu: bool = False, stream=None):
     _check(lib().psc_dense3x3_fwd(dtype_code(x), _dev(x, "x"), n, cin, h, w, _dev(wd, "w"), cout,
                                   _dev(bias, "bias"), int(bool(relu)), _dev(y, "y"), _stream(stream)),
            "psc_dense3x3_fwd")
+
+
+def probe_fma(blocks: int, iters: int, out, stream=None):
+    """psc_probe_fma: 2 * 8 * iters * blocks * 256 fp32 FMA flops into out
+    [blocks*256] (measurement only)."""
+    _check(lib().psc_probe_fma(int(blocks), int(iters), _dev(out, "out"), _stream(stream)), "psc_probe_fma")
 
 
 def maxpool2x2(x, y, stream=None):
