@@ -37,7 +37,8 @@ constexpr int64_t kSplitWaves = 4096;
 //
 // Launch configuration.  Rows per lane R minimise the lane-rows loaded
 // (ceil(units / S) * (R + 2)) in throughput-bound grids, the lane-rows
-// issued (ceil(units / S) * R) otherwise, larger R on ties; even R when
+// issued (ceil(units / S) * R) otherwise, larger R on ties (7 over 8 for
+// staged single-segment grids of long kernel chains); even R when
 // pooling; R = 8 only with one segment per wave.  A workgroup holds 4
 // filters, or fewer filters split into KS shares (KS doubles up to 8) while
 // the grid holds under 4 waves per SIMD.  Returns false when the tuned kernels do not
@@ -130,12 +131,17 @@ bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
     const bool many_waves = (units4 + g.S - 1) / g.S * a.cout >= kManyWaves;
     // 8 rows per lane only with one segment per wave (see the note on R = 8
     // above)
+    // filters with long kernel chains (32 or more kept kernels) on one
+    // full-row segment per wave run staged (below); there R = 7 beats R = 8
+    // at the same cost (one more band, more waves)
+    const bool long_chains = a.cout > 0 && a.keep >= 32 * int64_t(a.cout);
+    const bool prefer_small = !g.cols_mode && g.S == 1 && long_chains;
     for (int rr : cand) {
         if (a.pool && (rr & 1)) continue;               // pooled rows pair up inside a lane
         if (rr == 8 && g.S > 1) continue;
         const int64_t units = int64_t(a.n) * ((a.h + rr - 1) / rr) * g.CT;
         const int64_t cost = (units + g.S - 1) / g.S * (many_waves ? rr + 2 : rr);
-        if (best < 0 || cost < best) {
+        if (best < 0 || cost < best || (prefer_small && cost == best && rr == 7 && R == 8)) {
             best = cost;
             R = rr;
         }
@@ -145,6 +151,7 @@ bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
     const int sgroups = (g.U + g.S - 1) / g.S;
     g.KS = 1;
     while (g.KS < kMaxSplit && int64_t(sgroups) * a.cout * g.KS < kSplitWaves && a.cin >= 16 * g.KS) g.KS *= 2;
+    if (prefer_small && g.KS > 2) g.KS = 2;   // staged long chains: 2 shares measured best
     g.FW = g.KS >= 4 ? 1 : 4 / g.KS;
     if (g.FW > a.cout) g.FW = a.cout;
     const int fgroups = (a.cout + g.FW - 1) / g.FW;
@@ -181,9 +188,11 @@ bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
                           (a.dtype != DT_F16 || a.w % 2 == 0);
         // one full-row segment per wave and a grid of about one round of
         // waves (batch 1 at W >= 32) is bound by the per-kernel latency,
-        // which the direct loads keep shorter
+        // which the direct loads keep shorter -- unless each filter has a
+        // long chain of kernels, where the staged copies run ahead better
+        // (measured on the 56x56 VGG-16 layers at batch 1)
         const int64_t waves = int64_t(sgroups) * a.cout * 4;   // at 4 shares per filter
-        const bool throughput = g.S >= 2 || waves >= 2 * 6 * 1024;
+        const bool throughput = g.S >= 2 || waves >= 2 * 6 * 1024 || long_chains;
         g.lds = fits && throughput ? 1 : 0;
         if (g.lds && nruns_max > 1) g.lds = 2;             // several runs per wave: the general form
     }
