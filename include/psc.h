@@ -310,7 +310,8 @@ typedef struct psc_conv_config {
     int32_t kernel;            /* 0: tuned kernel, one output column per lane
                                   1: tuned kernel, 4 output columns per lane
                                   2: one-output-per-lane kernel
-                                  3: stride-2 kernel, one output column per lane
+                                  3: stride-2 kernel, 1 output column per lane
+                                     (2 when w is a multiple of 4)
                                   4: one output row per lane (all w columns) */
     int32_t staged;            /* 0: input rows loaded straight into registers,
                                   1: staged through LDS, one run per wave,

@@ -4,31 +4,34 @@
 //
 // As in the stride-1 kernels, one wave walks one reordered filter's
 // compressed storage (Sec. 3.4) and its lanes hold output pixels: a lane
-// owns output column j and R output rows of a band; a wave holds S bands of
-// full output rows, each followed by one zero lane.  Output (i, j) reads
-// input rows 2i-1..2i+1 and columns 2j-1..2j+1, so for each kernel a lane
-// loads, for the 2R+1 input rows its R output rows need, columns 2j and
-// 2j+1 in one 8-byte (fp32) or 4-byte (fp16) buffer load at an offset fixed
-// per lane and row (the channel enters as a scalar offset; padding rows and
-// lanes point past the buffer range and read zero), and column 2j-1 -- the
-// left lane's column 2(j-1)+1 -- is read by DPP inside the FMA
-// (v_fmac_f32_dpp wave_shr:1).  The wave walks the filter's storage one
-// pattern segment after another, each through a loop compiled with that
-// centre+3 shape's taps fixed (other masks take a loop that dispatches each
-// tap); channel index and weights are wave-uniform (scalar buffer loads).
-// The next kernel's rows load while the current kernel's FMAs run.
+// owns C adjacent output columns (C = 1, or 2 when W is a multiple of 4) and
+// R output rows of a band; a wave holds S bands of full output rows, each
+// followed by one zero lane.  Output (i, j) reads input rows 2i-1..2i+1 and
+// columns 2j-1..2j+1, so for each kernel a lane loads, for the 2R+1 input
+// rows its R output rows need, its 2C input columns in one buffer load (C =
+// 1: 8 bytes fp32 / 4 fp16; C = 2: 16 / 8) at an offset fixed per lane and
+// row (the channel enters as a scalar offset; padding rows and lanes point
+// past the buffer range and read zero); the column left of them -- the left
+// lane's last column -- is read by DPP inside the FMA (v_fmac_f32_dpp
+// wave_shr:1).  The wave walks the filter's storage one pattern segment after
+// another, each through a loop compiled with that centre+3 shape's taps fixed
+// (other masks take a loop that dispatches each tap); channel index and
+// weights are wave-uniform (scalar buffer loads).  The next kernel's rows
+// load while the current kernel's FMAs run.
 #include "conv_stream.h"
 
 namespace psc {
 namespace {
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kR2 = 4;                 // output rows per lane
 constexpr int kRows2 = 2 * kR2 + 1;    // input rows per lane and kernel
 
 struct Geo2 {
     int n, cin, H, W, cout, m, OH, OW;
+    int C;                             // output columns per lane
     int S, seg_len, RB, units, slots;
     int KS, FW, groups_x, nblocks;
     int64_t keep;
@@ -38,105 +41,117 @@ struct Geo2 {
     int8_t shape[kMaxPatterns];   // centre+3 shape index of each library pattern, -1 = other mask
 };
 
-// Raw words of a lane's column pair (2j, 2j+1) in each of its 2R+1 rows.
-template <int DT> struct Pairs {
-    uint32_t d[kRows2][DT == DT_F32 ? 2 : 1];
+// Raw words of a lane's 2C input columns in each of its 2R+1 rows.
+template <int DT, int C> struct Cols {
+    static constexpr int NW = DT == DT_F32 ? 2 * C : C;
+    uint32_t d[kRows2][NW];
+};
+
+// The 2C input columns of each row as fp32: v[c][r] is column 2C j + c.
+template <int C> struct ColVals {
+    float v[2 * C][kRows2];
 };
 
 struct Ctx2 {
     cs::Meta m;
     __amdgpu_buffer_rsrc_t xr;     // x, bounded to its size
     int chan_bytes;                // bytes of one input channel plane
-    uint32_t vo[kRows2];           // byte offset of column 2j of each row, channel 0 (2^31: padding)
+    uint32_t vo[kRows2];           // byte offset of the lane's first column of each row, channel 0 (2^31: padding)
 };
 
-template <int DT>
-__device__ __forceinline__ void load_pairs(const Ctx2& c, int ci, Pairs<DT>& p) {
+template <int DT, int C>
+__device__ __forceinline__ void load_cols(const Ctx2& c, int ci, Cols<DT, C>& p) {
     // wave-uniform: an SGPR operand.  A malformed channel index reads zeros
     // or other data of x, never memory outside it (range-checked loads).
     const int soff = __builtin_amdgcn_readfirstlane(ci * c.chan_bytes);
 #pragma unroll
     for (int r = 0; r < kRows2; ++r) {
-        if constexpr (DT == DT_F32) {
+        if constexpr (Cols<DT, C>::NW == 4) {
+            const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(c.xr, int(c.vo[r]), soff, 0);
+            p.d[r][0] = v.x, p.d[r][1] = v.y, p.d[r][2] = v.z, p.d[r][3] = v.w;
+        } else if constexpr (Cols<DT, C>::NW == 2) {
             const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(c.xr, int(c.vo[r]), soff, 0);
-            p.d[r][0] = v.x;
-            p.d[r][1] = v.y;
+            p.d[r][0] = v.x, p.d[r][1] = v.y;
         } else {
             p.d[r][0] = __builtin_amdgcn_raw_buffer_load_b32(c.xr, int(c.vo[r]), soff, 0);
         }
     }
 }
 
-// The even and odd columns as fp32; then an asm the compiler sees as writing
-// them (no VALU write of them can follow) and the two wait states a DPP read
-// needs after a VALU write of its source.
-template <int DT>
-__device__ __forceinline__ void unpack_pairs(const Pairs<DT>& p, float (&ev)[kRows2], float (&od)[kRows2]) {
+// The columns as fp32; then an asm the compiler sees as writing the last
+// column (the one the right neighbour reads by DPP: no VALU write of it can
+// follow) and the two wait states a DPP read needs after a VALU write of its
+// source.
+template <int DT, int C>
+__device__ __forceinline__ void unpack_cols(const Cols<DT, C>& p, ColVals<C>& x) {
 #pragma unroll
     for (int r = 0; r < kRows2; ++r) {
-        if constexpr (DT == DT_F32) {
-            ev[r] = __builtin_bit_cast(float, p.d[r][0]);
-            od[r] = __builtin_bit_cast(float, p.d[r][1]);
-        } else {
-            ev[r] = float(__builtin_bit_cast(_Float16, uint16_t(p.d[r][0])));
-            od[r] = float(__builtin_bit_cast(_Float16, uint16_t(p.d[r][0] >> 16)));
+#pragma unroll
+        for (int q = 0; q < 2 * C; ++q) {
+            if constexpr (DT == DT_F32)
+                x.v[q][r] = __builtin_bit_cast(float, p.d[r][q]);
+            else
+                x.v[q][r] = float(__builtin_bit_cast(_Float16, uint16_t(p.d[r][q / 2] >> (16 * (q & 1)))));
         }
     }
-    asm volatile("" : "+v"(od[0]), "+v"(od[1]), "+v"(od[2]), "+v"(od[3]), "+v"(od[4]));
-    asm volatile("" : "+v"(od[5]), "+v"(od[6]), "+v"(od[7]), "+v"(od[8]));
+    float (&l)[kRows2] = x.v[2 * C - 1];
+    asm volatile("" : "+v"(l[0]), "+v"(l[1]), "+v"(l[2]), "+v"(l[3]), "+v"(l[4]));
+    asm volatile("" : "+v"(l[5]), "+v"(l[6]), "+v"(l[7]), "+v"(l[8]));
     asm volatile("s_nop 1");
 }
 
-// The tap at kernel position Q = 3 ky + kx: acc[i] += w * x(row 2i + ky - 1,
-// column 2j + kx - 1) for the lane's R output rows.  Column 2j-1 is the odd
-// column of the lane to the left (DPP; a lane without one reads zero).
-template <int Q>
-__device__ __forceinline__ void tap2(float (&acc)[kR2], const float (&ev)[kRows2], const float (&od)[kRows2],
-                                     float w) {
+// The tap at kernel position Q = 3 ky + kx: for each output column c of the
+// lane and each output row i, acc[c][i] += w * x(row 2i + ky - 1, column
+// 2(Cj + c) + kx - 1).  Column 2Cj - 1 is the last column of the lane to the
+// left (DPP; a lane without one reads zero).
+template <int Q, int C>
+__device__ __forceinline__ void tap2(float (&acc)[C][kR2], const ColVals<C>& x, float w) {
     constexpr int ky = Q / 3, kx = Q % 3;
 #pragma unroll
-    for (int i = 0; i < kR2; ++i) {
-        if constexpr (kx == 0)
-            asm volatile("v_fmac_f32_dpp %0, %1, %2 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
-                         : "+v"(acc[i])
-                         : "v"(od[2 * i + ky]), "v"(w));
-        else if constexpr (kx == 1)
-            acc[i] = __builtin_fmaf(w, ev[2 * i + ky], acc[i]);
-        else
-            acc[i] = __builtin_fmaf(w, od[2 * i + ky], acc[i]);
+    for (int c = 0; c < C; ++c) {
+#pragma unroll
+        for (int i = 0; i < kR2; ++i) {
+            const int col = 2 * c + kx - 1;     // input column relative to the lane's first
+            if (col < 0)
+                asm volatile("v_fmac_f32_dpp %0, %1, %2 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+                             : "+v"(acc[c][i])
+                             : "v"(x.v[2 * C - 1][2 * i + ky]), "v"(w));
+            else
+                acc[c][i] = __builtin_fmaf(w, x.v[col][2 * i + ky], acc[c][i]);
+        }
     }
 }
 
-__device__ __forceinline__ void tap2_dyn(int q, float (&acc)[kR2], const float (&ev)[kRows2],
-                                         const float (&od)[kRows2], float w) {
+template <int C>
+__device__ __forceinline__ void tap2_dyn(int q, float (&acc)[C][kR2], const ColVals<C>& x, float w) {
     switch (q) {
-        case 0: tap2<0>(acc, ev, od, w); break;
-        case 1: tap2<1>(acc, ev, od, w); break;
-        case 2: tap2<2>(acc, ev, od, w); break;
-        case 3: tap2<3>(acc, ev, od, w); break;
-        case 4: tap2<4>(acc, ev, od, w); break;
-        case 5: tap2<5>(acc, ev, od, w); break;
-        case 6: tap2<6>(acc, ev, od, w); break;
-        case 7: tap2<7>(acc, ev, od, w); break;
-        default: tap2<8>(acc, ev, od, w); break;
+        case 0: tap2<0, C>(acc, x, w); break;
+        case 1: tap2<1, C>(acc, x, w); break;
+        case 2: tap2<2, C>(acc, x, w); break;
+        case 3: tap2<3, C>(acc, x, w); break;
+        case 4: tap2<4, C>(acc, x, w); break;
+        case 5: tap2<5, C>(acc, x, w); break;
+        case 6: tap2<6, C>(acc, x, w); break;
+        case 7: tap2<7, C>(acc, x, w); break;
+        default: tap2<8, C>(acc, x, w); break;
     }
 }
 
 // Kernels [k, e) of one pattern segment share (e > k), two per trip: the
 // rows of one load while the other's FMAs run; metadata is read two kernels
 // ahead; the single loop exit keeps the accumulators in place.
-template <int DT, class TapFn>
-__device__ __forceinline__ void run2(const Ctx2& c, int k, int e, float (&acc)[kR2], TapFn taps) {
+template <int DT, int C, class TapFn>
+__device__ __forceinline__ void run2(const Ctx2& c, int k, int e, float (&acc)[C][kR2], TapFn taps) {
     const int last = e - 1;
     float wA[4], wB[4];
     cs::meta_w<DT>(c.m, k, wA);
     int kk = k + 1 <= last ? k + 1 : last;
     int ciB = cs::meta_ci(c.m, kk);
     cs::meta_w<DT>(c.m, kk, wB);
-    Pairs<DT> pA, pB;
-    load_pairs<DT>(c, cs::meta_ci(c.m, k), pA);
+    Cols<DT, C> pA, pB;
+    load_cols<DT, C>(c, cs::meta_ci(c.m, k), pA);
     while (k + 1 < e) {
-        load_pairs<DT>(c, ciB, pB);                              // rows of kernel k+1
+        load_cols<DT, C>(c, ciB, pB);                            // rows of kernel k+1
         kk = k + 2 <= last ? k + 2 : last;
         const int ciA2 = cs::meta_ci(c.m, kk);
         float wA2[4];
@@ -146,15 +161,15 @@ __device__ __forceinline__ void run2(const Ctx2& c, int k, int e, float (&acc)[k
         float wB2[4];
         cs::meta_w<DT>(c.m, kk, wB2);
         {
-            float ev[kRows2], od[kRows2];
-            unpack_pairs<DT>(pA, ev, od);
-            taps(acc, ev, od, wA);                               // kernel k
+            ColVals<C> x;
+            unpack_cols<DT, C>(pA, x);
+            taps(acc, x, wA);                                    // kernel k
         }
-        load_pairs<DT>(c, ciA2, pA);                             // rows of kernel k+2
+        load_cols<DT, C>(c, ciA2, pA);                           // rows of kernel k+2
         {
-            float ev[kRows2], od[kRows2];
-            unpack_pairs<DT>(pB, ev, od);
-            taps(acc, ev, od, wB);                               // kernel k+1
+            ColVals<C> x;
+            unpack_cols<DT, C>(pB, x);
+            taps(acc, x, wB);                                    // kernel k+1
         }
         k += 2;
         wA[0] = wA2[0], wA[1] = wA2[1], wA[2] = wA2[2], wA[3] = wA2[3];
@@ -162,33 +177,33 @@ __device__ __forceinline__ void run2(const Ctx2& c, int k, int e, float (&acc)[k
         ciB = ciB2;
     }
     if (k < e) {
-        float ev[kRows2], od[kRows2];
-        unpack_pairs<DT>(pA, ev, od);
-        taps(acc, ev, od, wA);
+        ColVals<C> x;
+        unpack_cols<DT, C>(pA, x);
+        taps(acc, x, wA);
     }
 }
 
-template <int DT, int MASK>
-__device__ __forceinline__ void run_shape2(const Ctx2& c, int k, int e, float (&acc)[kR2]) {
+template <int DT, int C, int MASK>
+__device__ __forceinline__ void run_shape2(const Ctx2& c, int k, int e, float (&acc)[C][kR2]) {
     constexpr int Q0 = NthBit<MASK, 0>::value(), Q1 = NthBit<MASK, 1>::value();
     constexpr int Q2 = NthBit<MASK, 2>::value(), Q3 = NthBit<MASK, 3>::value();
-    run2<DT>(c, k, e, acc, [](float (&a)[kR2], const float (&ev)[kRows2], const float (&od)[kRows2],
-                              const float (&w)[4]) {
-        // the own-column taps first: they put FMAs between the unpack and the DPP reads
-        if constexpr (Q0 % 3 != 0) tap2<Q0>(a, ev, od, w[0]);
-        if constexpr (Q1 % 3 != 0) tap2<Q1>(a, ev, od, w[1]);
-        if constexpr (Q2 % 3 != 0) tap2<Q2>(a, ev, od, w[2]);
-        if constexpr (Q3 % 3 != 0) tap2<Q3>(a, ev, od, w[3]);
-        if constexpr (Q0 % 3 == 0) tap2<Q0>(a, ev, od, w[0]);
-        if constexpr (Q1 % 3 == 0) tap2<Q1>(a, ev, od, w[1]);
-        if constexpr (Q2 % 3 == 0) tap2<Q2>(a, ev, od, w[2]);
-        if constexpr (Q3 % 3 == 0) tap2<Q3>(a, ev, od, w[3]);
+    run2<DT, C>(c, k, e, acc, [](float (&a)[C][kR2], const ColVals<C>& x, const float (&w)[4]) {
+        // the taps without a DPP read first: they put FMAs between the unpack
+        // and the DPP reads
+        if constexpr (Q0 % 3 != 0) tap2<Q0, C>(a, x, w[0]);
+        if constexpr (Q1 % 3 != 0) tap2<Q1, C>(a, x, w[1]);
+        if constexpr (Q2 % 3 != 0) tap2<Q2, C>(a, x, w[2]);
+        if constexpr (Q3 % 3 != 0) tap2<Q3, C>(a, x, w[3]);
+        if constexpr (Q0 % 3 == 0) tap2<Q0, C>(a, x, w[0]);
+        if constexpr (Q1 % 3 == 0) tap2<Q1, C>(a, x, w[1]);
+        if constexpr (Q2 % 3 == 0) tap2<Q2, C>(a, x, w[2]);
+        if constexpr (Q3 % 3 == 0) tap2<Q3, C>(a, x, w[3]);
     });
 }
 
 // Any 4-of-9 mask: each tap is chosen per kernel by a uniform branch.
-template <int DT>
-__device__ __forceinline__ void run_generic2(unsigned mask, const Ctx2& c, int k, int e, float (&acc)[kR2]) {
+template <int DT, int C>
+__device__ __forceinline__ void run_generic2(unsigned mask, const Ctx2& c, int k, int e, float (&acc)[C][kR2]) {
     int q0 = 4, q1 = 4, q2 = 4, q3 = 4, seen = 0;
 #pragma unroll
     for (int q = 0; q < 9; ++q) {
@@ -200,23 +215,22 @@ __device__ __forceinline__ void run_generic2(unsigned mask, const Ctx2& c, int k
             ++seen;
         }
     }
-    run2<DT>(c, k, e, acc, [=](float (&a)[kR2], const float (&ev)[kRows2], const float (&od)[kRows2],
-                               const float (&w)[4]) {
-        tap2_dyn(q0, a, ev, od, w[0]);
-        tap2_dyn(q1, a, ev, od, w[1]);
-        tap2_dyn(q2, a, ev, od, w[2]);
-        tap2_dyn(q3, a, ev, od, w[3]);
+    run2<DT, C>(c, k, e, acc, [=](float (&a)[C][kR2], const ColVals<C>& x, const float (&w)[4]) {
+        tap2_dyn<C>(q0, a, x, w[0]);
+        tap2_dyn<C>(q1, a, x, w[1]);
+        tap2_dyn<C>(q2, a, x, w[2]);
+        tap2_dyn<C>(q3, a, x, w[3]);
     });
 }
 
 #define PSC_S2_CASE(I) \
-    case I: run_shape2<DT, kCentre3.code[I]>(c, k, e, acc); return;
+    case I: run_shape2<DT, C, kCentre3.code[I]>(c, k, e, acc); return;
 #define PSC_S2_CASE8(I)                                                                             \
     PSC_S2_CASE(I) PSC_S2_CASE(I + 1) PSC_S2_CASE(I + 2) PSC_S2_CASE(I + 3) PSC_S2_CASE(I + 4)      \
     PSC_S2_CASE(I + 5) PSC_S2_CASE(I + 6) PSC_S2_CASE(I + 7)
-template <int DT>
+template <int DT, int C>
 __device__ __forceinline__ void run_pattern2(int shape, unsigned mask, const Ctx2& c, int k, int e,
-                                             float (&acc)[kR2]) {
+                                             float (&acc)[C][kR2]) {
     switch (shape) {
         PSC_S2_CASE8(0)
         PSC_S2_CASE8(8)
@@ -225,13 +239,13 @@ __device__ __forceinline__ void run_pattern2(int shape, unsigned mask, const Ctx
         PSC_S2_CASE8(32)
         PSC_S2_CASE8(40)
         PSC_S2_CASE8(48)
-        default: run_generic2<DT>(mask, c, k, e, acc); return;
+        default: run_generic2<DT, C>(mask, c, k, e, acc); return;
     }
 }
 #undef PSC_S2_CASE8
 #undef PSC_S2_CASE
 
-template <int DT>
+template <int DT, int C>
 __global__ __launch_bounds__(256) void k_conv_stride2(const typename Elt<DT>::T* __restrict__ x,
                                                       const int32_t* __restrict__ perm,
                                                       const int32_t* __restrict__ seg_ptr,
@@ -240,7 +254,7 @@ __global__ __launch_bounds__(256) void k_conv_stride2(const typename Elt<DT>::T*
                                                       const typename Elt<DT>::T* __restrict__ bias,
                                                       typename Elt<DT>::T* __restrict__ y, Geo2 g) {
     using E = Elt<DT>;
-    __shared__ float red[4][kR2][64];
+    __shared__ float red[4][C * kR2][64];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
     const int gf = wave / g.KS, sp = wave - gf * g.KS;          // filter slot, share
@@ -257,20 +271,23 @@ __global__ __launch_bounds__(256) void k_conv_stride2(const typename Elt<DT>::T*
     const int i = fg * g.FW + gf;
     const bool has_filter = i < g.cout;
 
+    // lane j of a band owns output columns Cj .. Cj + C - 1
     const int seg = lane / g.seg_len, j = lane - seg * g.seg_len;
     const int u = sg * g.S + seg;
     bool lane_ok = false;
     int nimg = 0, i0 = 0;
-    if (seg < g.S && u < g.units && j < g.OW) {
+    if (seg < g.S && u < g.units && C * j < g.OW) {
         lane_ok = true;
         nimg = u / g.RB;
         i0 = (u - nimg * g.RB) * kR2;
     }
     const int plane = g.H * g.W;
     constexpr int ESZ = int(sizeof(typename E::T));
-    float acc[kR2];
+    float acc[C][kR2];
 #pragma unroll
-    for (int r = 0; r < kR2; ++r) acc[r] = 0.f;
+    for (int c = 0; c < C; ++c)
+#pragma unroll
+        for (int r = 0; r < kR2; ++r) acc[c][r] = 0.f;
 
     if (has_filter) {
         const int* segp = seg_ptr + int64_t(i) * (g.m + 1);
@@ -281,20 +298,20 @@ __global__ __launch_bounds__(256) void k_conv_stride2(const typename Elt<DT>::T*
         c.m = cs::Meta{cs::scalar_rsrc(cin_idx, int(g.keep) * 4), cs::scalar_rsrc(vals, int(g.keep) * 4 * ESZ)};
         c.xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<typename E::T*>(x), int16_t(0), g.x_bytes, 0x00020000);
         c.chan_bytes = __builtin_amdgcn_readfirstlane(plane * ESZ);
-        // byte offset of input column 2j of each of the lane's rows in
+        // byte offset of input column 2Cj of each of the lane's rows in
         // channel 0 of its image; past the buffer range for padding
 #pragma unroll
         for (int r = 0; r < kRows2; ++r) {
             const int row = 2 * i0 - 1 + r;
             c.vo[r] = (lane_ok && row >= 0 && row < g.H)
-                          ? uint32_t(nimg * g.cin * plane + row * g.W + 2 * j) * uint32_t(ESZ)
+                          ? uint32_t(nimg * g.cin * plane + row * g.W + 2 * C * j) * uint32_t(ESZ)
                           : 0x80000000u;
         }
         for (int p = 0; p < g.m; ++p) {
             int k0 = segp[p], k1 = segp[p + 1];
             k0 = k0 < s0 ? s0 : k0;
             k1 = k1 > s1 ? s1 : k1;                               // malformed pointers stay in the share
-            if (k0 < k1) run_pattern2<DT>(g.shape[p], g.mask[p], c, k0, k1, acc);
+            if (k0 < k1) run_pattern2<DT, C>(g.shape[p], g.mask[p], c, k0, k1, acc);
         }
     }
     // add the KS partial sums of each filter in share order
@@ -302,16 +319,20 @@ __global__ __launch_bounds__(256) void k_conv_stride2(const typename Elt<DT>::T*
         for (int slot = 0; slot < g.FW; ++slot) {
             if (slot == gf) {
 #pragma unroll
-                for (int r = 0; r < kR2; ++r) red[sp][r][lane] = acc[r];
+                for (int c = 0; c < C; ++c)
+#pragma unroll
+                    for (int r = 0; r < kR2; ++r) red[sp][c * kR2 + r][lane] = acc[c][r];
             }
             __syncthreads();
             if (slot == gf) {
 #pragma unroll
-                for (int r = 0; r < kR2; ++r) {
-                    float v = 0.f;
-                    for (int t = 0; t < g.KS; ++t) v += red[t][r][lane];
-                    acc[r] = v;
-                }
+                for (int c = 0; c < C; ++c)
+#pragma unroll
+                    for (int r = 0; r < kR2; ++r) {
+                        float v = 0.f;
+                        for (int t = 0; t < g.KS; ++t) v += red[t][c * kR2 + r][lane];
+                        acc[c][r] = v;
+                    }
             }
             __syncthreads();
         }
@@ -319,14 +340,17 @@ __global__ __launch_bounds__(256) void k_conv_stride2(const typename Elt<DT>::T*
     if (!has_filter || !lane_ok) return;
     const int f = perm[i];
     const float bv = bias ? E::load(bias, f) : 0.f;
-    typename E::T* yp = y + (int64_t(nimg) * g.cout + f) * (g.OH * g.OW) + j;
+    typename E::T* yp = y + (int64_t(nimg) * g.cout + f) * (g.OH * g.OW) + C * j;
 #pragma unroll
     for (int r = 0; r < kR2; ++r) {
         const int row = i0 + r;
         if (row < g.OH && (r % g.KS) == sp) {
-            float v = acc[r] + bv;
-            if (g.relu) v = v > 0.f ? v : 0.f;
-            yp[row * g.OW] = E::from_f(v);
+#pragma unroll
+            for (int c = 0; c < C; ++c) {
+                float v = acc[c][r] + bv;
+                if (g.relu) v = v > 0.f ? v : 0.f;
+                yp[row * g.OW + c] = E::from_f(v);
+            }
         }
     }
 }
@@ -363,8 +387,12 @@ static bool plan_conv_stride2(const PatTable& tab, const ConvArgs& a, ConvForm* 
             for (int t = 0; t < 56; ++t)
                 if (kCentre3.code[t] == tab.mask[p]) g.shape[p] = int8_t(t);
     }
-    g.seg_len = OW + 1;
-    g.S = 65 / (OW + 1);
+    // two output columns per lane when the lane's 4 input columns start on
+    // a 16-byte (fp32) / 8-byte (fp16) boundary: W a multiple of 4
+    g.C = a.w % 4 == 0 ? 2 : 1;
+    const int lanes = (OW + g.C - 1) / g.C;
+    g.seg_len = lanes + 1;
+    g.S = 65 / (lanes + 1);
     g.RB = (OH + kR2 - 1) / kR2;
     g.units = a.n * g.RB;
     g.slots = (g.units + g.S - 1) / g.S;
@@ -374,7 +402,7 @@ static bool plan_conv_stride2(const PatTable& tab, const ConvArgs& a, ConvForm* 
     if (g.FW > a.cout) g.FW = a.cout;
     g.groups_x = (a.cout + g.FW - 1) / g.FW;
     g.nblocks = g.groups_x * g.slots;
-    if (form) *form = ConvForm{3, 0, kR2, 1, g.S, 1, g.KS, g.FW, g.nblocks, g.FW * g.KS * 64};
+    if (form) *form = ConvForm{3, 0, kR2, g.C, g.S, 1, g.KS, g.FW, g.nblocks, g.FW * g.KS * 64};
     if (out) *out = g;
     return true;
 }
@@ -387,14 +415,18 @@ hipError_t launch_conv_stride2(const PatTable& tab, const PackedView& pk, const 
     Geo2 g;
     if (!plan_conv_stride2(tab, a, nullptr, &g)) return hipErrorNotSupported;
     const dim3 grid(unsigned(g.nblocks)), block(unsigned(g.FW * g.KS * 64));
-    if (a.dtype == DT_F16)
-        hipLaunchKernelGGL(k_conv_stride2<DT_F16>, grid, block, 0, stream, static_cast<const uint16_t*>(a.x),
-                           pk.filter_perm, pk.seg_ptr, pk.cin_idx, static_cast<const uint16_t*>(pk.values),
-                           static_cast<const uint16_t*>(a.bias), static_cast<uint16_t*>(a.y), g);
-    else
-        hipLaunchKernelGGL(k_conv_stride2<DT_F32>, grid, block, 0, stream, static_cast<const float*>(a.x),
-                           pk.filter_perm, pk.seg_ptr, pk.cin_idx, static_cast<const float*>(pk.values),
-                           static_cast<const float*>(a.bias), static_cast<float*>(a.y), g);
+#define PSC_S2_LAUNCH(DT, T, C)                                                                              \
+    hipLaunchKernelGGL((k_conv_stride2<DT, C>), grid, block, 0, stream, static_cast<const T*>(a.x),            \
+                       pk.filter_perm, pk.seg_ptr, pk.cin_idx, static_cast<const T*>(pk.values),             \
+                       static_cast<const T*>(a.bias), static_cast<T*>(a.y), g)
+    if (a.dtype == DT_F16) {
+        if (g.C == 2) PSC_S2_LAUNCH(DT_F16, uint16_t, 2);
+        else PSC_S2_LAUNCH(DT_F16, uint16_t, 1);
+    } else {
+        if (g.C == 2) PSC_S2_LAUNCH(DT_F32, float, 2);
+        else PSC_S2_LAUNCH(DT_F32, float, 1);
+    }
+#undef PSC_S2_LAUNCH
     return hipGetLastError();
 }
 

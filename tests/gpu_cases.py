@@ -178,12 +178,17 @@ def form_cases():
                                 found[key] = (work, (key, n, cin, cout, hw, hw, dt, pool, 1, 0))
     out = [v[1] for v in found.values()]
     for dt in (B.PSC_F32, B.PSC_F16):
-        # the tuned stride-2 kernel: whole filters and split filters, ragged
-        # output bands, several bands per wave
-        for n, cin, cout, h, w in ((2, 9, 7, 14, 12), (1, 64, 8, 16, 16), (3, 5, 6, 13, 6), (1, 24, 5, 9, 126)):
+        # the tuned stride-2 kernel, one output column per lane (w = 2 mod 4)
+        # and two (w a multiple of 4): whole filters and split filters,
+        # ragged output bands, several bands per wave, a band of one lane,
+        # the widest rows
+        for n, cin, cout, h, w in ((2, 9, 7, 14, 12), (1, 64, 8, 16, 16), (3, 5, 6, 13, 6), (1, 24, 5, 9, 126),
+                                   (5, 7, 5, 9, 4), (1, 32, 6, 11, 124), (2, 48, 4, 28, 28), (1, 17, 9, 21, 56),
+                                   (3, 40, 5, 10, 14)):
             L = B.Layer(cout, cin, list(FORM_MASKS), cin * cout // 2, dt)
             cfg = B.conv3x3_config(L, dt, n, h, w, False, 2, 0)
-            out.append((("stride2", cfg["kernel"], cfg["shares"] > 1), n, cin, cout, h, w, dt, False, 2, 0))
+            out.append((("stride2", cfg["kernel"], cfg["cols_per_lane"], w, cfg["shares"] > 1),
+                        n, cin, cout, h, w, dt, False, 2, 0))
         # the one-row-per-lane kernel (algo 2) at every compiled width: ragged
         # image groups, a partial wave, split filters, rows unequal to columns,
         # and (fp16, width 7, odd cin and n) the last row of x read through a

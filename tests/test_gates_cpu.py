@@ -81,7 +81,9 @@ def test_form_search_reaches_every_form():
     # the automatic choice takes the rows kernel for whole-wave batches on small planes
     assert any(isinstance(c[0][0], int) and c[0][0] == 4 for c in cases)
     s2 = [c[0] for c in cases if c[0][0] == "stride2"]
-    assert all(k[1] == 3 for k in s2) and any(k[2] for k in s2) and any(not k[2] for k in s2)
+    assert all(k[1] == 3 for k in s2) and any(k[4] for k in s2) and any(not k[4] for k in s2)
+    assert {k[2] for k in s2} == {1, 2} and all(k[2] == (2 if k[3] % 4 == 0 else 1) for k in s2)
+    assert any(k[2] == 2 and k[4] for k in s2) and any(k[2] == 2 and not k[4] for k in s2)
 
 
 def test_config_query_validates():
@@ -94,6 +96,8 @@ def test_config_query_validates():
         with pytest.raises(B.PscError):
             B.conv3x3_config(L, *args)
     assert B.conv3x3_config(L, B.PSC_F32, 2, 16, 16, False, 2, 0)["kernel"] == 3      # tuned stride 2
+    assert B.conv3x3_config(L, B.PSC_F32, 2, 16, 16, False, 2, 0)["cols_per_lane"] == 2
+    assert B.conv3x3_config(L, B.PSC_F32, 2, 16, 14, False, 2, 0)["cols_per_lane"] == 1
     assert B.conv3x3_config(L, B.PSC_F32, 2, 16, 15, False, 2, 0)["kernel"] == 2      # odd width
     assert B.conv3x3_config(L, B.PSC_F32, 2, 16, 16, False, 2, 1)["kernel"] == 2      # algo 1
     assert B.conv3x3_config(L, B.PSC_F32, 1, 8, 8, False, 1, 2)["kernel"] == 4        # algo 2: one row per lane
