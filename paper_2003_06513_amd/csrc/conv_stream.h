@@ -775,9 +775,10 @@ __device__ __forceinline__ void run_pattern4(int shape, unsigned mask, const Run
 #undef PSC_SHAPE_CASE
 
 // Wide form of the kernel (fp32): same blocks, shares, reduction and
-// epilogue as the one-column form, 4 columns per lane.
+// epilogue as the one-column form, 4 columns per lane.  With 4 rows per lane
+// the compiler is held to 128 VGPRs (4 waves per SIMD).
 template <int R>
-__global__ __launch_bounds__(512) void k_conv_wide(const float* __restrict__ x, const int32_t* __restrict__ perm,
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(R <= 2 ? 6 : 4))) void k_conv_wide(const float* __restrict__ x, const int32_t* __restrict__ perm,
                                                    const int32_t* __restrict__ seg_ptr,
                                                    const int32_t* __restrict__ cin_idx,
                                                    const float* __restrict__ vals, const float* __restrict__ bias,

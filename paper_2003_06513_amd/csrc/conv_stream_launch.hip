@@ -20,7 +20,7 @@ PSC_EXTERN_R(DT_F16, 4)
 PSC_EXTERN_R(DT_F16, 7)
 PSC_EXTERN_R(DT_F16, 8)
 #undef PSC_EXTERN_R
-extern template hipError_t cs::launch_wide<2>(const PackedView&, const ConvArgs&, const Geo&, hipStream_t);
+extern template hipError_t cs::launch_wide<4>(const PackedView&, const ConvArgs&, const Geo&, hipStream_t);
 
 // Grids of at least this many waves are throughput-bound (16 waves per SIMD).
 constexpr int64_t kManyWaves = 16384;
@@ -76,14 +76,15 @@ bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
         g.S = 64 / g.seg_len;
         g.Wt = a.w;
         g.CT = 1;
-        // two rows per lane: 4(R+2) row values a kernel, twice for the
-        // prefetch, keep the wave near 80 VGPRs (6 waves per SIMD)
-        constexpr int R = 2;
+        // four rows per lane: 16 outputs for 6 row loads a kernel, 128
+        // VGPRs (4 waves per SIMD); shares only below about one wave per
+        // SIMD (at 112-224 columns one share measured fastest)
+        constexpr int R = 4;
         g.RB = (a.h + R - 1) / R;
         g.U = a.n * g.RB;
         const int sgroups = (g.U + g.S - 1) / g.S;
         g.KS = 1;
-        while (g.KS < kMaxSplit && int64_t(sgroups) * a.cout * g.KS < 4096 && a.cin >= 16 * g.KS) g.KS *= 2;
+        while (g.KS < kMaxSplit && int64_t(sgroups) * a.cout * g.KS < 1024 && a.cin >= 16 * g.KS) g.KS *= 2;
         g.FW = g.KS >= 4 ? 1 : 4 / g.KS;
         if (g.FW > a.cout) g.FW = a.cout;
         g.groups_x = (a.cout + g.FW - 1) / g.FW;
@@ -205,7 +206,7 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
                               hipStream_t stream) {
     Geo g;
     if (!plan_conv_stream(tab, a, g)) return hipErrorNotSupported;
-    if (g.form == 1) return launch_wide<2>(pk, a, g, stream);
+    if (g.form == 1) return launch_wide<4>(pk, a, g, stream);
     switch (g.R) {
         case 8: return a.dtype == DT_F16 ? launch_r<DT_F16, 8>(pk, a, g, stream)
                                          : launch_r<DT_F32, 8>(pk, a, g, stream);
