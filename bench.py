@@ -6,8 +6,11 @@ fused ReLU and the four 2x2 max-pools (fused into the conv launch they follow
 where that is faster, as timed at start-up) on a 1x3x224x224 synthetic
 image; for the other workloads every listed layer on its own resident input.
 Weights are pruned and packed on the GPU (projection, selection, packing)
-before timing.  The step's launches are captured once in a HIP graph and the
-timed steps are its replays (--no-graph times eager launches).
+before timing.  The timed steps are eager launches on one stream; the same
+run also captures the step once in a HIP graph, checks a replay against the
+eager output and times the replays (--launch graph reports those instead;
+on this path graph replay measures 2-5 % slower than eager launches, whose
+host-side submission stays ahead of the GPU).
 
 The same run measures the other workloads the metric is quoted on (by
 default the 16 ResNet-50 3x3 layers in fp16 at batch 1 and 32).  For every
@@ -42,7 +45,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "nonzero-MAC GFLOP/s + ms/layer, pattern-sparse 3x3 conv fwd, batch 1 and 32"
 # MI355X published fp32 vector peak (256 CUs x 2.4 GHz).  The kernels issue
-# non-packed v_fmac_f32 (packed fp32 is disabled in this build); the measured
+# non-packed v_fmac_f32 (the library is compiled with packed fp32 disabled); the measured
 # ceilings in the bench line give the rate that instruction reaches here.
 PEAK_VALU_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
@@ -66,8 +69,9 @@ def parse():
     ap.add_argument("--no-ceilings", dest="ceilings", action="store_false",
                     help="skip the measured ceilings (FMA probe, HBM copy, launch latency)")
     ap.add_argument("--list", action="store_true")
-    ap.add_argument("--no-graph", action="store_true",
-                    help="time eager launches instead of replays of a captured HIP graph of the step")
+    ap.add_argument("--launch", choices=("eager", "graph"), default="eager",
+                    help="the timed steps: eager launches, or replays of a captured HIP graph of the step "
+                         "(both are timed and reported)")
     ap.add_argument("--fuse-pool", default="auto",
                     help="pooled layers whose pool runs inside the conv launch: auto (the faster form, "
                          "timed at start-up), all, none, or layer names separated by commas")
@@ -197,9 +201,10 @@ def time_launches(fn, warm=10, samples=30, reps=5):
     return float(np.median(t)), float(np.percentile(t, 10)), float(np.percentile(t, 90)), float(t.mean())
 
 
-def time_step(net, steps, warmup, graph):
-    """ms per step: ``steps`` timed steps (eager, or replays of a HIP graph of
-    the step whose output is checked against the eager step's)."""
+def time_step(net, steps, warmup):
+    """ms per step, eager and as replays of a HIP graph of the step (whose
+    output is checked against the eager step's): ``warmup`` untimed steps,
+    then ``steps`` timed ones between two device synchronisations."""
     import torch
     for _ in range(warmup):
         net.step()
@@ -209,8 +214,6 @@ def time_step(net, steps, warmup, graph):
         net.step()
     torch.cuda.synchronize()
     ms_eager = (time.perf_counter() - t0) * 1e3 / steps
-    if not graph:
-        return ms_eager, ms_eager
     eager_out = net.output().clone()
     g = torch.cuda.CUDAGraph()
     side = torch.cuda.Stream()
@@ -230,7 +233,7 @@ def time_step(net, steps, warmup, graph):
     for _ in range(steps):
         g.replay()
     torch.cuda.synchronize()
-    return (time.perf_counter() - t0) * 1e3 / steps, ms_eager
+    return ms_eager, (time.perf_counter() - t0) * 1e3 / steps
 
 
 def layer_table(net, miopen):
@@ -440,7 +443,8 @@ def measure(wl, args, headline):
     """Everything reported for one workload."""
     net = Net(wl, args.algo)
     net.choose_fusion(args.fuse_pool)
-    ms_step, ms_eager = time_step(net, args.steps, args.warmup, not args.no_graph)
+    ms_eager, ms_graph = time_step(net, args.steps, args.warmup)
+    ms_step = ms_graph if args.launch == "graph" else ms_eager
     rows = layer_table(net, not args.no_miopen)
     nz = [net.nz_flops(li) for li in range(len(net.layers))]
     conv_ms = sum(r["mean_ms"] for r in rows)
@@ -448,7 +452,8 @@ def measure(wl, args, headline):
     res = {
         "batch": wl.batch, "dtype": wl.dtype, "m": wl.m, "layers": len(wl.layers),
         "ms_per_step": round(ms_step, 4), "ms_per_step_eager": round(ms_eager, 4),
-        "step_launch": "eager" if args.no_graph else "hip graph replay",
+        "ms_per_step_graph": round(ms_graph, 4),
+        "step_launch": "hip graph replay" if args.launch == "graph" else "eager, one stream",
         "nz_gflops": round(sum(nz) / (ms_step * 1e-3) / 1e9, 2),
         "conv_ms_per_step": round(conv_ms, 4),
         "roofline_frac": round(achieved / PEAK_VALU_TFLOPS, 4),
@@ -478,7 +483,7 @@ def measure(wl, args, headline):
 
 def measure_ceilings():
     """Measured ceilings beside the published ones: the fp32 FMA rate of the
-    vector ALUs as this build issues it (psc_probe_fma: v_fmac_f32, packed
+    vector ALUs as the library issues it (psc_probe_fma: v_fmac_f32, packed
     fp32 disabled), the HBM bandwidth of a 1 GiB device copy (read + write
     bytes), and the launch latency of a tiny library kernel, eager and as a
     HIP graph replay."""
@@ -562,7 +567,7 @@ def main():
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the pattern-sparse layer shards by batch with no "
-              "exchange, so multi-GPU runs are not part of this build", file=sys.stderr)
+              "exchange, and multi-GPU runs are not implemented", file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2003_06513_amd import binding as B
@@ -610,6 +615,7 @@ def main():
                    "stack": "conv+relu, 2x2 max-pool after conv2/4/7/10" if head.chained else "independent layers",
                    "pool_fused_into": hr["pool_fused_into"]},
         "step_launch": hr["step_launch"], "ms_per_step_eager": hr["ms_per_step_eager"],
+        "ms_per_step_graph": hr["ms_per_step_graph"],
         "ms_per_layer": hr["ms_per_layer"],
         "roofline": roofs[head.name],
     }

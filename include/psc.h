@@ -46,7 +46,7 @@ extern "C" {
 typedef enum {
     PSC_OK = 0,
     PSC_ERR_ARG = 1,          /* a null pointer, bad size, bad mask, ... */
-    PSC_ERR_UNSUPPORTED = 2,  /* a valid request this build does not run */
+    PSC_ERR_UNSUPPORTED = 2,  /* a valid request the library does not run */
     PSC_ERR_WORKSPACE = 3,    /* workspace pointer missing or too small */
     PSC_ERR_DEVICE = 4,       /* a HIP call or kernel launch failed */
     PSC_ERR_INTERNAL = 5
@@ -343,8 +343,8 @@ psc_status psc_maxpool2x2(int32_t dtype, const void *d_x, int32_t n, int32_t c,
                           int32_t h, int32_t w, void *d_y, void *stream);
 
 /* Measurement probe, not part of the method: blocks x 256 lanes each run 8
- * independent chains of iters fp32 FMAs (v_fmac_f32; packed fp32 is disabled
- * in this build) and store one sum to d_out [blocks*256] (fp32, device).
+ * independent chains of iters fp32 FMAs (v_fmac_f32; the library is compiled
+ * with packed fp32 disabled) and store one sum to d_out [blocks*256] (fp32, device).
  * Timing it gives the vector-ALU FMA rate the conv kernels can reach:
  * 2 * 8 * iters * blocks * 256 flops.  blocks in 1..2^20, iters >= 0. */
 psc_status psc_probe_fma(int32_t blocks, int32_t iters, float *d_out, void *stream);

@@ -55,6 +55,11 @@ namespace psc {
 namespace cs {
 
 constexpr int kMaxSplit = 8;
+// Waves (one share per filter) from which a grid of 28..63-column images
+// (and fp16 images of any width) takes the wide form: 6 per SIMD.  Measured:
+// 3584 waves 7 % slower than the one-column form, 7168 waves 17 % faster,
+// batch-1 grids of up to 1024 waves 0-15 % slower.
+constexpr int64_t kWideMinWaves = 6144;
 
 typedef psc_i32x4 int32x4;
 
@@ -573,14 +578,14 @@ __device__ __forceinline__ int run_pattern_lds(int shape, unsigned mask, const L
 #undef PSC_SHAPE_CASE
 
 // ------------------------------------------------------------------ wide rows
-// Images 64..252 columns wide whose rows start on 64-byte boundaries (fp32,
-// width a multiple of 16): a lane owns 4 adjacent output columns and R rows
-// of a full-row band, and each input row arrives as one aligned 16-byte load
-// per lane, which the vector memory path serves at full rate.  The
-// neighbour columns left of the lane's first and right of its last column
-// come from the adjacent lanes through DPP; the other taps read the lane's
-// own values.  Segments are padded to a multiple of 4 lanes so that every
-// 4-lane group of a load stays in one 64-byte block.
+// Images 28..252 columns wide, width a multiple of 4: a lane owns 4 adjacent
+// output columns and R rows of a full-row band, and each input row arrives as
+// one aligned load per lane (16 bytes fp32, 8 bytes fp16), so one load
+// instruction feeds 4 columns' taps.  The neighbour columns left of the
+// lane's first and right of its last column come from the adjacent lanes
+// through DPP; the other taps read the lane's own values.  Segments are
+// padded to a multiple of 4 lanes (with rows on 64-byte boundaries, every
+// 4-lane group of a load stays in one 64-byte block).
 
 // One output row of a tap: a[c] += w * x[c + DS - 1] over the lane's 4
 // columns, with x[-1] / x[4] taken from the lane to the left / right.
@@ -677,7 +682,7 @@ __device__ __forceinline__ void kernel_taps4_dyn(const int (&q)[4], float (&a)[4
     }
 }
 
-// The R+2 input rows (4 columns each) of channel ci for this lane.
+// The R+2 input rows (4 columns each) of channel ci for this lane (fp32).
 template <int R>
 __device__ __forceinline__ void load_rows4(const RunCtx& c, const uint32_t (&vo)[R + 2], int ci,
                                            float (&x)[R + 2][4]) {
@@ -689,51 +694,121 @@ __device__ __forceinline__ void load_rows4(const RunCtx& c, const uint32_t (&vo)
     }
 }
 
+// fp16: the R+2 rows as raw words (4 halves in 2 words per row), widened
+// just before their taps.
+template <int R> struct Half4Rows {
+    uint32_t d[R + 2][2];
+};
+
+template <int R>
+__device__ __forceinline__ void load_rows4_f16(const RunCtx& c, const uint32_t (&vo)[R + 2], int ci,
+                                               Half4Rows<R>& p) {
+    const int soff = __builtin_amdgcn_readfirstlane(ci * c.chan_bytes);
+#pragma unroll
+    for (int r = 0; r < R + 2; ++r) {
+        const psc_i32x2 v = __builtin_bit_cast(psc_i32x2, __builtin_amdgcn_raw_buffer_load_b64(c.xr, vo[r], soff, 0));
+        p.d[r][0] = uint32_t(v.x), p.d[r][1] = uint32_t(v.y);
+    }
+}
+
+// Widen to fp32; then an asm the compiler sees as writing the first and last
+// column of every row (the ones the neighbours read by DPP: no VALU write of
+// them can follow) and the two wait states a DPP read needs after a VALU
+// write of its source.
+template <int R>
+__device__ __forceinline__ void unpack_rows4(const Half4Rows<R>& p, float (&x)[R + 2][4]) {
+#pragma unroll
+    for (int r = 0; r < R + 2; ++r) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            x[r][q] = float(__builtin_bit_cast(_Float16, uint16_t(p.d[r][q / 2] >> (16 * (q & 1)))));
+    }
+#pragma unroll
+    for (int r = 0; r < R + 2; ++r) asm volatile("" : "+v"(x[r][0]), "+v"(x[r][3]));
+    asm volatile("s_nop 1");
+}
+
 // Kernels [k, e) of one pattern segment share; two per trip as in the
 // one-column form.
-template <int R, class TapFn>
+template <int DT, int R, class TapFn>
 __device__ __forceinline__ void run_kernels4(const RunCtx& c, const uint32_t (&vo)[R + 2], int k, int e,
                                              float (&acc)[4 * R], TapFn taps) {
     const int last = e - 1;
     float wA[4], wB[4];
-    meta_w<DT_F32>(c.m, k, wA);
+    meta_w<DT>(c.m, k, wA);
     int kk = k + 1 <= last ? k + 1 : last;
     int ciB = meta_ci(c.m, kk);
-    meta_w<DT_F32>(c.m, kk, wB);
-    float xA[R + 2][4], xB[R + 2][4];
-    load_rows4<R>(c, vo, meta_ci(c.m, k), xA);
-    while (k + 1 < e) {
-        load_rows4<R>(c, vo, ciB, xB);                         // rows of kernel k+1
-        kk = k + 2 <= last ? k + 2 : last;
-        const int ciA2 = meta_ci(c.m, kk);
-        float wA2[4];
-        meta_w<DT_F32>(c.m, kk, wA2);
-        kk = k + 3 <= last ? k + 3 : last;
-        const int ciB2 = meta_ci(c.m, kk);
-        float wB2[4];
-        meta_w<DT_F32>(c.m, kk, wB2);
-        taps(acc, xA, wA);                                     // kernel k
-        load_rows4<R>(c, vo, ciA2, xA);                        // rows of kernel k+2
-        taps(acc, xB, wB);                                     // kernel k+1
-        k += 2;
-        wA[0] = wA2[0], wA[1] = wA2[1], wA[2] = wA2[2], wA[3] = wA2[3];
-        wB[0] = wB2[0], wB[1] = wB2[1], wB[2] = wB2[2], wB[3] = wB2[3];
-        ciB = ciB2;
+    meta_w<DT>(c.m, kk, wB);
+    if constexpr (DT == DT_F32) {
+        float xA[R + 2][4], xB[R + 2][4];
+        load_rows4<R>(c, vo, meta_ci(c.m, k), xA);
+        while (k + 1 < e) {
+            load_rows4<R>(c, vo, ciB, xB);                     // rows of kernel k+1
+            kk = k + 2 <= last ? k + 2 : last;
+            const int ciA2 = meta_ci(c.m, kk);
+            float wA2[4];
+            meta_w<DT>(c.m, kk, wA2);
+            kk = k + 3 <= last ? k + 3 : last;
+            const int ciB2 = meta_ci(c.m, kk);
+            float wB2[4];
+            meta_w<DT>(c.m, kk, wB2);
+            taps(acc, xA, wA);                                 // kernel k
+            load_rows4<R>(c, vo, ciA2, xA);                    // rows of kernel k+2
+            taps(acc, xB, wB);                                 // kernel k+1
+            k += 2;
+            wA[0] = wA2[0], wA[1] = wA2[1], wA[2] = wA2[2], wA[3] = wA2[3];
+            wB[0] = wB2[0], wB[1] = wB2[1], wB[2] = wB2[2], wB[3] = wB2[3];
+            ciB = ciB2;
+        }
+        if (k < e) taps(acc, xA, wA);
+    } else {
+        Half4Rows<R> pA, pB;
+        load_rows4_f16<R>(c, vo, meta_ci(c.m, k), pA);
+        while (k + 1 < e) {
+            load_rows4_f16<R>(c, vo, ciB, pB);                 // rows of kernel k+1
+            kk = k + 2 <= last ? k + 2 : last;
+            const int ciA2 = meta_ci(c.m, kk);
+            float wA2[4];
+            meta_w<DT>(c.m, kk, wA2);
+            kk = k + 3 <= last ? k + 3 : last;
+            const int ciB2 = meta_ci(c.m, kk);
+            float wB2[4];
+            meta_w<DT>(c.m, kk, wB2);
+            {
+                float x[R + 2][4];
+                unpack_rows4<R>(pA, x);
+                taps(acc, x, wA);                              // kernel k
+            }
+            load_rows4_f16<R>(c, vo, ciA2, pA);                // rows of kernel k+2
+            {
+                float x[R + 2][4];
+                unpack_rows4<R>(pB, x);
+                taps(acc, x, wB);                              // kernel k+1
+            }
+            k += 2;
+            wA[0] = wA2[0], wA[1] = wA2[1], wA[2] = wA2[2], wA[3] = wA2[3];
+            wB[0] = wB2[0], wB[1] = wB2[1], wB[2] = wB2[2], wB[3] = wB2[3];
+            ciB = ciB2;
+        }
+        if (k < e) {
+            float x[R + 2][4];
+            unpack_rows4<R>(pA, x);
+            taps(acc, x, wA);
+        }
     }
-    if (k < e) taps(acc, xA, wA);
 }
 
-template <int R, int MASK>
+template <int DT, int R, int MASK>
 __device__ __forceinline__ void run_shape4(const RunCtx& c, const uint32_t (&vo)[R + 2], int k, int e,
                                            float (&acc)[4 * R]) {
     constexpr int Q0 = NthBit<MASK, 0>::value(), Q1 = NthBit<MASK, 1>::value();
     constexpr int Q2 = NthBit<MASK, 2>::value(), Q3 = NthBit<MASK, 3>::value();
-    run_kernels4<R>(c, vo, k, e, acc, [](float (&a)[4 * R], const float (&x)[R + 2][4], const float (&w)[4]) {
+    run_kernels4<DT, R>(c, vo, k, e, acc, [](float (&a)[4 * R], const float (&x)[R + 2][4], const float (&w)[4]) {
         kernel_taps4<R, Q0, Q1, Q2, Q3>(a, x, w);
     });
 }
 
-template <int R>
+template <int DT, int R>
 __device__ __forceinline__ void run_generic4(unsigned mask, const RunCtx& c, const uint32_t (&vo)[R + 2], int k,
                                              int e, float (&acc)[4 * R]) {
     int q[4] = {4, 4, 4, 4}, seen = 0;
@@ -747,17 +822,17 @@ __device__ __forceinline__ void run_generic4(unsigned mask, const RunCtx& c, con
             ++seen;
         }
     }
-    run_kernels4<R>(c, vo, k, e, acc, [=](float (&a)[4 * R], const float (&x)[R + 2][4], const float (&w)[4]) {
+    run_kernels4<DT, R>(c, vo, k, e, acc, [=](float (&a)[4 * R], const float (&x)[R + 2][4], const float (&w)[4]) {
         kernel_taps4_dyn<R>(q, a, x, w);
     });
 }
 
 #define PSC_SHAPE_CASE(I) \
-    case I: run_shape4<R, kCentre3.code[I]>(c, vo, k, e, acc); return;
+    case I: run_shape4<DT, R, kCentre3.code[I]>(c, vo, k, e, acc); return;
 #define PSC_SHAPE_CASE8(I)                                                                     \
     PSC_SHAPE_CASE(I) PSC_SHAPE_CASE(I + 1) PSC_SHAPE_CASE(I + 2) PSC_SHAPE_CASE(I + 3)        \
     PSC_SHAPE_CASE(I + 4) PSC_SHAPE_CASE(I + 5) PSC_SHAPE_CASE(I + 6) PSC_SHAPE_CASE(I + 7)
-template <int R>
+template <int DT, int R>
 __device__ __forceinline__ void run_pattern4(int shape, unsigned mask, const RunCtx& c, const uint32_t (&vo)[R + 2],
                                              int k, int e, float (&acc)[4 * R]) {
     switch (shape) {
@@ -768,21 +843,22 @@ __device__ __forceinline__ void run_pattern4(int shape, unsigned mask, const Run
         PSC_SHAPE_CASE8(32)
         PSC_SHAPE_CASE8(40)
         PSC_SHAPE_CASE8(48)
-        default: run_generic4<R>(mask, c, vo, k, e, acc); return;
+        default: run_generic4<DT, R>(mask, c, vo, k, e, acc); return;
     }
 }
 #undef PSC_SHAPE_CASE8
 #undef PSC_SHAPE_CASE
 
-// Wide form of the kernel (fp32): same blocks, shares, reduction and
-// epilogue as the one-column form, 4 columns per lane.  With 4 rows per lane
-// the compiler is held to 128 VGPRs (4 waves per SIMD).
-template <int R>
-__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(R <= 2 ? 6 : 4))) void k_conv_wide(const float* __restrict__ x, const int32_t* __restrict__ perm,
-                                                   const int32_t* __restrict__ seg_ptr,
-                                                   const int32_t* __restrict__ cin_idx,
-                                                   const float* __restrict__ vals, const float* __restrict__ bias,
-                                                   float* __restrict__ y, Geo g) {
+// Wide form of the kernel: same blocks, shares, reduction and epilogue as
+// the one-column form, 4 columns per lane.  With 4 rows per lane the
+// compiler is held to 128 VGPRs (4 waves per SIMD).
+template <int DT, int R>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(R <= 2 ? 6 : 4))) void k_conv_wide(
+    const typename Elt<DT>::T* __restrict__ x, const int32_t* __restrict__ perm, const int32_t* __restrict__ seg_ptr,
+    const int32_t* __restrict__ cin_idx, const typename Elt<DT>::T* __restrict__ vals,
+    const typename Elt<DT>::T* __restrict__ bias, typename Elt<DT>::T* __restrict__ y, Geo g) {
+    using E = Elt<DT>;
+    constexpr int ESZ = int(sizeof(typename E::T));
     constexpr int ROWS = R + 2;
     extern __shared__ float psc_smem4[];
     const int lane = threadIdx.x & 63;
@@ -813,7 +889,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(R <= 2 ? 6 
 #pragma unroll
     for (int r = 0; r < ROWS; ++r) {
         const int row = h0 - 1 + r;
-        vo[r] = (col0 >= 0 && row >= 0 && row < g.H) ? uint32_t(nimg * g.cin * plane + row * g.W + col0) * 4u
+        vo[r] = (col0 >= 0 && row >= 0 && row < g.H) ? uint32_t(nimg * g.cin * plane + row * g.W + col0) * uint32_t(ESZ)
                                                      : 0x80000000u;
     }
     float acc[4 * R];
@@ -825,14 +901,15 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(R <= 2 ? 6 
         const int f0 = segp[0], f1 = segp[g.m];
         const int len = f1 - f0;
         const int s0 = f0 + len * sp / g.KS, s1 = f0 + len * (sp + 1) / g.KS;
-        const RunCtx ctx{Meta{scalar_rsrc(cin_idx, g.keep * 4), scalar_rsrc(vals, g.keep * 16)},
-                         __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(x), int16_t(0), g.x_bytes, 0x00020000),
-                         __builtin_amdgcn_readfirstlane(plane * 4)};
+        const RunCtx ctx{Meta{scalar_rsrc(cin_idx, g.keep * 4), scalar_rsrc(vals, g.keep * 4 * ESZ)},
+                         __builtin_amdgcn_make_buffer_rsrc(const_cast<typename E::T*>(x), int16_t(0), g.x_bytes,
+                                                           0x00020000),
+                         __builtin_amdgcn_readfirstlane(plane * ESZ)};
         for (int p = 0; p < g.m; ++p) {
             int k0 = segp[p], k1 = segp[p + 1];
             k0 = k0 < s0 ? s0 : k0;
             k1 = k1 > s1 ? s1 : k1;
-            if (k0 < k1) run_pattern4<R>(g.shape[p], g.mask[p], ctx, vo, k0, k1, acc);
+            if (k0 < k1) run_pattern4<DT, R>(g.shape[p], g.mask[p], ctx, vo, k0, k1, acc);
         }
     }
 
@@ -857,12 +934,12 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(R <= 2 ? 6 
     }
     if (!has_filter || col0 < 0) return;
     const int f = perm[i];
-    const float bv = bias ? bias[f] : 0.f;
+    const float bv = bias ? E::load(bias, f) : 0.f;
     if constexpr (R % 2 == 0) {
         if (g.pool) {
             // 2x2/2 max-pool: the lane's 4 columns give 2 pooled columns
             const int OH = g.H / 2, OW = g.W / 2;
-            float* yp = y + (nimg * g.cout + f) * (OH * OW) + col0 / 2;
+            typename E::T* yp = y + (nimg * g.cout + f) * (OH * OW) + col0 / 2;
 #pragma unroll
             for (int j = 0; j < R / 2; ++j) {
                 const int prow = h0 / 2 + j;
@@ -874,14 +951,14 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(R <= 2 ? 6 
                         p0 = p0 > 0.f ? p0 : 0.f;
                         p1 = p1 > 0.f ? p1 : 0.f;
                     }
-                    yp[prow * OW] = p0;
-                    yp[prow * OW + 1] = p1;
+                    yp[prow * OW] = E::from_f(p0);
+                    yp[prow * OW + 1] = E::from_f(p1);
                 }
             }
             return;
         }
     }
-    float* yp = y + (nimg * g.cout + f) * plane + col0;
+    typename E::T* yp = y + (nimg * g.cout + f) * plane + col0;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         const int row = h0 + r;
@@ -893,7 +970,14 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(R <= 2 ? 6 
                 v.z = v.z > 0.f ? v.z : 0.f;
                 v.w = v.w > 0.f ? v.w : 0.f;
             }
-            *reinterpret_cast<psc_f32x4*>(yp + row * g.W) = v;
+            if constexpr (DT == DT_F32) {
+                *reinterpret_cast<psc_f32x4*>(yp + row * g.W) = v;
+            } else {
+                // 4 halves, 8 bytes: col0 and the width are multiples of 4
+                const uint32_t lo = uint32_t(E::from_f(v.x)) | (uint32_t(E::from_f(v.y)) << 16);
+                const uint32_t hi = uint32_t(E::from_f(v.z)) | (uint32_t(E::from_f(v.w)) << 16);
+                *reinterpret_cast<psc_i32x2*>(yp + row * g.W) = psc_i32x2{int32_t(lo), int32_t(hi)};
+            }
         }
     }
 }
@@ -1123,14 +1207,14 @@ __global__ __launch_bounds__(512) void k_conv_stream(const typename Elt<DT>::T* 
     }
 }
 
-template <int R>
+template <int DT, int R>
 hipError_t launch_wide(const PackedView& pk, const ConvArgs& a, const Geo& g, hipStream_t stream) {
+    using T = typename Elt<DT>::T;
     const int waves = g.FW * g.KS;
     const size_t smem = g.KS > 1 ? size_t(g.KS) * 4 * R * 64 * sizeof(float) : 0;
-    hipLaunchKernelGGL((k_conv_wide<R>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)), smem, stream,
-                       static_cast<const float*>(a.x), pk.filter_perm, pk.seg_ptr, pk.cin_idx,
-                       static_cast<const float*>(pk.values), static_cast<const float*>(a.bias),
-                       static_cast<float*>(a.y), g);
+    hipLaunchKernelGGL((k_conv_wide<DT, R>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)), smem, stream,
+                       static_cast<const T*>(a.x), pk.filter_perm, pk.seg_ptr, pk.cin_idx,
+                       static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), static_cast<T*>(a.y), g);
     return hipGetLastError();
 }
 

@@ -20,7 +20,8 @@ PSC_EXTERN_R(DT_F16, 4)
 PSC_EXTERN_R(DT_F16, 7)
 PSC_EXTERN_R(DT_F16, 8)
 #undef PSC_EXTERN_R
-extern template hipError_t cs::launch_wide<4>(const PackedView&, const ConvArgs&, const Geo&, hipStream_t);
+extern template hipError_t cs::launch_wide<DT_F32, 4>(const PackedView&, const ConvArgs&, const Geo&, hipStream_t);
+extern template hipError_t cs::launch_wide<DT_F16, 4>(const PackedView&, const ConvArgs&, const Geo&, hipStream_t);
 
 // Grids of at least this many waves are throughput-bound (16 waves per SIMD).
 constexpr int64_t kManyWaves = 16384;
@@ -67,31 +68,41 @@ bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
             for (int t = 0; t < 56; ++t)
                 if (kCentre3.code[t] == tab.mask[p]) g.shape[p] = int8_t(t);
     }
-    // wide form: fp32 rows of 64..252 columns starting on 64-byte boundaries
-    // (width a multiple of 16): 4 columns per lane, full-row segments padded
-    // to a multiple of 4 lanes
-    if (a.dtype == DT_F32 && a.w % 16 == 0 && a.w >= 64 && a.w / 4 + 1 <= 64) {
-        g.cols_mode = 0;
-        g.seg_len = (a.w / 4 + 1 + 3) / 4 * 4;
-        g.S = 64 / g.seg_len;
-        g.Wt = a.w;
-        g.CT = 1;
-        // four rows per lane: 16 outputs for 6 row loads a kernel, 128
-        // VGPRs (4 waves per SIMD); shares only below about one wave per
-        // SIMD (at 112-224 columns one share measured fastest)
+    // wide form (4 columns per lane, 4 rows): widths 28..252, multiples of 4,
+    // segments padded to a multiple of 4 lanes.  Taken for fp32 rows of 64+
+    // columns on 64-byte boundaries (faster at batch 1 too), and otherwise
+    // when the grid is large enough to be bound by the vector-memory path
+    // rather than by the latency of each wave's kernel chain: there 4 columns
+    // per load instruction beat 1 (32x32 fp32 at batch 256: 2.1x; 56x56 fp16
+    // at batch 32: 1.2x).
+    if (a.w % 4 == 0 && a.w >= 28 && a.w / 4 + 1 <= 64) {
         constexpr int R = 4;
-        g.RB = (a.h + R - 1) / R;
-        g.U = a.n * g.RB;
-        const int sgroups = (g.U + g.S - 1) / g.S;
-        g.KS = 1;
-        while (g.KS < kMaxSplit && int64_t(sgroups) * a.cout * g.KS < 1024 && a.cin >= 16 * g.KS) g.KS *= 2;
-        g.FW = g.KS >= 4 ? 1 : 4 / g.KS;
-        if (g.FW > a.cout) g.FW = a.cout;
-        g.groups_x = (a.cout + g.FW - 1) / g.FW;
-        g.nblocks = g.groups_x * sgroups;
-        g.R = R;
-        g.form = 1;
-        return true;
+        const int seg_len = (a.w / 4 + 1 + 3) / 4 * 4;
+        const int S = 64 / seg_len;
+        const int RB = (a.h + R - 1) / R;
+        const int64_t U = int64_t(a.n) * RB;
+        const int64_t sgroups = (U + S - 1) / S;
+        const bool aligned64 = a.dtype == DT_F32 && a.w % 16 == 0 && a.w >= 64;
+        if (aligned64 || sgroups * a.cout >= kWideMinWaves) {
+            g.cols_mode = 0;
+            g.seg_len = seg_len;
+            g.S = S;
+            g.Wt = a.w;
+            g.CT = 1;
+            g.RB = RB;
+            g.U = int(U);
+            // shares only below about one wave per SIMD (at 112-224 columns
+            // one share measured fastest)
+            g.KS = 1;
+            while (g.KS < kMaxSplit && sgroups * a.cout * g.KS < 1024 && a.cin >= 16 * g.KS) g.KS *= 2;
+            g.FW = g.KS >= 4 ? 1 : 4 / g.KS;
+            if (g.FW > a.cout) g.FW = a.cout;
+            g.groups_x = (a.cout + g.FW - 1) / g.FW;
+            g.nblocks = int(g.groups_x * sgroups);
+            g.R = R;
+            g.form = 1;
+            return true;
+        }
     }
     // lane layout: full-row segments if they use the lanes at least as well
     // as haloed column tiles
@@ -206,7 +217,8 @@ hipError_t launch_conv_stream(const PatTable& tab, const PackedView& pk, const C
                               hipStream_t stream) {
     Geo g;
     if (!plan_conv_stream(tab, a, g)) return hipErrorNotSupported;
-    if (g.form == 1) return launch_wide<4>(pk, a, g, stream);
+    if (g.form == 1) return a.dtype == DT_F16 ? launch_wide<DT_F16, 4>(pk, a, g, stream)
+                                              : launch_wide<DT_F32, 4>(pk, a, g, stream);
     switch (g.R) {
         case 8: return a.dtype == DT_F16 ? launch_r<DT_F16, 8>(pk, a, g, stream)
                                          : launch_r<DT_F32, 8>(pk, a, g, stream);

@@ -1,7 +1,7 @@
 // Measurement probe (not part of the method): the vector-ALU fp32 FMA rate
-// this build can issue, for the roofline of the conv kernels.  Each lane runs
-// 8 independent chains of v_fmac_f32 (packed fp32 is disabled in this build,
-// like in every kernel here); the result is stored so nothing is elided.
+// the library's kernels can issue, for the roofline of the conv kernels.  Each lane runs
+// 8 independent chains of v_fmac_f32 (the library is compiled with packed fp32
+// disabled); the result is stored so nothing is elided.
 #include "common.h"
 #include "launch.h"
 

@@ -210,6 +210,18 @@ def form_cases():
             L = B.Layer(cout, cin, list(FORM_MASKS), cin * cout // 2, dt)
             cfg = B.conv3x3_config(L, dt, n, h, w, False, 2, 2)
             out.append((("rows2", cfg["kernel"], w, cfg["shares"] > 1), n, cin, cout, h, w, dt, False, 2, 2))
+        # the wide form below 64 columns and in fp16, which the automatic
+        # choice takes only for grids of 6144+ waves: many filters over few
+        # channels keep the oracle cheap; ragged bands, a pooled epilogue,
+        # every segment count from 3 to 8 per wave
+        for n, cin, cout, h, w, pool in ((64, 5, 1024, 5, 28, False), (40, 3, 1024, 6, 32, False),
+                                         (16, 4, 1024, 7, 56, False), (16, 3, 1024, 8, 56, True),
+                                         (12, 3, 2048, 4, 64, False)):
+            if dt == B.PSC_F32 and w == 64:
+                continue
+            L = B.Layer(cout, cin, list(FORM_MASKS), cin * cout // 2, dt)
+            cfg = B.conv3x3_config(L, dt, n, h, w, pool, 1, 0)
+            out.append((("wide", cfg["kernel"], cfg["cols_per_lane"], w), n, cin, cout, h, w, dt, pool, 1, 0))
         out.append((("simple-stride2",), 2, 9, 7, 13, 11, dt, False, 2, 0))
         out.append((("simple-algo1",), 2, 9, 7, 13, 11, dt, False, 1, 1))
         out.append((("simple-algo1-pool",), 2, 9, 7, 12, 10, dt, True, 1, 1))

@@ -68,7 +68,12 @@ def test_form_search_reaches_every_form():
     assert any(k[0] == 1 and k[3] for k in keys) and any(k[0] == 1 and k[4] for k in keys)
     assert any(k[2] for k in keys)                                                         # column tiles
     assert {c[0][0] for c in cases if not isinstance(c[0][0], int)} == \
-        {"stride2", "rows", "rows2", "simple-stride2", "simple-algo1", "simple-algo1-pool"}
+        {"stride2", "rows", "rows2", "wide", "simple-stride2", "simple-algo1", "simple-algo1-pool"}
+    wide = [c for c in cases if c[0][0] == "wide"]
+    assert all(c[0][1] == 1 and c[0][2] == 4 for c in wide)
+    assert {(c[6], c[5]) for c in wide} == {(B.PSC_F32, 28), (B.PSC_F32, 32), (B.PSC_F32, 56), (B.PSC_F16, 28),
+                                           (B.PSC_F16, 32), (B.PSC_F16, 56), (B.PSC_F16, 64)}
+    assert any(c[7] for c in wide if c[6] == B.PSC_F16) and any(c[7] for c in wide if c[6] == B.PSC_F32)
     rows = [c for c in cases if c[0][0] == "rows"]
     assert all(c[0][1] == 4 for c in rows)
     for dt in (B.PSC_F32, B.PSC_F16):

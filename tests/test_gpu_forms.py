@@ -45,6 +45,8 @@ def test_form_parity_guard_rerun(case):
         assert (got["kernel"], got["staged"], got["rows_per_lane"]) == (key[0], key[1], key[5])
     elif key[0] == "stride2":
         assert got["kernel"] == key[1] == 3 and got["cols_per_lane"] == key[2] == (2 if w % 4 == 0 else 1)
+    elif key[0] == "wide":
+        assert got["kernel"] == key[1] == 1 and got["cols_per_lane"] == key[2] == 4 and got["rows_per_lane"] == 4
     elif key[0] in ("rows", "rows2"):
         assert got["kernel"] == key[1] == 4 and got["cols_per_lane"] == (w - 1) // stride + 1
     else:
