@@ -17,7 +17,9 @@
 // the chunk, the R+2 rows of x around them, so one dy load feeds KC kernels.
 // The lane layout is the forward's: a lane owns one column and R rows of a
 // band (a wave holds S bands of full rows separated by a zero lane, or a
-// column tile with one halo lane on each side).  Rows come through buffer
+// column tile with one halo lane on each side), or, for widths that are
+// multiples of 4, 4 adjacent columns and R rows (each row one 16-byte fp32 /
+// 8-byte fp16 load).  Rows come through buffer
 // loads at offsets fixed per lane and row, the channel entering as a scalar
 // offset and padding reading zero; the left and right neighbour columns of x
 // are read by DPP inside the FMA.  The taps of a chunk are compiled for its
@@ -43,6 +45,7 @@ struct WGeo {
     int Wt;         // output columns per segment
     int cols_mode;  // 0: full-row segments with zero separators, 1: haloed column tiles
     int rows;       // 1: one image row per lane (small planes at large batch; S images per wave)
+    int wide;       // 1: 4 columns per lane (full-row segments padded to a multiple of 4 lanes)
     int RB, CT;     // row bands and column tiles per image
     int units;      // n * RB * CT (rows: n)
     int slots;      // waves' worth of units: ceil(units / S)
@@ -272,6 +275,221 @@ __device__ __forceinline__ void run_chunk(const WGeo& g, const WCtx& c, const in
     }
 }
 
+// ---- four columns per lane.  A lane owns columns 4c..4c+3 and R rows of a
+// full-row band; segments are padded to a multiple of 4 lanes, so every
+// segment ends in at least one zero lane.  Per band a lane loads its R dy rows
+// and, for each kernel of the chunk, its R+2 x rows, each as one load; the
+// column left of the lane's four is the left lane's last (DPP wave_shr), the
+// one right of them the right lane's first (wave_shl).
+
+// R rows of 4 columns through a buffer descriptor, widened to fp32.
+template <int DT, int N>
+__device__ __forceinline__ void load_row4(__amdgpu_buffer_rsrc_t rs, const uint32_t (&vo)[N], int soff,
+                                          float (&v)[N][4]) {
+#pragma unroll
+    for (int r = 0; r < N; ++r) {
+        if constexpr (DT == DT_F32) {
+            // the words are copied out before the casts: hipcc compiles a bit
+            // cast of a vector-element lvalue as a read of element 0
+            const rw::u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(rs, int(vo[r]), soff, 0);
+            const uint32_t w0 = w.x, w1 = w.y, w2 = w.z, w3 = w.w;
+            v[r][0] = __builtin_bit_cast(float, w0), v[r][1] = __builtin_bit_cast(float, w1);
+            v[r][2] = __builtin_bit_cast(float, w2), v[r][3] = __builtin_bit_cast(float, w3);
+        } else {
+            const rw::u32x2 w = __builtin_amdgcn_raw_buffer_load_b64(rs, int(vo[r]), soff, 0);
+            v[r][0] = float(__builtin_bit_cast(_Float16, uint16_t(w.x)));
+            v[r][1] = float(__builtin_bit_cast(_Float16, uint16_t(w.x >> 16)));
+            v[r][2] = float(__builtin_bit_cast(_Float16, uint16_t(w.y)));
+            v[r][3] = float(__builtin_bit_cast(_Float16, uint16_t(w.y >> 16)));
+        }
+    }
+}
+
+#define PSC_W_SHR "v_fmac_f32_dpp %0, %1, %2 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+#define PSC_W_SHL "v_fmac_f32_dpp %0, %1, %2 wave_shl:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+// Column c of row r of the tap at kernel position Q: acc += x(row r + ky,
+// column c + kx - 1) * dy(row r, column c).
+template <int Q, int C, int R>
+__device__ __forceinline__ void wtap4_at(float& acc, const float (&x)[R + 2][4], const float (&dy)[R][4], int r) {
+    constexpr int ky = Q / 3, col = C + Q % 3 - 1;
+    if constexpr (col < 0)
+        asm volatile(PSC_W_SHR : "+v"(acc) : "v"(x[r + ky][3]), "v"(dy[r][C]));
+    else if constexpr (col > 3)
+        asm volatile(PSC_W_SHL : "+v"(acc) : "v"(x[r + ky][0]), "v"(dy[r][C]));
+    else
+        acc = __builtin_fmaf(x[r + ky][col], dy[r][C], acc);
+}
+#undef PSC_W_SHL
+#undef PSC_W_SHR
+
+template <int Q, int R>
+__device__ __forceinline__ void wtap4(float& acc, const float (&x)[R + 2][4], const float (&dy)[R][4]) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        wtap4_at<Q, 0, R>(acc, x, dy, r);
+        wtap4_at<Q, 1, R>(acc, x, dy, r);
+        wtap4_at<Q, 2, R>(acc, x, dy, r);
+        wtap4_at<Q, 3, R>(acc, x, dy, r);
+    }
+}
+
+template <int R>
+__device__ __forceinline__ void wtap4_dyn(int q, float& acc, const float (&x)[R + 2][4], const float (&dy)[R][4]) {
+    switch (q) {
+        case 0: wtap4<0, R>(acc, x, dy); break;
+        case 1: wtap4<1, R>(acc, x, dy); break;
+        case 2: wtap4<2, R>(acc, x, dy); break;
+        case 3: wtap4<3, R>(acc, x, dy); break;
+        case 4: wtap4<4, R>(acc, x, dy); break;
+        case 5: wtap4<5, R>(acc, x, dy); break;
+        case 6: wtap4<6, R>(acc, x, dy); break;
+        case 7: wtap4<7, R>(acc, x, dy); break;
+        default: wtap4<8, R>(acc, x, dy); break;
+    }
+}
+
+// The chunk [k0, k0 + kc) as in run_chunk, four columns per lane.
+template <int DT, int R, int NT, bool QD, int Q0, int Q1, int Q2, int Q3>
+__device__ __forceinline__ void run_chunk_wide(const WGeo& g, const WCtx& c, const int32_t* __restrict__ cin_idx,
+                                               int f, int k0, int kc, int ci0, const int (&q)[4], int sl0, int sl1,
+                                               int lane, float* __restrict__ out) {
+    constexpr int ESZ = DT == DT_F32 ? 4 : 2;
+    float acc[kKC][NT];
+#pragma unroll
+    for (int j = 0; j < kKC; ++j)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[j][t] = 0.f;
+    int ci[kKC];
+#pragma unroll
+    for (int j = 0; j < kKC; ++j) {
+        const int kj = k0 + (j < kc ? j : 0);
+        // malformed channel indices read zeros (a range-checked load past x)
+        const int cj = g.dense ? ci0 + (j < kc ? j : 0) : cin_idx[kj];
+        ci[j] = __builtin_amdgcn_readfirstlane(unsigned(cj) < unsigned(g.cin) ? cj : 0x7fffffff / c.chan_bytes);
+    }
+    const int seg = lane / g.seg_len, cidx = lane - seg * g.seg_len;
+    for (int sl = sl0; sl < sl1; ++sl) {
+        const int u = sl * g.S + seg;
+        int col0 = -1, nimg = 0, h0 = 0;
+        if (seg < g.S && u < g.units) {
+            nimg = u / g.RB;
+            h0 = (u - nimg * g.RB) * R;
+            if (4 * cidx < g.W) col0 = 4 * cidx;
+        }
+        uint32_t vy[R], vx[R + 2];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int row = h0 + r;
+            vy[r] = (col0 >= 0 && row < g.H) ? uint32_t(((nimg * g.cout + f) * g.H + row) * g.W + col0) * uint32_t(ESZ)
+                                             : 0x80000000u;
+        }
+#pragma unroll
+        for (int r = 0; r < R + 2; ++r) {
+            const int row = h0 - 1 + r;
+            vx[r] = (col0 >= 0 && row >= 0 && row < g.H)
+                        ? uint32_t((nimg * g.cin * g.H + row) * g.W + col0) * uint32_t(ESZ)
+                        : 0x80000000u;
+        }
+        float dyr[R][4];
+        load_row4<DT, R>(c.dys, vy, 0, dyr);
+        float xk[kKC][R + 2][4];
+#pragma unroll
+        for (int j = 0; j < kKC; ++j)
+            if (j < kc) load_row4<DT, R + 2>(c.xs, vx, ci[j] * c.chan_bytes, xk[j]);
+        // the DPP sources (first and last column of every x row) as written
+        // by an asm, then the wait states a DPP read needs after a VALU write
+#pragma unroll
+        for (int j = 0; j < kKC; ++j)
+#pragma unroll
+            for (int r = 0; r < R + 2; ++r) asm volatile("" : "+v"(xk[j][r][0]), "+v"(xk[j][r][3]));
+        asm volatile("s_nop 1");
+#pragma unroll
+        for (int j = 0; j < kKC; ++j) {
+            if (j < kc) {
+                if constexpr (NT == 9) {
+                    wtap4<0, R>(acc[j][0], xk[j], dyr);
+                    wtap4<1, R>(acc[j][1], xk[j], dyr);
+                    wtap4<2, R>(acc[j][2], xk[j], dyr);
+                    wtap4<3, R>(acc[j][3], xk[j], dyr);
+                    wtap4<4, R>(acc[j][4], xk[j], dyr);
+                    wtap4<5, R>(acc[j][5], xk[j], dyr);
+                    wtap4<6, R>(acc[j][6], xk[j], dyr);
+                    wtap4<7, R>(acc[j][7], xk[j], dyr);
+                    wtap4<8, R>(acc[j][8], xk[j], dyr);
+                } else if constexpr (QD) {
+                    wtap4_dyn<R>(q[0], acc[j][0], xk[j], dyr);
+                    wtap4_dyn<R>(q[1], acc[j][1], xk[j], dyr);
+                    wtap4_dyn<R>(q[2], acc[j][2], xk[j], dyr);
+                    wtap4_dyn<R>(q[3], acc[j][3], xk[j], dyr);
+                } else {
+                    wtap4<Q0, R>(acc[j][0], xk[j], dyr);
+                    wtap4<Q1, R>(acc[j][1], xk[j], dyr);
+                    wtap4<Q2, R>(acc[j][2], xk[j], dyr);
+                    wtap4<Q3, R>(acc[j][3], xk[j], dyr);
+                }
+            }
+        }
+    }
+    if constexpr (NT == 4) {
+        float a[kKC * 4];
+#pragma unroll
+        for (int j = 0; j < kKC; ++j)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) a[j * 4 + t] = acc[j][t];
+        const int v = wave_reduce_scatter<kKC * 4>(a, lane);
+        // lanes with the same index hold the same sum: the lowest one writes it
+        if ((lane & (64 / (kKC * 4) - 1)) == 0 && v / 4 < kc) out[int64_t(k0 + v / 4) * 4 + (v % 4)] = a[0];
+    } else {
+#pragma unroll
+        for (int j = 0; j < kKC; ++j)
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                float v = acc[j][t];
+                for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+                acc[j][t] = v;
+            }
+        if (lane == 0)
+#pragma unroll
+            for (int j = 0; j < kKC; ++j)
+                if (j < kc)
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) out[int64_t(k0 + j) * NT + t] = acc[j][t];
+    }
+}
+
+template <int DT, int R, int MASK>
+__device__ __forceinline__ void run_chunk_wide_shape(const WGeo& g, const WCtx& c, const int32_t* cin_idx, int f,
+                                                     int k0, int kc, const int (&q)[4], int sl0, int sl1, int lane,
+                                                     float* out) {
+    run_chunk_wide<DT, R, 4, false, NthBit<MASK, 0>::value(), NthBit<MASK, 1>::value(), NthBit<MASK, 2>::value(),
+                   NthBit<MASK, 3>::value()>(g, c, cin_idx, f, k0, kc, 0, q, sl0, sl1, lane, out);
+}
+
+#define PSC_WW_CASE(I) \
+    case I: run_chunk_wide_shape<DT, R, kCentre3.code[I]>(g, c, cin_idx, f, k0, kc, q, sl0, sl1, lane, out); return;
+#define PSC_WW_CASE8(I)                                                                             \
+    PSC_WW_CASE(I) PSC_WW_CASE(I + 1) PSC_WW_CASE(I + 2) PSC_WW_CASE(I + 3) PSC_WW_CASE(I + 4)      \
+    PSC_WW_CASE(I + 5) PSC_WW_CASE(I + 6) PSC_WW_CASE(I + 7)
+template <int DT, int R>
+__device__ __forceinline__ void run_chunk_wide_pattern(int shape, const WGeo& g, const WCtx& c,
+                                                       const int32_t* cin_idx, int f, int k0, int kc,
+                                                       const int (&q)[4], int sl0, int sl1, int lane, float* out) {
+    switch (shape) {
+        PSC_WW_CASE8(0)
+        PSC_WW_CASE8(8)
+        PSC_WW_CASE8(16)
+        PSC_WW_CASE8(24)
+        PSC_WW_CASE8(32)
+        PSC_WW_CASE8(40)
+        PSC_WW_CASE8(48)
+        default:
+            run_chunk_wide<DT, R, 4, true, 0, 0, 0, 0>(g, c, cin_idx, f, k0, kc, 0, q, sl0, sl1, lane, out);
+            return;
+    }
+}
+#undef PSC_WW_CASE8
+#undef PSC_WW_CASE
+
 // ---- one image row per lane (small planes at large batch).  A wave holds S
 // images, H row lanes each and a zero lane after each image; per image group
 // a lane loads its dy row once (16-byte loads) and, for each kernel of the
@@ -436,8 +654,9 @@ __device__ __forceinline__ void run_chunk_pattern(int shape, const WGeo& g, cons
 // One wave per (filter, chunk group, image share); chunk j of the filter
 // (counted over its pattern segments in storage order) belongs to group
 // j % G.
-// W > 0: one image row per lane (masked gradients on planes of W columns).
-template <int DT, int R, int NT, int W = 0>
+// W > 0: one image row per lane (masked gradients on planes of W columns);
+// WIDE: 4 columns per lane.
+template <int DT, int R, int NT, int W = 0, bool WIDE = false>
 __global__ __launch_bounds__(256) void k_wgrad(const typename Elt<DT>::T* __restrict__ x,
                                                const typename Elt<DT>::T* __restrict__ dy,
                                                const int32_t* __restrict__ perm, const int32_t* __restrict__ seg_ptr,
@@ -464,7 +683,12 @@ __global__ __launch_bounds__(256) void k_wgrad(const typename Elt<DT>::T* __rest
         for (int c0 = 0; c0 < g.cin; c0 += kKC, ++j) {
             if (j % g.G != grp) continue;
             const int kc = g.cin - c0 < kKC ? g.cin - c0 : kKC;
-            run_chunk<DT, R, 9, false, 0, 0, 0, 0>(g, c, nullptr, f, f * g.cin + c0, kc, c0, q0, sl0, sl1, lane, o);
+            if constexpr (WIDE)
+                run_chunk_wide<DT, R, 9, false, 0, 0, 0, 0>(g, c, nullptr, f, f * g.cin + c0, kc, c0, q0, sl0, sl1,
+                                                            lane, o);
+            else
+                run_chunk<DT, R, 9, false, 0, 0, 0, 0>(g, c, nullptr, f, f * g.cin + c0, kc, c0, q0, sl0, sl1, lane,
+                                                       o);
         }
     } else {
         const int f = perm[i];
@@ -482,7 +706,9 @@ __global__ __launch_bounds__(256) void k_wgrad(const typename Elt<DT>::T* __rest
             for (int k0 = segp[p]; k0 < k1; k0 += kKC, ++j) {
                 if (j % g.G != grp) continue;
                 const int kc = k1 - k0 < kKC ? k1 - k0 : kKC;
-                if constexpr (W > 0)
+                if constexpr (WIDE)
+                    run_chunk_wide_pattern<DT, R>(g.shape[p], g, c, cin_idx, f, k0, kc, q, sl0, sl1, lane, o);
+                else if constexpr (W > 0)
                     run_chunk_rows_pattern<DT, W>(g.shape[p], g, c, cin_idx, f, k0, kc, q, sl0, sl1, lane, o);
                 else
                     run_chunk_pattern<DT, R>(g.shape[p], g, c, cin_idx, f, k0, kc, q, sl0, sl1, lane, o);
@@ -491,35 +717,71 @@ __global__ __launch_bounds__(256) void k_wgrad(const typename Elt<DT>::T* __rest
     }
 }
 
-// out[e] = sum over shares s (in order) of part[s][e].
+// out[e] = sum over shares s (in order) of part[s][e]; the loads of four
+// shares are issued together, the adds keep the share order.
 __global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ part, int KS, int64_t n,
                                                       float* __restrict__ out) {
     for (int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x; e < n; e += int64_t(gridDim.x) * 256) {
         float v = part[e];
-        for (int s = 1; s < KS; ++s) v += part[int64_t(s) * n + e];
+        int s = 1;
+        for (; s + 4 <= KS; s += 4) {
+            const float a = part[int64_t(s) * n + e], b = part[int64_t(s + 1) * n + e];
+            const float c = part[int64_t(s + 2) * n + e], d = part[int64_t(s + 3) * n + e];
+            v += a;
+            v += b;
+            v += c;
+            v += d;
+        }
+        for (; s < KS; ++s) v += part[int64_t(s) * n + e];
         out[e] = v;
     }
 }
 
-// db[f] = sum over images and pixels of dy[n, f]; one block per filter.
+// Bias gradient db[f] = sum over images and pixels of dy[n, f], in P parts
+// per filter: part p of filter f sums elements [total p / P, total (p+1) / P)
+// of its images x pixels (total = n * plane; element e is pixel e % plane of
+// image e / plane), each thread with 4 independent accumulators; the parts
+// go to out[p * cout + f] (P > 1; k_wgrad_reduce adds them in part order) or
+// to db (P = 1).  Grid (cout, P), 256 threads.
+constexpr int kBiasPartElems = 8192;
+
+int bias_parts(int n, int plane) {
+    const int64_t total = int64_t(n) * plane;
+    int64_t P = (total + kBiasPartElems - 1) / kBiasPartElems;
+    return int(P < 1 ? 1 : P > 1024 ? 1024 : P);
+}
+
 template <int DT>
 __global__ __launch_bounds__(256) void k_bias_grad(const typename Elt<DT>::T* __restrict__ dy, int n, int cout,
-                                                   int plane, float* __restrict__ db) {
+                                                   int plane, int P, float* __restrict__ out) {
     using E = Elt<DT>;
     __shared__ float part[4];
-    const int f = blockIdx.x;
-    float acc = 0.f;
-    for (int nn = 0; nn < n; ++nn) {
-        const typename E::T* yc = dy + (int64_t(nn) * cout + f) * plane;
-        for (int q = threadIdx.x; q < plane; q += 256) acc += E::load(yc, q);
+    const int f = blockIdx.x, p = blockIdx.y;
+    const int64_t total = int64_t(n) * plane;
+    const int64_t e0 = total * p / P, e1 = total * (p + 1) / P;
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+    auto at = [&](int64_t e) -> float {
+        const int64_t img = e / plane;
+        return E::load(dy, (img * cout + f) * plane + (e - img * plane));
+    };
+    int64_t e = e0 + threadIdx.x;
+    for (; e + 768 < e1; e += 1024) {
+        const float v0 = at(e), v1 = at(e + 256), v2 = at(e + 512), v3 = at(e + 768);
+        a0 += v0;
+        a1 += v1;
+        a2 += v2;
+        a3 += v3;
     }
+    for (; e < e1; e += 256) a0 += at(e);
+    float acc = (a0 + a1) + (a2 + a3);
     for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
     if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
     __syncthreads();
-    if (threadIdx.x == 0) db[f] = (part[0] + part[1]) + (part[2] + part[3]);
+    if (threadIdx.x == 0) out[P > 1 ? int64_t(p) * cout + f : f] = (part[0] + part[1]) + (part[2] + part[3]);
 }
 
 constexpr int64_t kTargetWaves = 16384;   // 16 waves per SIMD
+constexpr int kWideRows = 2;              // rows per lane of the 4-column layout
 constexpr int kMaxShares = 64;
 
 WGeo plan(int n, int cin, int cout, int h, int w, int64_t nk, bool dense, const PatTable* tab, int dtype) {
@@ -555,6 +817,15 @@ WGeo plan(int n, int cin, int cout, int h, int w, int64_t nk, bool dense, const 
         g.RB = 1;
         g.units = n;
         g.slots = (n + g.S - 1) / g.S;
+    } else if (w % 4 == 0 && w / 4 + 1 <= 64) {
+        // four columns per lane: full-row segments padded to a multiple of 4
+        // lanes (at least one zero lane after each)
+        g.wide = 1;
+        g.cols_mode = 0;
+        g.seg_len = (w / 4 + 1 + 3) / 4 * 4;
+        g.S = 64 / g.seg_len;
+        g.Wt = w;
+        g.CT = 1;
     } else {
         // full-row segments if they use the lanes at least as well as
         // haloed column tiles (the forward's choice)
@@ -584,7 +855,7 @@ WGeo plan(int n, int cin, int cout, int h, int w, int64_t nk, bool dense, const 
         }
     }
     if (!g.rows) {
-        const int R = h >= 8 ? 8 : 4;
+        const int R = g.wide ? kWideRows : h >= 8 ? 8 : 4;
         g.RB = (h + R - 1) / R;
         g.units = n * g.RB * g.CT;
         g.slots = (g.units + g.S - 1) / g.S;
@@ -629,6 +900,11 @@ hipError_t run(const WGeo& g, const void* x, const void* dy, const int32_t* perm
         }
     }
 #undef PSC_WROWS
+    if (!done && g.wide) {
+        hipLaunchKernelGGL((k_wgrad<DT, kWideRows, NT, 0, true>), grid, dim3(256), 0, stream,
+                           static_cast<const T*>(x), static_cast<const T*>(dy), perm, seg_ptr, cin_idx, g, dst);
+        done = true;
+    }
     if (!done) {
         if (g.H >= 8)
             hipLaunchKernelGGL((k_wgrad<DT, 8, NT>), grid, dim3(256), 0, stream, static_cast<const T*>(x),
@@ -646,10 +922,18 @@ hipError_t run(const WGeo& g, const void* x, const void* dy, const int32_t* perm
     return hipGetLastError();
 }
 
+// db through P parts per filter (partials after the weight-gradient
+// partials in the workspace when P > 1).
 template <int DT>
-hipError_t bias_grad(const void* dy, int n, int cout, int plane, float* db, hipStream_t stream) {
-    hipLaunchKernelGGL(k_bias_grad<DT>, dim3(unsigned(cout)), dim3(256), 0, stream,
-                       static_cast<const typename Elt<DT>::T*>(dy), n, cout, plane, db);
+hipError_t bias_grad(const void* dy, int n, int cout, int plane, float* db, float* part, hipStream_t stream) {
+    const int P = bias_parts(n, plane);
+    float* dst = P > 1 ? part : db;
+    hipLaunchKernelGGL(k_bias_grad<DT>, dim3(unsigned(cout), unsigned(P)), dim3(256), 0, stream,
+                       static_cast<const typename Elt<DT>::T*>(dy), n, cout, plane, P, dst);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || P == 1) return e;
+    hipLaunchKernelGGL(k_wgrad_reduce, dim3(unsigned((cout + 255) / 256)), dim3(256), 0, stream, part, P,
+                       int64_t(cout), db);
     return hipGetLastError();
 }
 
@@ -661,9 +945,17 @@ bool wgrad_fits(int n, int cin, int cout, int h, int w, int dtype) {
     return int64_t(n) * cin * h * w * esz <= 0x7fffffff && int64_t(n) * cout * h * w * esz <= 0x7fffffff;
 }
 
+// Workspace: the image shares' weight-gradient sums (KS > 1), then the bias
+// parts (P > 1).
+static size_t wgrad_part_bytes(const WGeo& g, int64_t nk, bool dense) {
+    return g.KS > 1 && g.n > 0 ? size_t(g.KS) * size_t(nk) * (dense ? 9 : 4) * sizeof(float) : 0;
+}
+
 size_t wgrad_workspace_bytes(int n, int cin, int cout, int h, int w, int64_t nk, bool dense) {
+    if (n <= 0) return 0;
     const WGeo g = plan(n, cin, cout, h, w, nk, dense, nullptr, DT_F32);
-    return g.KS > 1 && n > 0 ? size_t(g.KS) * size_t(nk) * (dense ? 9 : 4) * sizeof(float) : 0;
+    const int P = bias_parts(n, h * w);
+    return wgrad_part_bytes(g, nk, dense) + (P > 1 ? size_t(P) * size_t(cout) * sizeof(float) : 0);
 }
 
 hipError_t launch_bwd_weight(const PatTable& tab, const PackedView& pk, int dtype, int n, int cin, int h, int w,
@@ -674,8 +966,9 @@ hipError_t launch_bwd_weight(const PatTable& tab, const PackedView& pk, int dtyp
                        ? run<DT_F16, 4>(g, x, dy, pk.filter_perm, pk.seg_ptr, pk.cin_idx, dv, ws, stream)
                        : run<DT_F32, 4>(g, x, dy, pk.filter_perm, pk.seg_ptr, pk.cin_idx, dv, ws, stream);
     if (e != hipSuccess || !db) return e;
-    return dtype == DT_F16 ? bias_grad<DT_F16>(dy, n, cout, h * w, db, stream)
-                           : bias_grad<DT_F32>(dy, n, cout, h * w, db, stream);
+    float* bpart = ws ? reinterpret_cast<float*>(static_cast<char*>(ws) + wgrad_part_bytes(g, keep, false)) : nullptr;
+    return dtype == DT_F16 ? bias_grad<DT_F16>(dy, n, cout, h * w, db, bpart, stream)
+                           : bias_grad<DT_F32>(dy, n, cout, h * w, db, bpart, stream);
 }
 
 hipError_t launch_dense_wgrad(const float* x, const float* g_, int n, int cin, int h, int w, int cout, float* dw,
@@ -683,7 +976,9 @@ hipError_t launch_dense_wgrad(const float* x, const float* g_, int n, int cin, i
     const WGeo g = plan(n, cin, cout, h, w, int64_t(cout) * cin, true, nullptr, DT_F32);
     hipError_t e = run<DT_F32, 9>(g, x, g_, nullptr, nullptr, nullptr, dw, ws, stream);
     if (e != hipSuccess || !db) return e;
-    return bias_grad<DT_F32>(g_, n, cout, h * w, db, stream);
+    float* bpart =
+        ws ? reinterpret_cast<float*>(static_cast<char*>(ws) + wgrad_part_bytes(g, int64_t(cout) * cin, true)) : nullptr;
+    return bias_grad<DT_F32>(g_, n, cout, h * w, db, bpart, stream);
 }
 
 }  // namespace psc

@@ -77,7 +77,7 @@ def _check_iteration(st, x, target_d, rho, scale, what):
 CASES = [
     # cout, cin, h, w, T, m, drop
     (8, 3, 9, 11, 2, 4, 0), (12, 10, 7, 6, 3, 6, 50), (16, 24, 14, 14, 2, 8, 60), (5, 7, 1, 1, 4, 8, 30),
-    (20, 6, 5, 70, 2, 8, 40),
+    (20, 6, 5, 70, 2, 8, 40), (6, 5, 9, 12, 2, 6, 40), (4, 3, 6, 28, 3, 8, 50),
 ]
 
 

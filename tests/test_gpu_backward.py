@@ -42,6 +42,10 @@ SHAPES = [
     # last row of x and of dy at the end of its buffer)
     (13, 5, 6, 4, 4), (9, 7, 5, 7, 7), (11, 3, 5, 7, 7), (8, 16, 9, 8, 8), (7, 4, 5, 5, 8),
     (5, 6, 7, 14, 14), (4, 10, 6, 16, 16), (32, 64, 64, 7, 7),
+    # widths that are multiples of 4 below a whole wave of images (4 columns
+    # per lane in the weight gradient): one to sixteen row bands per wave,
+    # ragged last bands, a 63-lane segment
+    (1, 3, 5, 6, 4), (3, 9, 7, 11, 32), (2, 6, 5, 7, 64), (1, 8, 4, 9, 224), (1, 3, 4, 5, 252),
 ]
 
 
