@@ -232,16 +232,18 @@ __global__ __launch_bounds__(64) void k_pack_count(const uint8_t* __restrict__ p
 
 // Rank of each filter under (count desc, per-pattern counts lexicographically
 // desc, index asc); the key is a total order, so ranks form a permutation.
+// One block per filter f: its threads compare f with every other filter g
+// (g = t, t + 256, ...) and the block adds up how many come first.
 __global__ __launch_bounds__(256) void k_pack_rank(const int32_t* __restrict__ cnt,
                                                    const int32_t* __restrict__ nf, int cout, int m,
                                                    int32_t* __restrict__ perm,
                                                    int32_t* __restrict__ nf_sorted) {
-    const int f = blockIdx.x * 256 + threadIdx.x;
-    if (f >= cout) return;
+    __shared__ int part[4];
+    const int f = blockIdx.x;
     const int nff = nf[f];
     const int32_t* cf = cnt + int64_t(f) * m;
     int rank = 0;
-    for (int g = 0; g < cout; ++g) {
+    for (int g = threadIdx.x; g < cout; g += 256) {
         if (g == f) continue;
         const int ng = nf[g];
         bool before;
@@ -259,8 +261,14 @@ __global__ __launch_bounds__(256) void k_pack_rank(const int32_t* __restrict__ c
         }
         rank += before ? 1 : 0;
     }
-    perm[rank] = f;
-    nf_sorted[rank] = nff;
+    for (int off = 32; off > 0; off >>= 1) rank += __shfl_xor(rank, off);
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = rank;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int r = part[0] + part[1] + part[2] + part[3];
+        perm[r] = f;
+        nf_sorted[r] = nff;
+    }
 }
 
 // out[0..n] = exclusive prefix sums of in[0..n-1], out[n] = total.
@@ -479,7 +487,7 @@ hipError_t launch_pack(const PatTable& tab, int dtype, int cout, int cin, int64_
     const int m = tab.m;
     const unsigned g256 = unsigned((cout + 255) / 256);
     hipLaunchKernelGGL(k_pack_count, dim3(cout), dim3(64), 0, stream, pat, keep, cin, m, cnt, nf);
-    hipLaunchKernelGGL(k_pack_rank, dim3(g256), dim3(256), 0, stream, cnt, nf, cout, m,
+    hipLaunchKernelGGL(k_pack_rank, dim3(unsigned(cout)), dim3(256), 0, stream, cnt, nf, cout, m,
                        out.filter_perm, nfs);
     hipLaunchKernelGGL(k_scan_excl_i32, dim3(1), dim3(1024), 0, stream, nfs, out.filter_ptr, cout);
     hipLaunchKernelGGL(k_pack_seg, dim3(g256), dim3(256), 0, stream, cnt, out.filter_perm,

@@ -110,3 +110,22 @@ def test_config_query_validates():
     assert B.conv3x3_config(L, B.PSC_F32, 6, 8, 8, False, 1, 0)["kernel"] == 0        # less than a wave
     assert B.conv3x3_config(L, B.PSC_F32, 7, 8, 8, False, 1, 3)["kernel"] == 0        # algo 3: column per lane
     assert B.conv3x3_config(L, B.PSC_F32, 64, 28, 28, False, 1, 0)["kernel"] == 0     # wider than 16
+
+
+def test_r8_with_several_segments_is_never_planned():
+    """R = 8 rows per lane with more than one row band per wave (direct form)
+    faulted the device once, on the batch-256 fp32 layers 128@16x16 and
+    256@8x8; the cause was not found, so the planner must never choose it.
+    The configuration query covers every stride-1 shape class of the
+    workloads and the form grid, at batch 1 to 256."""
+    for dt in (B.PSC_F32, B.PSC_F16):
+        for n in (1, 4, 32, 64, 256):
+            for cin, cout in ((3, 64), (64, 64), (128, 128), (256, 256), (512, 512)):
+                for hw in (4, 7, 8, 10, 14, 16, 20, 28, 32, 56, 62, 63):
+                    L = B.Layer(cout, cin, [23, 282, 58, 90, 153, 216, 120, 57], cin * cout // 3, dt)
+                    for pool in ((False, True) if hw % 2 == 0 else (False,)):
+                        for algo in (0, 3):
+                            cfg = B.conv3x3_config(L, dt, n, hw, hw, pool, 1, algo)
+                            if cfg["kernel"] == 0:
+                                assert not (cfg["rows_per_lane"] == 8 and cfg["segments_per_wave"] > 1), \
+                                    (dt, n, cin, cout, hw, pool, algo, cfg)

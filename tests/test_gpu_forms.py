@@ -79,3 +79,10 @@ def test_form_parity_guard_rerun(case):
         "write outside the output"
     ref, s = oracle_ref(x, packed, masks, cout, bias=bias, relu=relu, stride=stride, pool=pool)
     check_output(y.cpu().numpy(), ref, s, dtype, max_terms(packed), "form %s" % (key,))
+
+
+@pytest.mark.skip(reason="R = 8 rows per lane with several row bands per wave (direct form, fp32, batch 256, "
+                         "128@16x16 and 256@8x8) faulted the device once; the cause is not found, so no entry "
+                         "point can select it (test_r8_with_several_segments_is_never_planned guards the planner)")
+def test_r8_several_segments_direct_form():
+    pytest.fail("no entry point selects this form")
