@@ -48,7 +48,7 @@ constexpr int64_t kSplitWaves = 4096;
 bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
     const int64_t x_bytes = int64_t(a.n) * a.cin * a.h * a.w * (a.dtype == DT_F16 ? 2 : 4);
     // buffer descriptors address at most 2 GiB (x) and the packed weights
-    if (x_bytes > (int64_t(1) << 31) || a.keep * 4 * (a.dtype == DT_F16 ? 2 : 4) > 0x7fffffff)
+    if (x_bytes >= (int64_t(1) << 31) || a.keep * 4 * (a.dtype == DT_F16 ? 2 : 4) > 0x7fffffff)
         return false;
     std::memset(&g, 0, sizeof g);
     g.n = a.n;
@@ -58,7 +58,7 @@ bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
     g.cout = a.cout;
     g.m = tab.m;
     g.relu = a.relu;
-    g.x_bytes = int(x_bytes > 0x7fffffff ? 0x7fffffff : x_bytes);
+    g.x_bytes = int(x_bytes);
     g.keep = int(a.keep);
     g.pool = a.pool;
     for (int p = 0; p < kMaxPatterns; ++p) {

@@ -167,6 +167,25 @@ def test_conv_many_channel_chunks(dtype):
     check_conv(prep, packed, x, masks, dtype=dtype)
 
 
+@pytest.mark.parametrize("cin,kernel", [(8191, 0), (8192, 2)])
+def test_conv_at_the_2gib_input_limit(cin, kernel):
+    """fp32 x at the limit of a buffer descriptor's range (2^31 - 1 bytes):
+    2^31 - 256 KiB bytes run the tuned kernel, whose last channel ends just
+    below the limit; exactly 2^31 bytes take the one-output-per-lane kernel.
+    The last channel's kernels carry the largest weights, so they are kept
+    and its last rows are read."""
+    n, cout, h, w = 1, 4, 256, 256
+    wt, masks, _ = _case(777, cout, cin, 8, 0, np.float32)
+    wt[:, cin - 1] *= 100.0
+    prep, packed = prepared_case(wt, masks, 64)
+    assert (packed["cin_idx"] == cin - 1).sum() == cout
+    assert B.conv3x3_config(prep.layer, B.PSC_F32, n, h, w, False, 1, 0)["kernel"] == kernel
+    x = inputs.normal_activations(778, (n, cin, h, w))
+    assert x.nbytes == (1 << 31) - (8192 - cin) * h * w * 4
+    note("conv at the 2 GiB input limit, cin=%d" % cin)
+    check_conv(prep, packed, x, masks, what="2 GiB limit cin=%d" % cin)
+
+
 def test_conv_deterministic_and_in_bounds():
     torch = torch_mod()
     n, cin, cout, h, w = 2, 40, 24, 14, 14
