@@ -83,6 +83,9 @@ def parse():
                     help="skip the ADMM pruning iteration timings")
     ap.add_argument("--profile-only", action="store_true",
                     help="only the headline workload's warm-up and timed eager steps (for profiler runs)")
+    ap.add_argument("--profile-part", choices=("forward", "backward", "admm"), default="forward",
+                    help="with --profile-only: the forward step, the retraining kernels (dx and masked dW of "
+                         "every stride-1 layer) or ADMM iterations of the ADMM workload --workload names")
     return ap.parse_args()
 
 
@@ -319,6 +322,31 @@ def cpu_baseline(net, budget_s=8.0):
             "value_1thread": round(flops1 / tt / 1e9, 3)}
 
 
+def backward_calls(net):
+    """One retraining pass over the stride-1 layers of a prepared workload
+    (dx through the transposed packing, then dv and db), as a callable."""
+    import torch
+    from paper_2003_06513_amd import binding as B
+    calls = []
+    for L in net.layers:
+        lay = L["lay"]
+        if lay.stride != 1:
+            continue
+        pt = B.prepare_transposed(L["prep"], L["w"])
+        dy = torch.randn((net.wl.batch, lay.cout, lay.h, lay.w), device="cuda").to(net.tdt)
+        dx = torch.empty((net.wl.batch, lay.cin, lay.h, lay.w), dtype=net.tdt, device="cuda")
+        dv = torch.empty(4 * lay.keep, dtype=torch.float32, device="cuda")
+        db = torch.empty(lay.cout, dtype=torch.float32, device="cuda")
+        ws = B.conv3x3_bwd_weight_workspace(L["prep"].layer, L["prep"].layer.dtype, net.wl.batch, lay.h, lay.w)
+        calls.append((pt, L, dy, dx, dv, db, ws))
+
+    def run():
+        for pt, L, dy, dx, dv, db, ws in calls:
+            B.conv3x3_fwd(pt.layer, pt.packed, dy, dx)
+            B.conv3x3_bwd_weight(L["prep"].layer, L["prep"].packed, L["x"], dy, dv, db, ws=ws)
+    return run
+
+
 def measure_backward(net):
     """Retraining kernels (Sec. 3.3) on every stride-1 layer of a prepared
     workload: dx through the transposed packing (the tuned forward kernels)
@@ -357,7 +385,7 @@ def measure_backward(net):
     return out
 
 
-def measure_admm(wl, iters=10):
+def measure_admm(wl, iters=10, parts=True):
     """One ADMM iteration of one layer (Algorithm 1): the pre-trained target,
     the current layer, the loss gradient, the dense weight gradient, the SGD
     step, the projection (project + select) and the dual step, on a new
@@ -387,6 +415,8 @@ def measure_admm(wl, iters=10):
     e.record()
     torch.cuda.synchronize()
     ms_iter = s.elapsed_time(e) / iters
+    if not parts:
+        return {"ms_per_iteration": round(ms_iter, 4)}
     x = xs[0]
     z = st._bufs["z"]
     dense_fl = 18.0 * wl.batch * wl.layer.h * wl.layer.w * wl.layer.cin * wl.layer.cout
@@ -587,7 +617,26 @@ def main():
                           "launches": 5}))
         return
     B.lib()
+    if args.profile_only and args.profile_part == "admm":
+        from synthetic import inputs
+        found = [w for w in inputs.admm_workloads() if w.name == args.workload]
+        if not found:
+            raise SystemExit("unknown ADMM workload %s; admm workloads: %s"
+                             % (args.workload, ", ".join(w.name for w in inputs.admm_workloads())))
+        measure_admm(found[0], iters=args.steps, parts=False)
+        print(json.dumps({"admm_workload": found[0].name, "steps": args.steps}), flush=True)
+        return
     head = find_workload(args.workload)
+    if args.profile_only and args.profile_part == "backward":
+        net = Net(head, args.algo)
+        net.choose_fusion("none")
+        run = backward_calls(net)
+        for _ in range(args.warmup + args.steps):
+            run()
+        torch.cuda.synchronize()
+        print(json.dumps({"workload": head.name, "part": "backward", "steps": args.steps,
+                          "warmup": args.warmup}), flush=True)
+        return
     if args.profile_only:
         net = Net(head, args.algo)
         net.choose_fusion(args.fuse_pool)
