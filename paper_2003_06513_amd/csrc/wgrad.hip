@@ -46,6 +46,7 @@ struct WGeo {
     int cols_mode;  // 0: full-row segments with zero separators, 1: haloed column tiles
     int rows;       // 1: one image row per lane (small planes at large batch; S images per wave)
     int wide;       // 1: 4 columns per lane (full-row segments padded to a multiple of 4 lanes)
+    int pipe;       // 1: one slot per wave, chunks pipelined (masked gradients, one-column layout)
     int RB, CT;     // row bands and column tiles per image
     int units;      // n * RB * CT (rows: n)
     int slots;      // waves' worth of units: ceil(units / S)
@@ -272,6 +273,196 @@ __device__ __forceinline__ void run_chunk(const WGeo& g, const WCtx& c, const in
                 if (j < kc)
 #pragma unroll
                     for (int t = 0; t < NT; ++t) out[int64_t(k0 + j) * NT + t] = acc[j][t];
+    }
+}
+
+// ---- one band group per wave (small planes at small batch): the wave's dy
+// rows are loaded once, and the channel indices and x rows of its next chunk
+// load while the current chunk's FMAs and wave reduction run.  A wave takes
+// the chunks j = grp, grp + G, ... of its filter (counted over the pattern
+// segments in storage order).
+
+// Per-lane byte offsets of the R dy rows and the R+2 x rows (channel 0) of
+// slot sl in the one-column layout; past the buffer range for padding.
+template <int DT, int R>
+__device__ __forceinline__ void slot_offsets(const WGeo& g, int f, int sl, int lane, uint32_t (&vy)[R],
+                                             uint32_t (&vx)[R + 2]) {
+    constexpr int ESZ = DT == DT_F32 ? 4 : 2;
+    const int seg = lane / g.seg_len, cidx = lane - seg * g.seg_len;
+    const int u = sl * g.S + seg;
+    int ld_col = -1, out_col = -1, nimg = 0, h0 = 0;
+    if (seg < g.S && u < g.units) {
+        nimg = u / (g.RB * g.CT);
+        const int rb = (u / g.CT) % g.RB, ct = u % g.CT;
+        h0 = rb * R;
+        if (!g.cols_mode) {
+            if (cidx < g.W) ld_col = out_col = cidx;
+        } else {
+            const int col = ct * g.Wt + cidx - 1;
+            if (col >= 0 && col < g.W) ld_col = col;
+            if (cidx >= 1 && cidx <= g.Wt && col < g.W) out_col = col;
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int row = h0 + r;
+        vy[r] = (out_col >= 0 && row < g.H) ? uint32_t(((nimg * g.cout + f) * g.H + row) * g.W + out_col) * uint32_t(ESZ)
+                                            : 0x80000000u;
+    }
+#pragma unroll
+    for (int r = 0; r < R + 2; ++r) {
+        const int row = h0 - 1 + r;
+        vx[r] = (ld_col >= 0 && row >= 0 && row < g.H)
+                    ? uint32_t((nimg * g.cin * g.H + row) * g.W + ld_col) * uint32_t(ESZ)
+                    : 0x80000000u;
+    }
+}
+
+// One chunk of the wave's sequence: kernels [k0, k0 + kc) of segment p.
+struct WChunk {
+    int p, k0, kc;
+    bool valid;
+};
+
+// The chunk with index j of the filter (j counted over the segments from
+// segment p on, whose first chunk has index jb), or invalid past the end.
+__device__ __forceinline__ WChunk chunk_at(const WGeo& g, const int32_t* segp, int p, int jb, int j) {
+    for (; p < g.m; ++p) {
+        const int a = segp[p], b = segp[p + 1];
+        const int nc = b > a ? (b - a + kKC - 1) / kKC : 0;
+        if (j < jb + nc) {
+            const int k0 = a + (j - jb) * kKC;
+            return WChunk{p, k0, b - k0 < kKC ? b - k0 : kKC, true};
+        }
+        jb += nc;
+    }
+    return WChunk{g.m, 0, 0, false};
+}
+
+template <int DT, int R>
+__device__ __forceinline__ void load_chunk(const WGeo& g, const WCtx& c, const int32_t* __restrict__ cin_idx,
+                                           const WChunk& ch, const uint32_t (&vx)[R + 2], float (&xk)[kKC][R + 2]) {
+#pragma unroll
+    for (int j = 0; j < kKC; ++j) {
+        if (j < ch.kc) {
+            const int cj = cin_idx[ch.k0 + j];
+            // malformed channel indices read zeros (a range-checked load past x)
+            const int ci = __builtin_amdgcn_readfirstlane(unsigned(cj) < unsigned(g.cin) ? cj : 0x7fffffff / c.chan_bytes);
+            load_col<DT, R + 2>(c.xs, vx, ci * c.chan_bytes, xk[j]);
+        }
+    }
+}
+
+template <int R, bool QD, int Q0, int Q1, int Q2, int Q3>
+__device__ __forceinline__ void chunk_taps(float (&acc)[kKC][4], float (&xk)[kKC][R + 2], const float (&dyr)[R],
+                                           int kc, const int (&q)[4]) {
+#pragma unroll
+    for (int j = 0; j < kKC; ++j) {
+        if (j < kc) {
+            settle<R + 2>(xk[j]);
+            if constexpr (QD) {
+                wtap_dyn<R>(q[0], acc[j][0], xk[j], dyr);
+                wtap_dyn<R>(q[1], acc[j][1], xk[j], dyr);
+                wtap_dyn<R>(q[2], acc[j][2], xk[j], dyr);
+                wtap_dyn<R>(q[3], acc[j][3], xk[j], dyr);
+            } else {
+                wtap<R, Q0>(acc[j][0], xk[j], dyr);
+                wtap<R, Q1>(acc[j][1], xk[j], dyr);
+                wtap<R, Q2>(acc[j][2], xk[j], dyr);
+                wtap<R, Q3>(acc[j][3], xk[j], dyr);
+            }
+        }
+    }
+}
+
+#define PSC_WP_CASE(I)                                                                                      \
+    case I:                                                                                                 \
+        chunk_taps<R, false, NthBit<kCentre3.code[I], 0>::value(), NthBit<kCentre3.code[I], 1>::value(),    \
+                   NthBit<kCentre3.code[I], 2>::value(), NthBit<kCentre3.code[I], 3>::value()>(acc, xk, dyr, \
+                                                                                               kc, q);      \
+        return;
+#define PSC_WP_CASE8(I)                                                                             \
+    PSC_WP_CASE(I) PSC_WP_CASE(I + 1) PSC_WP_CASE(I + 2) PSC_WP_CASE(I + 3) PSC_WP_CASE(I + 4)      \
+    PSC_WP_CASE(I + 5) PSC_WP_CASE(I + 6) PSC_WP_CASE(I + 7)
+template <int R>
+__device__ __forceinline__ void chunk_taps_pattern(int shape, float (&acc)[kKC][4], float (&xk)[kKC][R + 2],
+                                                   const float (&dyr)[R], int kc, const int (&q)[4]) {
+    switch (shape) {
+        PSC_WP_CASE8(0)
+        PSC_WP_CASE8(8)
+        PSC_WP_CASE8(16)
+        PSC_WP_CASE8(24)
+        PSC_WP_CASE8(32)
+        PSC_WP_CASE8(40)
+        PSC_WP_CASE8(48)
+        default: chunk_taps<R, true, 0, 0, 0, 0>(acc, xk, dyr, kc, q); return;
+    }
+}
+#undef PSC_WP_CASE8
+#undef PSC_WP_CASE
+
+// The chunk's kc x 4 sums over the wave, written by the lanes that hold them.
+__device__ __forceinline__ void chunk_write(float (&acc)[kKC][4], int k0, int kc, int lane, float* __restrict__ out) {
+    float a[kKC * 4];
+#pragma unroll
+    for (int j = 0; j < kKC; ++j)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) a[j * 4 + t] = acc[j][t];
+    const int v = wave_reduce_scatter<kKC * 4>(a, lane);
+    if ((lane & (64 / (kKC * 4) - 1)) == 0 && v / 4 < kc) out[int64_t(k0 + v / 4) * 4 + (v % 4)] = a[0];
+}
+
+__device__ __forceinline__ void pattern_taps(unsigned mk, int (&q)[4]) {
+    int t = 0;
+    q[0] = q[1] = q[2] = q[3] = 4;
+    for (int u = 0; u < 9; ++u)
+        if ((mk >> u) & 1u) {
+            if (t < 4) q[t] = u;
+            ++t;
+        }
+}
+
+// One chunk of the pipeline: the next chunk's rows start loading into xn,
+// then the current chunk's taps and reduction run on xc.
+template <int DT, int R>
+__device__ __forceinline__ WChunk pipe_step(const WGeo& g, const WCtx& c, const int32_t* segp,
+                                            const int32_t* __restrict__ cin_idx, const uint32_t (&vx)[R + 2],
+                                            const float (&dyr)[R], const WChunk& cur, int jc,
+                                            float (&xc)[kKC][R + 2], float (&xn)[kKC][R + 2], int lane,
+                                            float* __restrict__ out) {
+    const WChunk nx = chunk_at(g, segp, cur.p, jc - (cur.k0 - segp[cur.p]) / kKC, jc + g.G);
+    if (nx.valid) load_chunk<DT, R>(g, c, cin_idx, nx, vx, xn);
+    float acc[kKC][4];
+#pragma unroll
+    for (int j = 0; j < kKC; ++j)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[j][t] = 0.f;
+    int q[4];
+    pattern_taps(g.mask[cur.p], q);
+    chunk_taps_pattern<R>(g.shape[cur.p], acc, xc, dyr, cur.kc, q);
+    chunk_write(acc, cur.k0, cur.kc, lane, out);
+    return nx;
+}
+
+template <int DT, int R>
+__device__ __forceinline__ void run_filter_pipe(const WGeo& g, const WCtx& c, const int32_t* segp,
+                                                const int32_t* __restrict__ cin_idx, int f, int grp, int lane,
+                                                float* __restrict__ out) {
+    uint32_t vy[R], vx[R + 2];
+    slot_offsets<DT, R>(g, f, 0, lane, vy, vx);
+    float dyr[R];
+    load_col<DT, R>(c.dys, vy, 0, dyr);
+    WChunk cA = chunk_at(g, segp, 0, 0, grp);
+    if (!cA.valid) return;
+    int jA = grp;
+    float xA[kKC][R + 2], xB[kKC][R + 2];
+    load_chunk<DT, R>(g, c, cin_idx, cA, vx, xA);
+    while (true) {
+        const WChunk cB = pipe_step<DT, R>(g, c, segp, cin_idx, vx, dyr, cA, jA, xA, xB, lane, out);
+        if (!cB.valid) break;
+        cA = pipe_step<DT, R>(g, c, segp, cin_idx, vx, dyr, cB, jA + g.G, xB, xA, lane, out);
+        jA += 2 * g.G;
+        if (!cA.valid) break;
     }
 }
 
@@ -655,8 +846,8 @@ __device__ __forceinline__ void run_chunk_pattern(int shape, const WGeo& g, cons
 // (counted over its pattern segments in storage order) belongs to group
 // j % G.
 // W > 0: one image row per lane (masked gradients on planes of W columns);
-// WIDE: 4 columns per lane.
-template <int DT, int R, int NT, int W = 0, bool WIDE = false>
+// WIDE: 4 columns per lane; PIPE: one slot per wave, chunks pipelined.
+template <int DT, int R, int NT, int W = 0, bool WIDE = false, bool PIPE = false>
 __global__ __launch_bounds__(256) void k_wgrad(const typename Elt<DT>::T* __restrict__ x,
                                                const typename Elt<DT>::T* __restrict__ dy,
                                                const int32_t* __restrict__ perm, const int32_t* __restrict__ seg_ptr,
@@ -693,6 +884,10 @@ __global__ __launch_bounds__(256) void k_wgrad(const typename Elt<DT>::T* __rest
     } else {
         const int f = perm[i];
         const int* segp = seg_ptr + int64_t(i) * (g.m + 1);
+        if constexpr (PIPE) {
+            run_filter_pipe<DT, R>(g, c, segp, cin_idx, f, grp, lane, o);
+            return;
+        }
         int j = 0;
         for (int p = 0; p < g.m; ++p) {
             const int k1 = segp[p + 1];
@@ -782,6 +977,7 @@ __global__ __launch_bounds__(256) void k_bias_grad(const typename Elt<DT>::T* __
 
 constexpr int64_t kTargetWaves = 16384;   // 16 waves per SIMD
 constexpr int kWideRows = 2;              // rows per lane of the 4-column layout
+constexpr int64_t kPipeWaves = 3072;      // grid of the pipelined one-slot layout (3 waves per SIMD)
 constexpr int kMaxShares = 64;
 
 WGeo plan(int n, int cin, int cout, int h, int w, int64_t nk, bool dense, const PatTable* tab, int dtype) {
@@ -865,6 +1061,16 @@ WGeo plan(int n, int cin, int cout, int h, int w, int64_t nk, bool dense, const 
     // split the images into shares until the grid holds about kTargetWaves
     const int64_t per = cout > 0 ? (dense ? cin : (nk + cout - 1) / cout) : 0;
     const int64_t chunks = (per + kKC - 1) / kKC;
+    if (!dense && !g.rows && !g.wide && g.slots == 1 && cout > 0) {
+        // one slot: about kPipeWaves waves, each with at least 4 chunks to
+        // pipeline where the filters have that many
+        g.pipe = 1;
+        int64_t G = kPipeWaves / cout;
+        if (G > chunks / 4) G = chunks / 4;
+        g.G = int(G < 1 ? 1 : G);
+        g.KS = 1;
+        return g;
+    }
     int64_t G = cout > 0 ? kTargetWaves / cout : 1;
     if (G > chunks) G = chunks;
     g.G = int(G < 1 ? 1 : G);
@@ -900,6 +1106,19 @@ hipError_t run(const WGeo& g, const void* x, const void* dy, const int32_t* perm
         }
     }
 #undef PSC_WROWS
+    if constexpr (NT == 4) {
+        if (!done && g.pipe) {
+            if (g.H >= 8)
+                hipLaunchKernelGGL((k_wgrad<DT, 8, NT, 0, false, true>), grid, dim3(256), 0, stream,
+                                   static_cast<const T*>(x), static_cast<const T*>(dy), perm, seg_ptr, cin_idx, g,
+                                   dst);
+            else
+                hipLaunchKernelGGL((k_wgrad<DT, 4, NT, 0, false, true>), grid, dim3(256), 0, stream,
+                                   static_cast<const T*>(x), static_cast<const T*>(dy), perm, seg_ptr, cin_idx, g,
+                                   dst);
+            done = true;
+        }
+    }
     if (!done && g.wide) {
         hipLaunchKernelGGL((k_wgrad<DT, kWideRows, NT, 0, true>), grid, dim3(256), 0, stream,
                            static_cast<const T*>(x), static_cast<const T*>(dy), perm, seg_ptr, cin_idx, g, dst);

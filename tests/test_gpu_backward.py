@@ -46,6 +46,9 @@ SHAPES = [
     # per lane in the weight gradient): one to sixteen row bands per wave,
     # ragged last bands, a 63-lane segment
     (1, 3, 5, 6, 4), (3, 9, 7, 11, 32), (2, 6, 5, 7, 64), (1, 8, 4, 9, 224), (1, 3, 4, 5, 252),
+    # one band group per wave at batch 1 (the weight gradient pipelines a
+    # wave's chunks): full-size VGG-16 14x14 and ResNet-50 7x7 layers
+    (1, 512, 512, 14, 14), (1, 512, 512, 7, 7),
 ]
 
 
