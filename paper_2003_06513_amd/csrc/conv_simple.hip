@@ -75,10 +75,15 @@ __global__ __launch_bounds__(256) void k_conv_simple(const typename Elt<DT>::T* 
     y[(int64_t(n) * cout + f) * oplane + pix] = E::from_f(best);
 }
 
-// Dense comparator: a block computes a 16x16 output tile for 4 filters of
-// one image; input channels are staged through LDS with a 1-pixel halo.
-constexpr int kDT = 16;   // tile edge
-constexpr int kDF = 4;    // filters per block
+// Dense comparator (and the dense layer of the ADMM loop): a block computes
+// a 32x16 output tile (two rows per thread, ty and ty + 16) for 8 filters of
+// one image.  Input channels are staged through LDS 8 at a time with a
+// 1-pixel halo; the 8 weights of a (channel, tap) sit side by side, so two
+// 16-byte LDS reads (the same address in every lane) give them all: 16 FMAs
+// per 2 input reads and 2 weight reads.  Only the channels present are run.
+constexpr int kDTH = 32;  // tile rows
+constexpr int kDTW = 16;  // tile columns
+constexpr int kDF = 8;    // filters per block
 constexpr int kDC = 8;    // channels per stage
 
 template <int DT>
@@ -87,54 +92,66 @@ __global__ __launch_bounds__(256) void k_dense(const typename Elt<DT>::T* __rest
                                                int cout, const typename Elt<DT>::T* __restrict__ bias,
                                                int relu, typename Elt<DT>::T* __restrict__ y) {
     using E = Elt<DT>;
-    __shared__ float xs[kDC][kDT + 2][kDT + 2];
-    __shared__ float ws[kDF][kDC][9];
-    const int tiles_w = (W + kDT - 1) / kDT;
-    const int th0 = (blockIdx.x / tiles_w) * kDT, tw0 = (blockIdx.x % tiles_w) * kDT;
+    __shared__ float xs[kDC][kDTH + 2][kDTW + 2];
+    __shared__ __align__(16) float ws[kDC][9][kDF];
+    const int tiles_w = (W + kDTW - 1) / kDTW;
+    const int th0 = (blockIdx.x / tiles_w) * kDTH, tw0 = (blockIdx.x % tiles_w) * kDTW;
     const int f0 = blockIdx.y * kDF, n = blockIdx.z;
-    const int ty = threadIdx.x / kDT, tx = threadIdx.x % kDT;
+    const int ty = threadIdx.x / kDTW, tx = threadIdx.x % kDTW;
     const int plane = H * W;
     const typename E::T* xn = x + int64_t(n) * cin * plane;
-    float acc[kDF];
+    float acc0[kDF], acc1[kDF];
 #pragma unroll
-    for (int g = 0; g < kDF; ++g) acc[g] = 0.f;
+    for (int g = 0; g < kDF; ++g) acc0[g] = acc1[g] = 0.f;
     for (int c0 = 0; c0 < cin; c0 += kDC) {
-        for (int e = threadIdx.x; e < kDC * (kDT + 2) * (kDT + 2); e += 256) {
-            const int c = e / ((kDT + 2) * (kDT + 2));
-            const int r = (e / (kDT + 2)) % (kDT + 2);
-            const int s = e % (kDT + 2);
+        const int cn = cin - c0 < kDC ? cin - c0 : kDC;
+        for (int e = threadIdx.x; e < cn * (kDTH + 2) * (kDTW + 2); e += 256) {
+            const int c = e / ((kDTH + 2) * (kDTW + 2));
+            const int r = (e / (kDTW + 2)) % (kDTH + 2);
+            const int s = e % (kDTW + 2);
             const int ih = th0 + r - 1, iw = tw0 + s - 1;
             float v = 0.f;
-            if (c0 + c < cin && ih >= 0 && ih < H && iw >= 0 && iw < W)
-                v = E::load(xn, int64_t(c0 + c) * plane + ih * W + iw);
+            if (ih >= 0 && ih < H && iw >= 0 && iw < W) v = E::load(xn, int64_t(c0 + c) * plane + ih * W + iw);
             xs[c][r][s] = v;
         }
-        for (int e = threadIdx.x; e < kDF * kDC * 9; e += 256) {
-            const int g = e / (kDC * 9), c = (e / 9) % kDC, q = e % 9;
+        for (int e = threadIdx.x; e < cn * 9 * kDF; e += 256) {
+            const int c = e / (9 * kDF), q = (e / kDF) % 9, g = e % kDF;
             float v = 0.f;
-            if (f0 + g < cout && c0 + c < cin) v = E::load(wd, (int64_t(f0 + g) * cin + c0 + c) * 9 + q);
-            ws[g][c][q] = v;
+            if (f0 + g < cout) v = E::load(wd, (int64_t(f0 + g) * cin + c0 + c) * 9 + q);
+            ws[c][q][g] = v;
         }
         __syncthreads();
-        for (int c = 0; c < kDC; ++c)
+        for (int c = 0; c < cn; ++c)
 #pragma unroll
             for (int q = 0; q < 9; ++q) {
-                const float xv = xs[c][ty + q / 3][tx + q % 3];
+                const float x0 = xs[c][ty + q / 3][tx + q % 3];
+                const float x1 = xs[c][ty + 16 + q / 3][tx + q % 3];
+                const float4 wa = *reinterpret_cast<const float4*>(&ws[c][q][0]);
+                const float4 wb = *reinterpret_cast<const float4*>(&ws[c][q][4]);
+                const float wv[kDF] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
 #pragma unroll
-                for (int g = 0; g < kDF; ++g) acc[g] = fmaf(ws[g][c][q], xv, acc[g]);
+                for (int g = 0; g < kDF; ++g) {
+                    acc0[g] = fmaf(wv[g], x0, acc0[g]);
+                    acc1[g] = fmaf(wv[g], x1, acc1[g]);
+                }
             }
         __syncthreads();
     }
-    const int oh = th0 + ty, ow = tw0 + tx;
-    if (oh >= H || ow >= W) return;
+    const int ow = tw0 + tx;
+    if (ow >= W) return;
 #pragma unroll
-    for (int g = 0; g < kDF; ++g) {
-        const int f = f0 + g;
-        if (f >= cout) break;
-        float v = acc[g];
-        if (bias) v += E::load(bias, f);
-        if (relu) v = v > 0.f ? v : 0.f;
-        y[(int64_t(n) * cout + f) * plane + oh * W + ow] = E::from_f(v);
+    for (int half = 0; half < 2; ++half) {
+        const int oh = th0 + ty + 16 * half;
+        if (oh >= H) break;
+#pragma unroll
+        for (int g = 0; g < kDF; ++g) {
+            const int f = f0 + g;
+            if (f >= cout) break;
+            float v = half ? acc1[g] : acc0[g];
+            if (bias) v += E::load(bias, f);
+            if (relu) v = v > 0.f ? v : 0.f;
+            y[(int64_t(n) * cout + f) * plane + oh * W + ow] = E::from_f(v);
+        }
     }
 }
 
@@ -209,7 +226,7 @@ void describe_conv(const PatTable& tab, const ConvArgs& a, int algo, ConvForm& o
 
 hipError_t launch_dense(int dtype, const void* x, int n, int cin, int h, int w, const void* wd, int cout,
                         const void* bias, int relu, void* y, hipStream_t stream) {
-    const dim3 grid(unsigned(((h + kDT - 1) / kDT) * ((w + kDT - 1) / kDT)),
+    const dim3 grid(unsigned(((h + kDTH - 1) / kDTH) * ((w + kDTW - 1) / kDTW)),
                     unsigned((cout + kDF - 1) / kDF), unsigned(n));
     if (dtype == DT_F16)
         hipLaunchKernelGGL(k_dense<DT_F16>, grid, dim3(256), 0, stream, static_cast<const uint16_t*>(x), cin,
