@@ -19,16 +19,19 @@
 // band (a wave holds S bands of full rows separated by a zero lane, or a
 // column tile with one halo lane on each side), or, for widths that are
 // multiples of 4, 4 adjacent columns and R rows (each row one 16-byte fp32 /
-// 8-byte fp16 load).  Rows come through buffer
-// loads at offsets fixed per lane and row, the channel entering as a scalar
-// offset and padding reading zero; the left and right neighbour columns of x
-// are read by DPP inside the FMA.  The taps of a chunk are compiled for its
-// centre+3 shape (other masks dispatch each tap).  At the end of a chunk the
-// KC x 4 per-lane sums are added across the wave by a reduce-scatter (each
-// step halves the values a lane holds).  The chunks of a filter are dealt
-// round-robin to G waves; with several image shares the share sums go to a
-// workspace and a second kernel adds them in share order, so results do not
-// depend on scheduling.
+// 8-byte fp16 load), or, for small planes at large batch, one image row.
+// Rows come through buffer loads at offsets fixed per lane and row, the
+// channel entering as a scalar offset and padding reading zero; the left and
+// right neighbour columns of x are read by DPP inside the FMA.  The taps of a
+// chunk are compiled for its centre+3 shape (other masks dispatch each tap).
+// At the end of a chunk the KC x 4 per-lane sums are added across the wave
+// by a reduce-scatter (each step halves the values a lane holds).  The
+// chunks of a filter are dealt round-robin to G waves; when a wave has a
+// single band group, its chunks run as a pipeline (the next chunk's rows
+// load during the current one's FMAs and reduction).  With several image
+// shares the share sums go to a workspace and a second kernel adds them in
+// share order, so results do not depend on scheduling; the bias gradient is
+// summed in parts that are added the same way.
 #include "common.h"
 #include "launch.h"
 #include "conv_rows.h"
