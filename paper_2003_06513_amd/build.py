@@ -55,8 +55,11 @@ def build(verbose: bool = False, incremental: bool = False) -> str:
     object, counting the headers) and link libpsc.so."""
     os.makedirs(OUT_DIR, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
-    # the largest translation units first, so the pool finishes early
-    srcs.sort(key=lambda f: -os.path.getsize(f) - (1 << 20) * f.endswith("_r8.hip"))
+    # the slowest translation units first, so the pool finishes early: the
+    # pipelined weight-gradient units (small files over a large header), then
+    # the largest files
+    srcs.sort(key=lambda f: -os.path.getsize(f) - (1 << 20) * f.endswith("_r8.hip")
+              - (1 << 21) * os.path.basename(f).startswith("wgrad_pipe"))
     with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
         objs = list(ex.map(lambda s: _compile(s, incremental), srcs))
     tmp = LIB + ".tmp%d" % os.getpid()
