@@ -216,8 +216,8 @@ def form_cases():
         # every segment count from 3 to 8 per wave
         for n, cin, cout, h, w, pool in ((64, 5, 1024, 5, 28, False), (40, 3, 1024, 6, 32, False),
                                          (16, 4, 1024, 7, 56, False), (16, 3, 1024, 8, 56, True),
-                                         (12, 3, 2048, 4, 64, False)):
-            if dt == B.PSC_F32 and w == 64:
+                                         (12, 3, 2048, 4, 64, False), (4, 3, 1024, 7, 252, False)):
+            if dt == B.PSC_F32 and w in (64, 252):
                 continue
             L = B.Layer(cout, cin, list(FORM_MASKS), cin * cout // 2, dt)
             cfg = B.conv3x3_config(L, dt, n, h, w, pool, 1, 0)

@@ -72,7 +72,7 @@ def test_form_search_reaches_every_form():
     wide = [c for c in cases if c[0][0] == "wide"]
     assert all(c[0][1] == 1 and c[0][2] == 4 for c in wide)
     assert {(c[6], c[5]) for c in wide} == {(B.PSC_F32, 28), (B.PSC_F32, 32), (B.PSC_F32, 56), (B.PSC_F16, 28),
-                                           (B.PSC_F16, 32), (B.PSC_F16, 56), (B.PSC_F16, 64)}
+                                           (B.PSC_F16, 32), (B.PSC_F16, 56), (B.PSC_F16, 64), (B.PSC_F16, 252)}
     assert any(c[7] for c in wide if c[6] == B.PSC_F16) and any(c[7] for c in wide if c[6] == B.PSC_F32)
     rows = [c for c in cases if c[0][0] == "rows"]
     assert all(c[0][1] == 4 for c in rows)
