@@ -581,9 +581,9 @@ def measure_ceilings():
                    "HIP graph"}
 
 
-def write_jsonl(path, configs):
+def write_jsonl(path, results):
     with open(path, "w") as f:
-        for name, res in configs.items():
+        for name, res in results.items():
             bw = {r["layer"]: r for r in res.get("backward", {}).get("layers", [])}
             for r in res["layer_detail"]:
                 row = {"workload": name, "batch": res["batch"], "dtype": res["dtype"]}
@@ -653,13 +653,13 @@ def main():
         names = [n for n in args.configs.split(",") if n]
     if head.name not in names:
         names.insert(0, head.name)
-    configs, roofs = {}, {}
+    results, roofs = {}, {}
     for name in names:
         print("[bench] %s" % name, file=sys.stderr, flush=True)
         _, res, roof = measure(find_workload(name), args, name == head.name)
-        configs[name] = res
+        results[name] = res
         roofs[name] = roof
-    hr = configs[head.name]
+    hr = results[head.name]
     line = {
         "metric": METRIC, "value": hr["nz_gflops"], "unit": "GFLOP/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": hr["ms_per_step"],
@@ -682,7 +682,7 @@ def main():
         line["roofline"]["measured_fma_tflops"] = meas
         line["roofline"]["frac_of_measured_fma"] = round(line["roofline"]["achieved"] / meas, 4)
     line["configs"] = {}
-    for name, res in configs.items():
+    for name, res in results.items():
         c = {k: v for k, v in res.items() if k not in ("layer_detail", "cpu_baseline", "backward")}
         if "backward" in res:
             c["backward"] = {k: v for k, v in res["backward"].items() if k != "layers"}
@@ -704,9 +704,9 @@ def main():
     print(json.dumps(line), flush=True)
     if args.details:
         with open(args.details, "w") as f:
-            json.dump({"line": line, "configs": configs}, f, indent=1)
+            json.dump({"line": line, "configs": results}, f, indent=1)
     if args.jsonl:
-        write_jsonl(args.jsonl, configs)
+        write_jsonl(args.jsonl, results)
 
 
 if __name__ == "__main__":
