@@ -330,9 +330,11 @@ psc_status psc_conv3x3_config(const psc_layer *layer, int32_t act_dtype, int32_t
                               int32_t h, int32_t w, int32_t pool, int32_t stride,
                               int32_t algo, psc_conv_config *out);
 
-/* Comparator: the dense 3x3 convolution (stride 1, pad 1) of dense OIHW
- * weights d_w [cout][cin][3][3] on the vector ALUs, same conventions and
- * accumulation as psc_conv3x3_fwd. */
+/* Comparator, and the dense layer of the ADMM loop: the dense 3x3
+ * convolution (stride 1, pad 1) of dense OIHW weights d_w [cout][cin][3][3],
+ * same conventions as psc_conv3x3_fwd, fp32 accumulation (fp16 inputs
+ * widened exactly).  Layers of more than 8 input channels run on the matrix
+ * cores (fp32 MFMA), the others on the vector ALUs. */
 psc_status psc_dense3x3_fwd(int32_t dtype, const void *d_x, int32_t n, int32_t cin,
                             int32_t h, int32_t w, const void *d_w, int32_t cout,
                             const void *d_bias, int32_t relu, void *d_y, void *stream);

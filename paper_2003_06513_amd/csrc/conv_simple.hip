@@ -75,9 +75,11 @@ __global__ __launch_bounds__(256) void k_conv_simple(const typename Elt<DT>::T* 
     y[(int64_t(n) * cout + f) * oplane + pix] = E::from_f(best);
 }
 
-// Dense comparator (and the dense layer of the ADMM loop): a block computes
-// a 32x16 output tile (two rows per thread, ty and ty + 16) for 8 filters of
-// one image.  Input channels are staged through LDS 8 at a time with a
+// The dense 3x3 convolution of layers with at most 8 input channels (one
+// LDS stage: K = 9 cin <= 72 leaves the matrix cores idle and the layer is
+// bound by writing its output), on the vector ALUs: a block computes a 32x16
+// output tile (two rows per thread, ty and ty + 16) for 8 filters of one
+// image.  Input channels are staged through LDS 8 at a time with a
 // 1-pixel halo; the 8 weights of a (channel, tap) sit side by side, so two
 // 16-byte LDS reads (the same address in every lane) give them all: 16 FMAs
 // per 2 input reads and 2 weight reads.  Only the channels present are run.
@@ -155,6 +157,173 @@ __global__ __launch_bounds__(256) void k_dense(const typename Elt<DT>::T* __rest
     }
 }
 
+// The dense 3x3 convolution of layers with more than 8 input channels on the
+// matrix cores: an implicit GEMM with M = filters, N = output pixels
+// and K = (input channel, tap), k = 9c + q, computed by fp32 MFMA
+// 16x16x4 (fp16 inputs are widened exactly, so both dtypes accumulate in
+// fp32).  A block owns 64 filters and a 4x16 pixel tile of one image; each
+// of its 4 waves owns 32 filters x 32 pixels (two tile rows), i.e. 2 x 2
+// MFMA tiles of 16 x 16, so 16 lanes of a result register hold 16 adjacent
+// pixels of one row (64-byte stores).  Input channels are staged through LDS
+// 8 at a time: the 6x18 input tile with its 1-pixel halo and the weights
+// transposed to [k][f].  Per K step of 4 a lane reads 2 weights and 2 inputs
+// from LDS and the wave issues 4 MFMAs.  The next stage's inputs and weights
+// load into registers while the current stage computes, and each step's
+// LDS operands load while the previous step's MFMAs issue.
+//
+// Operand layout of v_mfma_f32_16x16x4_f32: lane l supplies A[l % 16][l / 16]
+// and B[l / 16][l % 16]; the result element D[i][j] sits in lane
+// j + 16 (i / 4), register i % 4.
+constexpr int kMTR = 4;          // output tile rows
+constexpr int kMTC = 16;         // output tile columns
+constexpr int kMXR = kMTR + 2;   // input tile rows and columns with the halo
+constexpr int kMXC = kMTC + 2;
+constexpr int kMF = 64;          // filters per block
+constexpr int kMC = 8;           // channels per stage
+constexpr int kMK = kMC * 9;     // K per stage
+constexpr int kMWS = 65;         // LDS row stride (floats) of the weight tile
+
+typedef float psc_mf4 __attribute__((ext_vector_type(4)));
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_dense_mfma(const typename Elt<DT>::T* __restrict__ x, int cin, int H,
+                                                    int W, const typename Elt<DT>::T* __restrict__ wd, int cout,
+                                                    const typename Elt<DT>::T* __restrict__ bias, int relu,
+                                                    typename Elt<DT>::T* __restrict__ y) {
+    using E = Elt<DT>;
+    __shared__ float xs[kMC * kMXR * kMXC];
+    __shared__ float ws[(kMK + 4) * kMWS];
+    const int tiles_w = (W + kMTC - 1) / kMTC;
+    const int th0 = (blockIdx.x / tiles_w) * kMTR, tw0 = (blockIdx.x % tiles_w) * kMTC;
+    const int f0 = blockIdx.y * kMF, n = blockIdx.z;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int fw = (wave >> 1) * 32, pw = (wave & 1) * 32;     // the wave's first filter and pixel
+    const int li = lane & 15, kq = lane >> 4;
+    const int plane = H * W;
+    // LDS offset of the top-left halo position of this lane's two B pixels
+    int pix[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        const int p = pw + 16 * t + li;
+        pix[t] = (p / kMTC) * kMXC + p % kMTC;
+    }
+    psc_mf4 acc[2][2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) acc[a][b] = psc_mf4{0.f, 0.f, 0.f, 0.f};
+
+    // A stage's inputs and weights pass through registers: thread t holds
+    // input tile elements t + 256 j and weight elements t + 256 j of the
+    // [f][k] (k < kMK) tile, loaded while the previous stage computes.  The
+    // loads go through buffer descriptors: a per-thread 32-bit offset that
+    // does not depend on the stage, the stage as a scalar offset, and
+    // elements outside the image, the stage or the filters at an offset past
+    // the range, which reads zero.
+    constexpr int ESZ = int(sizeof(typename E::T));
+    constexpr int kXS = kMC * kMXR * kMXC;           // 864
+    constexpr int kXJ = (kXS + 255) / 256;           // 4
+    constexpr int kWJ = kMF * kMK / 256;             // 18
+    static_assert(kMF * kMK % 256 == 0, "weight tile elements per thread");
+    const auto xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<typename E::T*>(x), int16_t(0),
+                                                      int(int64_t(gridDim.z) * cin * plane * ESZ), 0x00020000);
+    const auto wr = __builtin_amdgcn_make_buffer_rsrc(const_cast<typename E::T*>(wd), int16_t(0),
+                                                      int(int64_t(cout) * cin * 9 * ESZ), 0x00020000);
+    auto ld = [&](__amdgpu_buffer_rsrc_t rs, uint32_t vo, int so) -> float {
+        if constexpr (DT == DT_F32)
+            return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, int(vo), so, 0));
+        else
+            return float(__builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(rs, int(vo), so, 0)));
+    };
+    float rx[kXJ], rw[kWJ];
+    auto fetch = [&](int c0) {
+        const int cn = cin - c0 < kMC ? cin - c0 : kMC;
+#pragma unroll
+        for (int j = 0; j < kXJ; ++j) {
+            const int e = threadIdx.x + 256 * j;
+            const int c = e / (kMXR * kMXC), r = (e / kMXC) % kMXR, sx = e % kMXC;
+            const int ih = th0 + r - 1, iw = tw0 + sx - 1;
+            const bool in = c < cn && ih >= 0 && ih < H && iw >= 0 && iw < W;
+            const uint32_t vo = in ? uint32_t(((n * cin + c) * plane + ih * W + iw) * ESZ) : 0x80000000u;
+            rx[j] = ld(xr, vo, c0 * plane * ESZ);
+        }
+#pragma unroll
+        for (int j = 0; j < kWJ; ++j) {
+            const int e = threadIdx.x + 256 * j;
+            const int f = e / kMK, k = e % kMK;
+            const bool in = k < cn * 9 && f0 + f < cout;
+            const uint32_t vo = in ? uint32_t(((f0 + f) * cin * 9 + k) * ESZ) : 0x80000000u;
+            rw[j] = ld(wr, vo, c0 * 9 * ESZ);
+        }
+    };
+    // the operands of one K step of 4 (k = 4 st + lane / 16): 2 weights and
+    // 2 inputs from LDS; past kc a zero weight and a zero input (the address
+    // stays inside the tile, whatever the select compiles to)
+    auto operands = [&](int st, int kc, float (&o)[4]) {
+        const int k = 4 * st + kq;
+        const int c = k / 9, q = k - 9 * c;
+        const bool valid = k < kc;
+        const int xo = valid ? c * (kMXR * kMXC) + (q / 3) * kMXC + q % 3 : 0;
+        o[0] = ws[k * kMWS + fw + li];
+        o[1] = ws[k * kMWS + fw + 16 + li];
+        o[2] = valid ? xs[xo + pix[0]] : 0.f;
+        o[3] = valid ? xs[xo + pix[1]] : 0.f;
+    };
+    auto mfma4 = [&](const float (&o)[4]) {
+        acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(o[0], o[2], acc[0][0], 0, 0, 0);
+        acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(o[0], o[3], acc[0][1], 0, 0, 0);
+        acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(o[1], o[2], acc[1][0], 0, 0, 0);
+        acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(o[1], o[3], acc[1][1], 0, 0, 0);
+    };
+
+    fetch(0);
+    for (int c0 = 0; c0 < cin; c0 += kMC) {
+        const int cn = cin - c0 < kMC ? cin - c0 : kMC;
+#pragma unroll
+        for (int j = 0; j < kXJ; ++j) {
+            const int e = threadIdx.x + 256 * j;
+            if (e < kXS) xs[e] = rx[j];
+        }
+#pragma unroll
+        for (int j = 0; j < kWJ; ++j) {
+            const int e = threadIdx.x + 256 * j;
+            ws[(e % kMK) * kMWS + e / kMK] = rw[j];
+        }
+        __syncthreads();
+        if (c0 + kMC < cin) fetch(c0 + kMC);   // in flight during this stage's MFMAs
+        // the operands of step st + 1 load while step st's MFMAs issue
+        const int kc = cn * 9, steps = (kc + 3) / 4;
+        float oa[4], ob[4];
+        operands(0, kc, oa);
+        int st = 0;
+        for (; st + 2 <= steps; st += 2) {
+            operands(st + 1, kc, ob);
+            mfma4(oa);
+            if (st + 2 < steps) operands(st + 2, kc, oa);
+            mfma4(ob);
+        }
+        if (st < steps) mfma4(oa);
+        __syncthreads();
+    }
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int f = f0 + fw + 16 * a + 4 * kq + r;
+            if (f >= cout) continue;
+            const float bv = bias ? E::load(bias, f) : 0.f;
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const int p = pw + 16 * b + li;
+                const int oh = th0 + p / kMTC, ow = tw0 + p % kMTC;
+                if (oh >= H || ow >= W) continue;
+                float v = acc[a][b][r] + bv;
+                if (relu) v = v > 0.f ? v : 0.f;
+                y[(int64_t(n) * cout + f) * plane + oh * W + ow] = E::from_f(v);
+            }
+        }
+}
+
 template <int DT>
 __global__ __launch_bounds__(256) void k_maxpool(const typename Elt<DT>::T* __restrict__ x, int64_t total,
                                                  int H, int W, typename Elt<DT>::T* __restrict__ y) {
@@ -226,15 +395,33 @@ void describe_conv(const PatTable& tab, const ConvArgs& a, int algo, ConvForm& o
 
 hipError_t launch_dense(int dtype, const void* x, int n, int cin, int h, int w, const void* wd, int cout,
                         const void* bias, int relu, void* y, hipStream_t stream) {
-    const dim3 grid(unsigned(((h + kDTH - 1) / kDTH) * ((w + kDTW - 1) / kDTW)),
-                    unsigned((cout + kDF - 1) / kDF), unsigned(n));
+    // the matrix-core kernel addresses x and the weights through 32-bit
+    // buffer offsets
+    const int esz = dtype == DT_F16 ? 2 : 4;
+    const bool small = int64_t(n) * cin * h * w * esz < (int64_t(1) << 31) &&
+                       int64_t(cout) * cin * 9 * esz < (int64_t(1) << 31);
+    if (cin <= kDC || !small) {
+        const dim3 grid(unsigned(((h + kDTH - 1) / kDTH) * ((w + kDTW - 1) / kDTW)),
+                        unsigned((cout + kDF - 1) / kDF), unsigned(n));
+        if (dtype == DT_F16)
+            hipLaunchKernelGGL(k_dense<DT_F16>, grid, dim3(256), 0, stream, static_cast<const uint16_t*>(x), cin,
+                               h, w, static_cast<const uint16_t*>(wd), cout,
+                               static_cast<const uint16_t*>(bias), relu, static_cast<uint16_t*>(y));
+        else
+            hipLaunchKernelGGL(k_dense<DT_F32>, grid, dim3(256), 0, stream, static_cast<const float*>(x), cin,
+                               h, w, static_cast<const float*>(wd), cout, static_cast<const float*>(bias), relu,
+                               static_cast<float*>(y));
+        return hipGetLastError();
+    }
+    const dim3 grid(unsigned(((h + kMTR - 1) / kMTR) * ((w + kMTC - 1) / kMTC)),
+                    unsigned((cout + kMF - 1) / kMF), unsigned(n));
     if (dtype == DT_F16)
-        hipLaunchKernelGGL(k_dense<DT_F16>, grid, dim3(256), 0, stream, static_cast<const uint16_t*>(x), cin,
-                           h, w, static_cast<const uint16_t*>(wd), cout,
-                           static_cast<const uint16_t*>(bias), relu, static_cast<uint16_t*>(y));
+        hipLaunchKernelGGL(k_dense_mfma<DT_F16>, grid, dim3(256), 0, stream, static_cast<const uint16_t*>(x), cin,
+                           h, w, static_cast<const uint16_t*>(wd), cout, static_cast<const uint16_t*>(bias), relu,
+                           static_cast<uint16_t*>(y));
     else
-        hipLaunchKernelGGL(k_dense<DT_F32>, grid, dim3(256), 0, stream, static_cast<const float*>(x), cin, h,
-                           w, static_cast<const float*>(wd), cout, static_cast<const float*>(bias), relu,
+        hipLaunchKernelGGL(k_dense_mfma<DT_F32>, grid, dim3(256), 0, stream, static_cast<const float*>(x), cin,
+                           h, w, static_cast<const float*>(wd), cout, static_cast<const float*>(bias), relu,
                            static_cast<float*>(y));
     return hipGetLastError();
 }

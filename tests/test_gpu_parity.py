@@ -207,7 +207,11 @@ def test_conv_deterministic_and_in_bounds():
 
 # ---------------------------------------------------------------- comparators
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
-@pytest.mark.parametrize("shape", [(1, 3, 8, 5, 5), (2, 20, 17, 19, 23), (1, 64, 64, 32, 32)])
+@pytest.mark.parametrize("shape", [(1, 3, 8, 5, 5), (2, 20, 17, 19, 23), (1, 64, 64, 32, 32),
+                                   # the matrix-core tiles: 64 filters x 8x8 pixels, 8 channels a stage
+                                   (1, 13, 70, 9, 11), (2, 130, 96, 16, 24), (1, 9, 65, 7, 33),
+                                   # at most 8 channels: the vector-ALU tile kernel
+                                   (1, 3, 64, 40, 36), (3, 1, 1, 1, 1)])
 def test_dense_comparator(shape, dtype):
     torch = torch_mod()
     n, cin, cout, h, w = shape
