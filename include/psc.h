@@ -279,9 +279,12 @@ psc_status psc_admm_residual(const float *d_z, const float *d_target, int64_t nu
 /* The dense weight gradient of the 3x3 layer (stride 1, zero padding 1):
  *   d_dw[o][i][r][s] = sum over images and pixels of
  *                      g[n, o, h, w] * x[n, i, h + r - 1, w + s - 1]
- * and, if d_db is non-NULL, d_db[o] = sum of g[n, o, :, :]; fp32.  Workspace
- * as for psc_conv3x3_bwd_weight (psc_dense3x3_bwd_weight_workspace bytes);
- * x and g of more than 2 GiB each return PSC_ERR_UNSUPPORTED. */
+ * and, if d_db is non-NULL, d_db[o] = sum of g[n, o, :, :]; fp32.  Layers of
+ * at least 16 input channels run on the matrix cores (fp32 MFMA), the others
+ * on the vector ALUs; partial sums are added in a fixed order, so results
+ * are deterministic.  Workspace as for psc_conv3x3_bwd_weight
+ * (psc_dense3x3_bwd_weight_workspace bytes); x and g of more than 2 GiB
+ * each return PSC_ERR_UNSUPPORTED. */
 psc_status psc_dense3x3_bwd_weight_workspace(int32_t n, int32_t cin, int32_t h, int32_t w,
                                              int32_t cout, size_t *bytes);
 psc_status psc_dense3x3_bwd_weight(const float *d_x, const float *d_g, int32_t n, int32_t cin,

@@ -95,6 +95,19 @@ hipError_t launch_admm_residual(const float* z, const float* t, int64_t numel, f
                                 double* loss, void* ws, hipStream_t stream);
 hipError_t launch_dense_wgrad(const float* x, const float* g, int n, int cin, int h, int w, int cout, float* dw,
                               float* db, void* ws, hipStream_t stream);
+// The dense weight gradient on the matrix cores (layers of at least 16 input
+// channels): blocks of 64 filters x 16 channels, the 4x16 pixel tiles split
+// over KS blocks with KS partial-sum slots in the workspace.
+struct DenseWPlan {
+    int fb, cb;             // filter and channel blocks
+    int tiles_w, tiles_img; // pixel tiles per image row of tiles, per image
+    int64_t tiles;          // pixel tiles in all
+    int KS;                 // blocks the tiles are split over
+};
+bool dense_wgrad_mfma_plan(int n, int cin, int cout, int h, int w, DenseWPlan* p);
+size_t dense_wgrad_mfma_workspace(const DenseWPlan& p, int cin, int cout);
+hipError_t launch_dense_wgrad_mfma(const DenseWPlan& p, const float* x, const float* g, int n, int cin, int h,
+                                   int w, int cout, float* dst, hipStream_t stream);
 hipError_t launch_admm_primal(float* w, const float* dw, const float* a, const float* d, int64_t nw, float* b,
                               const float* db, int cout, float lr, float rho, float* v, hipStream_t stream);
 hipError_t launch_admm_dual(const PatTable& tab, const float* v, const uint8_t* pat, const uint8_t* keep, int64_t nk,

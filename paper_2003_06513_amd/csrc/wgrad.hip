@@ -295,9 +295,12 @@ static size_t wgrad_part_bytes(const WGeo& g, int64_t nk, bool dense) {
 
 size_t wgrad_workspace_bytes(int n, int cin, int cout, int h, int w, int64_t nk, bool dense) {
     if (n <= 0) return 0;
-    const WGeo g = plan(n, cin, cout, h, w, nk, dense, nullptr, DT_F32);
     const int P = bias_parts(n, h * w);
-    return wgrad_part_bytes(g, nk, dense) + (P > 1 ? size_t(P) * size_t(cout) * sizeof(float) : 0);
+    const size_t bias_bytes = P > 1 ? size_t(P) * size_t(cout) * sizeof(float) : 0;
+    DenseWPlan dp;
+    if (dense && dense_wgrad_mfma_plan(n, cin, cout, h, w, &dp)) return dense_wgrad_mfma_workspace(dp, cin, cout) + bias_bytes;
+    const WGeo g = plan(n, cin, cout, h, w, nk, dense, nullptr, DT_F32);
+    return wgrad_part_bytes(g, nk, dense) + bias_bytes;
 }
 
 hipError_t launch_bwd_weight(const PatTable& tab, const PackedView& pk, int dtype, int n, int cin, int h, int w,
@@ -315,11 +318,27 @@ hipError_t launch_bwd_weight(const PatTable& tab, const PackedView& pk, int dtyp
 
 hipError_t launch_dense_wgrad(const float* x, const float* g_, int n, int cin, int h, int w, int cout, float* dw,
                               float* db, void* ws, hipStream_t stream) {
-    const WGeo g = plan(n, cin, cout, h, w, int64_t(cout) * cin, true, nullptr, DT_F32);
-    hipError_t e = run<DT_F32, 9>(g, x, g_, nullptr, nullptr, nullptr, dw, ws, stream);
+    hipError_t e;
+    size_t part_bytes;
+    DenseWPlan dp;
+    if (dense_wgrad_mfma_plan(n, cin, cout, h, w, &dp)) {
+        // matrix cores: KS slots of partial sums, added in slot order
+        part_bytes = dense_wgrad_mfma_workspace(dp, cin, cout);
+        e = launch_dense_wgrad_mfma(dp, x, g_, n, cin, h, w, cout, dp.KS > 1 ? static_cast<float*>(ws) : dw, stream);
+        if (e == hipSuccess && dp.KS > 1) {
+            const int64_t ne = int64_t(cout) * cin * 9;
+            const int64_t gb = (ne + 255) / 256;
+            hipLaunchKernelGGL(k_wgrad_reduce, dim3(unsigned(gb > 8192 ? 8192 : gb)), dim3(256), 0, stream,
+                               static_cast<const float*>(ws), dp.KS, ne, dw);
+            e = hipGetLastError();
+        }
+    } else {
+        const WGeo g = plan(n, cin, cout, h, w, int64_t(cout) * cin, true, nullptr, DT_F32);
+        part_bytes = wgrad_part_bytes(g, int64_t(cout) * cin, true);
+        e = run<DT_F32, 9>(g, x, g_, nullptr, nullptr, nullptr, dw, ws, stream);
+    }
     if (e != hipSuccess || !db) return e;
-    float* bpart =
-        ws ? reinterpret_cast<float*>(static_cast<char*>(ws) + wgrad_part_bytes(g, int64_t(cout) * cin, true)) : nullptr;
+    float* bpart = ws ? reinterpret_cast<float*>(static_cast<char*>(ws) + part_bytes) : nullptr;
     return bias_grad<DT_F32>(g_, n, cout, h * w, db, bpart, stream);
 }
 

@@ -78,6 +78,9 @@ CASES = [
     # cout, cin, h, w, T, m, drop
     (8, 3, 9, 11, 2, 4, 0), (12, 10, 7, 6, 3, 6, 50), (16, 24, 14, 14, 2, 8, 60), (5, 7, 1, 1, 4, 8, 30),
     (20, 6, 5, 70, 2, 8, 40), (6, 5, 9, 12, 2, 6, 40), (4, 3, 6, 28, 3, 8, 50),
+    # the matrix-core weight gradient: 16-channel blocks, 64-filter blocks,
+    # ragged pixel tiles, partial sums over several blocks
+    (70, 40, 9, 17, 2, 8, 50), (16, 16, 4, 5, 3, 4, 30),
 ]
 
 
