@@ -199,6 +199,79 @@ __global__ __launch_bounds__(256) void k_sel_mark(const uint64_t* __restrict__ k
     }
 }
 
+// The whole selection in one workgroup of 1024 threads, for layers of at
+// most kSelOneBlockMax kernels, where the passes above would be bound by
+// their 19 launches: the same 8 radix passes (histogram of the keys that
+// match the digits found so far, then the digit by the same scan from the
+// top), then the same index-ordered rank of the keys equal to the threshold
+// -- each thread owns a contiguous run of indices -- so the keep mask is the
+// same bit for bit.
+constexpr int64_t kSelOneBlockMax = 65536;
+
+__global__ __launch_bounds__(1024) void k_sel_one(const uint64_t* __restrict__ keys, int64_t n, int64_t keep,
+                                                  uint8_t* __restrict__ out) {
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t part[1024];
+    __shared__ uint64_t s_prefix, s_mask;
+    __shared__ int64_t s_rem;
+    const int t = threadIdx.x;
+    if (t == 0) {
+        s_prefix = 0;
+        s_mask = 0;
+        s_rem = keep;
+    }
+    for (int shift = 56; shift >= 0; shift -= 8) {
+        if (t < 256) hist[t] = 0;
+        __syncthreads();
+        const uint64_t prefix = s_prefix, mask = s_mask;
+        for (int64_t i = t; i < n; i += 1024) {
+            const uint64_t key = keys[i];
+            if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        if (t == 0) {
+            const int64_t r = s_rem;
+            int64_t above = 0;
+            int d = 255;
+            for (; d > 0; --d) {
+                const int64_t c = hist[d];
+                if (above + c >= r) break;
+                above += c;
+            }
+            s_rem = r - above;
+            s_prefix = prefix | (uint64_t(d) << shift);
+            s_mask = mask | (uint64_t(255) << shift);
+        }
+        __syncthreads();
+    }
+    const uint64_t T = s_prefix;
+    const int64_t r = s_rem;
+    const int64_t per = (n + 1023) / 1024;
+    const int64_t beg = min<int64_t>(n, t * per), end = min<int64_t>(n, beg + per);
+    uint32_t c = 0;
+    for (int64_t i = beg; i < end; ++i) c += keys[i] == T ? 1u : 0u;
+    part[t] = c;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+        const uint32_t v = t >= off ? part[t - off] : 0u;
+        __syncthreads();
+        part[t] += v;
+        __syncthreads();
+    }
+    int64_t rank = int64_t(part[t] - c);
+    for (int64_t i = beg; i < end; ++i) {
+        const uint64_t key = keys[i];
+        uint8_t v = 0;
+        if (key > T) {
+            v = 1;
+        } else if (key == T) {
+            v = rank < r ? 1 : 0;
+            ++rank;
+        }
+        out[i] = v;
+    }
+}
+
 __global__ __launch_bounds__(256) void k_fill_u8(uint8_t* __restrict__ p, int64_t n, uint8_t v) {
     for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n; i += int64_t(gridDim.x) * 256) p[i] = v;
 }
@@ -421,6 +494,11 @@ hipError_t launch_select(int64_t n, int64_t keep, const double* energy, uint8_t*
     if (keep == 0 || keep == n) {
         hipLaunchKernelGGL(k_fill_u8, dim3(grid_for(n, 256, 4096)), dim3(256), 0, stream, keep_out, n,
                            uint8_t(keep == n ? 1 : 0));
+        return hipGetLastError();
+    }
+    if (n <= kSelOneBlockMax) {
+        hipLaunchKernelGGL(k_sel_one, dim3(1), dim3(1024), 0, stream, reinterpret_cast<const uint64_t*>(energy), n,
+                           keep, keep_out);
         return hipGetLastError();
     }
     char* base = static_cast<char*>(ws);

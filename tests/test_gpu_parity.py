@@ -62,6 +62,10 @@ def test_prepare_adversarial_ties():
     # equal-magnitude neighbours with mixed signs
     k = np.array([[1, -1, 1], [-1, 2, 1], [1, 1, -1]], dtype=np.float16)
     cases.append((np.tile(k, (9, 11, 1, 1)), 8, 60))
+    # many ties at both sizes of the selection: 65536 kernels (one
+    # workgroup) and 76800 (the multi-block passes)
+    cases.append((rng.integers(-2, 3, size=(256, 256, 3, 3)).astype(np.float32), 8, 55))
+    cases.append((rng.integers(-2, 3, size=(300, 256, 3, 3)).astype(np.float32), 8, 55))
     for w, m, drop in cases:
         cout, cin = w.shape[:2]
         masks = oracle.select_library(w, m)
