@@ -48,6 +48,7 @@ METRIC = "nonzero-MAC GFLOP/s + ms/layer, pattern-sparse 3x3 conv fwd, batch 1 a
 # non-packed v_fmac_f32 (the library is compiled with packed fp32 disabled); the measured
 # ceilings in the bench line give the rate that instruction reaches here.
 PEAK_VALU_TFLOPS = 157.3
+PEAK_MFMA_F32_TFLOPS = 157.3   # MI355X published dense fp32 matrix peak (the same figure)
 PEAK_HBM_GBS = 8000.0
 DEFAULT_CONFIGS = "vgg16_224_b1_f32,resnet50_3x3_b1_f16,resnet50_3x3_b32_f16"
 
@@ -434,8 +435,8 @@ def measure_admm(wl, iters=10, parts=True):
             "ms": {k: round(v, 4) for k, v in parts.items()},
             "dense_fwd_tflops": round(dense_fl / (parts["dense_fwd"] * 1e-3) / 1e12, 3),
             "dense_wgrad_tflops": round(dense_fl / (parts["dense_wgrad"] * 1e-3) / 1e12, 3),
-            "dense_fwd_roofline_frac": round(dense_fl / (parts["dense_fwd"] * 1e-3) / 1e12 / PEAK_VALU_TFLOPS, 4),
-            "dense_wgrad_roofline_frac": round(dense_fl / (parts["dense_wgrad"] * 1e-3) / 1e12 / PEAK_VALU_TFLOPS, 4)}
+            "dense_fwd_roofline_frac": round(dense_fl / (parts["dense_fwd"] * 1e-3) / 1e12 / PEAK_MFMA_F32_TFLOPS, 4),
+            "dense_wgrad_roofline_frac": round(dense_fl / (parts["dense_wgrad"] * 1e-3) / 1e12 / PEAK_MFMA_F32_TFLOPS, 4)}
 
 
 def conv_sources_digest():
@@ -519,7 +520,8 @@ def measure(wl, args, headline):
 def measure_ceilings():
     """Measured ceilings beside the published ones: the fp32 FMA rate of the
     vector ALUs as the library issues it (psc_probe_fma: v_fmac_f32, packed
-    fp32 disabled), the HBM bandwidth of a 1 GiB device copy (read + write
+    fp32 disabled), the fp32 matrix-core rate of the dense kernels'
+    instruction (psc_probe_mfma), the HBM bandwidth of a 1 GiB device copy (read + write
     bytes), and the launch latency of a tiny library kernel, eager and as a
     HIP graph replay."""
     import torch
@@ -536,6 +538,15 @@ def measure_ceilings():
     e.record()
     torch.cuda.synchronize()
     fma_tflops = 2.0 * 8 * iters * blocks * 256 * reps / (s.elapsed_time(e) * 1e-3) / 1e12
+    mblocks, miters = 4096, 4000
+    for _ in range(2):
+        B.probe_mfma(mblocks, miters, out)
+    s.record()
+    for _ in range(reps):
+        B.probe_mfma(mblocks, miters, out)
+    e.record()
+    torch.cuda.synchronize()
+    mfma_tflops = 32768.0 * miters * mblocks * reps / (s.elapsed_time(e) * 1e-3) / 1e12
     a = torch.ones(256 << 20, dtype=torch.float32, device="cuda")
     b = torch.empty_like(a)
     b.copy_(a)
@@ -574,9 +585,12 @@ def measure_ceilings():
     graph_us = s.elapsed_time(e) * 1e3 / n
     return {"valu_fp32_fma_tflops": round(fma_tflops, 2),
             "valu_fp32_fma_frac_of_peak": round(fma_tflops / PEAK_VALU_TFLOPS, 3),
+            "mfma_fp32_tflops": round(mfma_tflops, 2),
+            "mfma_fp32_frac_of_peak": round(mfma_tflops / PEAK_MFMA_F32_TFLOPS, 3),
             "hbm_copy_gbs": round(copy_gbs, 1), "hbm_copy_frac_of_8000": round(copy_gbs / 8000.0, 3),
             "launch_us_eager": round(eager_us, 2), "launch_us_graph": round(graph_us, 2),
-            "how": "psc_probe_fma 4096x256 lanes x 8 chains x 20000 v_fmac_f32; torch copy_ of 1 GiB fp32 "
+            "how": "psc_probe_fma 4096x256 lanes x 8 chains x 20000 v_fmac_f32; psc_probe_mfma 4096x4 waves x "
+                   "4 chains x 4000 v_mfma_f32_16x16x4_f32; torch copy_ of 1 GiB fp32 "
                    "(2 GiB moved); 200 back-to-back psc_maxpool2x2 launches on a 2x2 image, eager and in one "
                    "HIP graph"}
 

@@ -354,6 +354,15 @@ psc_status psc_maxpool2x2(int32_t dtype, const void *d_x, int32_t n, int32_t c,
  * 2 * 8 * iters * blocks * 256 flops.  blocks in 1..2^20, iters >= 0. */
 psc_status psc_probe_fma(int32_t blocks, int32_t iters, float *d_out, void *stream);
 
+/* Measurement probe, not part of the method: blocks x 4 waves each run 4
+ * independent chains of iters fp32 MFMA 16x16x4 (the instruction of the
+ * dense conv and dense weight gradient), with A all 1 and B all 1/4, so each
+ * MFMA adds exactly 1 to each result; d_out [blocks*256] (fp32, device)
+ * receives per lane the sum of its 16 results, 16 * iters.  Timing it gives
+ * the matrix-core rate those kernels can reach: 32768 * iters * blocks
+ * flops.  blocks in 1..2^20, iters >= 0. */
+psc_status psc_probe_mfma(int32_t blocks, int32_t iters, float *d_out, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

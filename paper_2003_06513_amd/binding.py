@@ -95,6 +95,7 @@ def lib() -> ctypes.CDLL:
         "psc_conv3x3_fwd": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, P], ctypes.c_int),
         "psc_conv3x3_fwd_algo": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, P], ctypes.c_int),
         "psc_probe_fma": ([i32, i32, P, P], ctypes.c_int),
+        "psc_probe_mfma": ([i32, i32, P, P], ctypes.c_int),
         "psc_conv3x3_fwd_pool2": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, P], ctypes.c_int),
         "psc_conv3x3_fwd_strided": ([LP, PP, i32, P, i32, i32, i32, P, i32, P, i32, i32, P], ctypes.c_int),
         "psc_conv3x3_config": ([LP, i32, i32, i32, i32, i32, i32, i32, ctypes.POINTER(CConvConfig)],
@@ -326,6 +327,12 @@ def probe_fma(blocks: int, iters: int, out, stream=None):
     """psc_probe_fma: 2 * 8 * iters * blocks * 256 fp32 FMA flops into out
     [blocks*256] (measurement only)."""
     _check(lib().psc_probe_fma(int(blocks), int(iters), _dev(out, "out"), _stream(stream)), "psc_probe_fma")
+
+
+def probe_mfma(blocks: int, iters: int, out, stream=None):
+    """psc_probe_mfma: 32768 * iters * blocks fp32 MFMA flops; out [blocks*256]
+    (fp32, device) receives 16 * iters per lane."""
+    _check(lib().psc_probe_mfma(int(blocks), int(iters), _dev(out, "out"), _stream(stream)), "psc_probe_mfma")
 
 
 def maxpool2x2(x, y, stream=None):

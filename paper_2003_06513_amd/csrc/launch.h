@@ -83,6 +83,8 @@ hipError_t launch_transpose_prep(int dtype, int cout, int cin, const void* w, co
 size_t wgrad_workspace_bytes(int n, int cin, int cout, int h, int w, int64_t nk, bool dense);
 // Measurement probe: blocks x 256 lanes, each 8 x iters fp32 FMAs; out [blocks*256].
 hipError_t launch_probe_fma(int blocks, int iters, float* out, hipStream_t stream);
+// Measurement probe: blocks x 4 waves, each 4 chains of iters fp32 MFMA 16x16x4; out [blocks*256].
+hipError_t launch_probe_mfma(int blocks, int iters, float* out, hipStream_t stream);
 // Whether x and dy fit the 2 GiB a buffer descriptor addresses.
 bool wgrad_fits(int n, int cin, int cout, int h, int w, int dtype);
 hipError_t launch_bwd_weight(const PatTable& tab, const PackedView& pk, int dtype, int n, int cin, int h, int w,

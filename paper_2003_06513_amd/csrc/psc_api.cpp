@@ -558,4 +558,10 @@ psc_status psc_probe_fma(int32_t blocks, int32_t iters, float* d_out, void* stre
     return device_status(psc::launch_probe_fma(blocks, iters, d_out, as_stream(stream)), "psc_probe_fma launch");
 }
 
+psc_status psc_probe_mfma(int32_t blocks, int32_t iters, float* d_out, void* stream) {
+    if (blocks < 1 || blocks > (1 << 20) || iters < 0) return fail(PSC_ERR_ARG, "blocks=%d iters=%d", blocks, iters);
+    if (!d_out) return fail(PSC_ERR_ARG, "d_out is NULL");
+    return device_status(psc::launch_probe_mfma(blocks, iters, d_out, as_stream(stream)), "psc_probe_mfma launch");
+}
+
 }  // extern "C"

@@ -1,5 +1,8 @@
-"""The measurement probe psc_probe_fma computes what it says: per lane, 8
-chains a_j = fma(a_j, b, c) started at lane + j, summed (fp32)."""
+"""The measurement probes compute what they say.  psc_probe_fma: per lane, 8
+chains a_j = fma(a_j, b, c) started at lane + j, summed (fp32).
+psc_probe_mfma: 4 chains of fp32 MFMA 16x16x4 with A all 1 and B all 1/4,
+each instruction adding exactly 1 to each result, so every lane's 16 results
+sum to 16 * iters."""
 import numpy as np
 import pytest
 
@@ -28,3 +31,15 @@ def test_probe_fma_values():
     got = out.cpu().numpy().reshape(blocks, 256)
     for k in range(blocks):
         np.testing.assert_allclose(got[k], s, rtol=1e-6, atol=0)
+
+
+@pytest.mark.parametrize("iters", [0, 1, 1000])
+def test_probe_mfma_values(iters):
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    blocks = 5
+    out = torch.full((blocks * 256,), -1.0, dtype=torch.float32, device="cuda")
+    B.probe_mfma(blocks, iters, out)
+    torch.cuda.synchronize()
+    assert bool((out == 16.0 * iters).all())
