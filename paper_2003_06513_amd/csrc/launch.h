@@ -110,6 +110,9 @@ bool dense_wgrad_mfma_plan(int n, int cin, int cout, int h, int w, DenseWPlan* p
 size_t dense_wgrad_mfma_workspace(const DenseWPlan& p, int cin, int cout);
 hipError_t launch_dense_wgrad_mfma(const DenseWPlan& p, const float* x, const float* g, int n, int cin, int h,
                                    int w, int cout, float* dst, hipStream_t stream);
+// The masked gradient of the stored kernels taken from a dense dw [cout][cin][9].
+hipError_t launch_gather_masked(const PatTable& tab, const PackedView& pk, int cout, int cin, const float* dw,
+                                float* dv, hipStream_t stream);
 hipError_t launch_admm_primal(float* w, const float* dw, const float* a, const float* d, int64_t nw, float* b,
                               const float* db, int cout, float lr, float rho, float* v, hipStream_t stream);
 hipError_t launch_admm_dual(const PatTable& tab, const float* v, const uint8_t* pat, const uint8_t* keep, int64_t nk,

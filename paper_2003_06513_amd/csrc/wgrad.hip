@@ -293,12 +293,29 @@ static size_t wgrad_part_bytes(const WGeo& g, int64_t nk, bool dense) {
     return g.KS > 1 && g.n > 0 ? size_t(g.KS) * size_t(nk) * (dense ? 9 : 4) * sizeof(float) : 0;
 }
 
+// The masked gradient of a batch-1 fp32 layer of at least 16 input channels
+// is taken from the dense one on the matrix cores: there the masked kernels
+// are bound by load latency, and the dense GEMM over one image's pixels was
+// measured faster on every VGG-16 layer although it does 9 / (4 keep) times
+// the work.  Larger batches keep the masked kernels.
+static bool masked_via_dense(int dtype, int n, int cin, int cout, int h, int w, DenseWPlan* dp) {
+    return dtype == DT_F32 && n == 1 && dense_wgrad_mfma_plan(n, cin, cout, h, w, dp);
+}
+
 size_t wgrad_workspace_bytes(int n, int cin, int cout, int h, int w, int64_t nk, bool dense) {
     if (n <= 0) return 0;
     const int P = bias_parts(n, h * w);
     const size_t bias_bytes = P > 1 ? size_t(P) * size_t(cout) * sizeof(float) : 0;
     DenseWPlan dp;
     if (dense && dense_wgrad_mfma_plan(n, cin, cout, h, w, &dp)) return dense_wgrad_mfma_workspace(dp, cin, cout) + bias_bytes;
+    // the masked route through the dense gradient needs the dense dW as well
+    // (fp32: the size query does not know the dtype, so it covers this route)
+    if (!dense && masked_via_dense(DT_F32, n, cin, cout, h, w, &dp)) {
+        const WGeo g = plan(n, cin, cout, h, w, nk, false, nullptr, DT_F32);
+        const size_t via = dense_wgrad_mfma_workspace(dp, cin, cout) + size_t(cout) * size_t(cin) * 9 * sizeof(float);
+        const size_t direct = wgrad_part_bytes(g, nk, false);
+        return (via > direct ? via : direct) + bias_bytes;
+    }
     const WGeo g = plan(n, cin, cout, h, w, nk, dense, nullptr, DT_F32);
     return wgrad_part_bytes(g, nk, dense) + bias_bytes;
 }
@@ -307,11 +324,33 @@ hipError_t launch_bwd_weight(const PatTable& tab, const PackedView& pk, int dtyp
                              int cout, int64_t keep, const void* x, const void* dy, float* dv, float* db, void* ws,
                              hipStream_t stream) {
     const WGeo g = plan(n, cin, cout, h, w, keep, false, &tab, dtype);
-    hipError_t e = dtype == DT_F16
-                       ? run<DT_F16, 4>(g, x, dy, pk.filter_perm, pk.seg_ptr, pk.cin_idx, dv, ws, stream)
-                       : run<DT_F32, 4>(g, x, dy, pk.filter_perm, pk.seg_ptr, pk.cin_idx, dv, ws, stream);
+    DenseWPlan dp;
+    hipError_t e;
+    size_t part_bytes = wgrad_part_bytes(g, keep, false);
+    if (keep > 0 && masked_via_dense(dtype, n, cin, cout, h, w, &dp)) {
+        // workspace: the matrix-core partial sums, then the dense dW, then
+        // (after the larger of this and the masked kernels' partial sums,
+        // as sized by wgrad_workspace_bytes) the bias parts
+        const size_t slots = dense_wgrad_mfma_workspace(dp, cin, cout);
+        float* dense_dw = reinterpret_cast<float*>(static_cast<char*>(ws) + slots);
+        e = launch_dense_wgrad_mfma(dp, static_cast<const float*>(x), static_cast<const float*>(dy), n, cin, h, w,
+                                    cout, dp.KS > 1 ? static_cast<float*>(ws) : dense_dw, stream);
+        if (e == hipSuccess && dp.KS > 1) {
+            const int64_t ne = int64_t(cout) * cin * 9;
+            const int64_t gb = (ne + 255) / 256;
+            hipLaunchKernelGGL(k_wgrad_reduce, dim3(unsigned(gb > 8192 ? 8192 : gb)), dim3(256), 0, stream,
+                               static_cast<const float*>(ws), dp.KS, ne, dense_dw);
+            e = hipGetLastError();
+        }
+        if (e == hipSuccess) e = launch_gather_masked(tab, pk, cout, cin, dense_dw, dv, stream);
+        const size_t via = slots + size_t(cout) * size_t(cin) * 9 * sizeof(float);
+        part_bytes = via > part_bytes ? via : part_bytes;
+    } else {
+        e = dtype == DT_F16 ? run<DT_F16, 4>(g, x, dy, pk.filter_perm, pk.seg_ptr, pk.cin_idx, dv, ws, stream)
+                            : run<DT_F32, 4>(g, x, dy, pk.filter_perm, pk.seg_ptr, pk.cin_idx, dv, ws, stream);
+    }
     if (e != hipSuccess || !db) return e;
-    float* bpart = ws ? reinterpret_cast<float*>(static_cast<char*>(ws) + wgrad_part_bytes(g, keep, false)) : nullptr;
+    float* bpart = ws ? reinterpret_cast<float*>(static_cast<char*>(ws) + part_bytes) : nullptr;
     return dtype == DT_F16 ? bias_grad<DT_F16>(dy, n, cout, h * w, db, bpart, stream)
                            : bias_grad<DT_F32>(dy, n, cout, h * w, db, bpart, stream);
 }

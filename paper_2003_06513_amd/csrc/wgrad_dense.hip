@@ -139,6 +139,33 @@ __global__ __launch_bounds__(256) void k_wgrad_mfma(const float* __restrict__ x,
     }
 }
 
+// The masked weight gradient (Sec. 3.3) from a dense one: for stored kernel
+// k of reordered filter i (original filter perm[i], channel cin_idx[k],
+// library pattern pat_id[k]), dv[4k + j] = dw[perm[i]][cin_idx[k]][q_j], q_j
+// the j-th kept position of the pattern in ascending order -- the order of
+// the stored weights.  One block per reordered filter.  A malformed channel
+// or pattern index gives zeros, a malformed filter index reads filter 0.
+__global__ __launch_bounds__(256) void k_gather_masked(const float* __restrict__ dw, const int32_t* __restrict__ perm,
+                                                       const int32_t* __restrict__ filter_ptr,
+                                                       const int32_t* __restrict__ cin_idx,
+                                                       const uint8_t* __restrict__ pat_id, PatTable tab, int cin,
+                                                       int cout, float* __restrict__ dv) {
+    const int i = blockIdx.x;
+    const int f = perm[i] >= 0 && perm[i] < cout ? perm[i] : 0;
+    const int k0 = filter_ptr[i], k1 = filter_ptr[i + 1];
+    for (int k = k0 + int(threadIdx.x); k < k1; k += 256) {
+        const int c = cin_idx[k], p = pat_id[k];
+        const unsigned mask = (c >= 0 && c < cin && p < tab.m) ? tab.mask[p] : 0u;
+        const float* src = dw + (int64_t(f) * cin + (c >= 0 && c < cin ? c : 0)) * 9;
+        float v[4] = {0.f, 0.f, 0.f, 0.f};
+        int j = 0;
+        for (int q = 0; q < 9; ++q)
+            if (((mask >> q) & 1u) && j < 4) v[j++] = src[q];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) dv[int64_t(k) * 4 + t] = v[t];
+    }
+}
+
 }  // namespace
 
 // Layers of at least 16 input channels (a full MFMA tile of channels).
@@ -169,4 +196,13 @@ hipError_t launch_dense_wgrad_mfma(const DenseWPlan& p, const float* x, const fl
     return hipGetLastError();
 }
 
+}  // namespace psc
+
+namespace psc {
+hipError_t launch_gather_masked(const PatTable& tab, const PackedView& pk, int cout, int cin, const float* dw,
+                                float* dv, hipStream_t stream) {
+    hipLaunchKernelGGL(k_gather_masked, dim3(unsigned(cout)), dim3(256), 0, stream, dw, pk.filter_perm, pk.filter_ptr,
+                       pk.cin_idx, pk.pat_id, tab, cin, cout, dv);
+    return hipGetLastError();
+}
 }  // namespace psc

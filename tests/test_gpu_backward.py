@@ -49,6 +49,10 @@ SHAPES = [
     # one band group per wave at batch 1 (the weight gradient pipelines a
     # wave's chunks): full-size VGG-16 14x14 and ResNet-50 7x7 layers
     (1, 512, 512, 14, 14), (1, 512, 512, 7, 7),
+    # batch 1, fp32, at least 16 channels: the masked gradient gathered from
+    # the matrix-core dense one (two filter blocks, a channel tail, ragged
+    # pixel tiles, partial sums over several blocks)
+    (1, 16, 70, 9, 17), (1, 33, 5, 6, 40), (1, 64, 64, 56, 56),
 ]
 
 
