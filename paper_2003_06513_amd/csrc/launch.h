@@ -108,8 +108,8 @@ struct DenseWPlan {
 };
 bool dense_wgrad_mfma_plan(int n, int cin, int cout, int h, int w, DenseWPlan* p);
 size_t dense_wgrad_mfma_workspace(const DenseWPlan& p, int cin, int cout);
-hipError_t launch_dense_wgrad_mfma(const DenseWPlan& p, const float* x, const float* g, int n, int cin, int h,
-                                   int w, int cout, float* dst, hipStream_t stream);
+hipError_t launch_dense_wgrad_mfma(const DenseWPlan& p, int dtype, const void* x, const void* g, int n, int cin,
+                                   int h, int w, int cout, float* dst, hipStream_t stream);
 // The masked gradient of the stored kernels taken from a dense dw [cout][cin][9].
 hipError_t launch_gather_masked(const PatTable& tab, const PackedView& pk, int cout, int cin, const float* dw,
                                 float* dv, hipStream_t stream);

@@ -293,13 +293,13 @@ static size_t wgrad_part_bytes(const WGeo& g, int64_t nk, bool dense) {
     return g.KS > 1 && g.n > 0 ? size_t(g.KS) * size_t(nk) * (dense ? 9 : 4) * sizeof(float) : 0;
 }
 
-// The masked gradient of a batch-1 fp32 layer of at least 16 input channels
-// is taken from the dense one on the matrix cores: there the masked kernels
-// are bound by load latency, and the dense GEMM over one image's pixels was
-// measured faster on every VGG-16 layer although it does 9 / (4 keep) times
-// the work.  Larger batches keep the masked kernels.
-static bool masked_via_dense(int dtype, int n, int cin, int cout, int h, int w, DenseWPlan* dp) {
-    return dtype == DT_F32 && n == 1 && dense_wgrad_mfma_plan(n, cin, cout, h, w, dp);
+// The masked gradient of a batch-1 layer of at least 16 input channels is
+// taken from the dense one on the matrix cores: there the masked kernels are
+// bound by load latency, and the dense GEMM over one image's pixels was
+// measured faster on the VGG-16 and ResNet-50 layers although it does
+// 9 / (4 keep) times the work.  Larger batches keep the masked kernels.
+static bool masked_via_dense(int n, int cin, int cout, int h, int w, DenseWPlan* dp) {
+    return n == 1 && dense_wgrad_mfma_plan(n, cin, cout, h, w, dp);
 }
 
 size_t wgrad_workspace_bytes(int n, int cin, int cout, int h, int w, int64_t nk, bool dense) {
@@ -309,8 +309,7 @@ size_t wgrad_workspace_bytes(int n, int cin, int cout, int h, int w, int64_t nk,
     DenseWPlan dp;
     if (dense && dense_wgrad_mfma_plan(n, cin, cout, h, w, &dp)) return dense_wgrad_mfma_workspace(dp, cin, cout) + bias_bytes;
     // the masked route through the dense gradient needs the dense dW as well
-    // (fp32: the size query does not know the dtype, so it covers this route)
-    if (!dense && masked_via_dense(DT_F32, n, cin, cout, h, w, &dp)) {
+    if (!dense && masked_via_dense(n, cin, cout, h, w, &dp)) {
         const WGeo g = plan(n, cin, cout, h, w, nk, false, nullptr, DT_F32);
         const size_t via = dense_wgrad_mfma_workspace(dp, cin, cout) + size_t(cout) * size_t(cin) * 9 * sizeof(float);
         const size_t direct = wgrad_part_bytes(g, nk, false);
@@ -327,14 +326,14 @@ hipError_t launch_bwd_weight(const PatTable& tab, const PackedView& pk, int dtyp
     DenseWPlan dp;
     hipError_t e;
     size_t part_bytes = wgrad_part_bytes(g, keep, false);
-    if (keep > 0 && masked_via_dense(dtype, n, cin, cout, h, w, &dp)) {
+    if (keep > 0 && masked_via_dense(n, cin, cout, h, w, &dp)) {
         // workspace: the matrix-core partial sums, then the dense dW, then
         // (after the larger of this and the masked kernels' partial sums,
         // as sized by wgrad_workspace_bytes) the bias parts
         const size_t slots = dense_wgrad_mfma_workspace(dp, cin, cout);
         float* dense_dw = reinterpret_cast<float*>(static_cast<char*>(ws) + slots);
-        e = launch_dense_wgrad_mfma(dp, static_cast<const float*>(x), static_cast<const float*>(dy), n, cin, h, w,
-                                    cout, dp.KS > 1 ? static_cast<float*>(ws) : dense_dw, stream);
+        e = launch_dense_wgrad_mfma(dp, dtype, x, dy, n, cin, h, w, cout, dp.KS > 1 ? static_cast<float*>(ws) : dense_dw,
+                                    stream);
         if (e == hipSuccess && dp.KS > 1) {
             const int64_t ne = int64_t(cout) * cin * 9;
             const int64_t gb = (ne + 255) / 256;
@@ -363,7 +362,8 @@ hipError_t launch_dense_wgrad(const float* x, const float* g_, int n, int cin, i
     if (dense_wgrad_mfma_plan(n, cin, cout, h, w, &dp)) {
         // matrix cores: KS slots of partial sums, added in slot order
         part_bytes = dense_wgrad_mfma_workspace(dp, cin, cout);
-        e = launch_dense_wgrad_mfma(dp, x, g_, n, cin, h, w, cout, dp.KS > 1 ? static_cast<float*>(ws) : dw, stream);
+        e = launch_dense_wgrad_mfma(dp, DT_F32, x, g_, n, cin, h, w, cout, dp.KS > 1 ? static_cast<float*>(ws) : dw,
+                                    stream);
         if (e == hipSuccess && dp.KS > 1) {
             const int64_t ne = int64_t(cout) * cin * 9;
             const int64_t gb = (ne + 255) / 256;

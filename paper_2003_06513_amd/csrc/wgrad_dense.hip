@@ -3,7 +3,8 @@
 // Eq. 4):
 //   dW[f][c][q] = sum over images and pixels p of g[n, f, p] x[n, c, p + off(q)]
 // is a GEMM with M = filters, N = (tap, input channel) and K = pixels,
-// computed by fp32 MFMA 16x16x4.  A block owns 64 filters x 16 channels x 9
+// computed by fp32 MFMA 16x16x4 (fp16 x and g are widened exactly as they
+// load, so both accumulate in fp32).  A block owns 64 filters x 16 channels x 9
 // taps; each of its 4 waves owns 16 filters x 16 channels x 9 taps, i.e. one
 // MFMA tile per tap.  K runs over 4x16 pixel tiles of the images: a tile's
 // gradient values (transposed to [pixel][filter]) and its 16 input channels
@@ -39,9 +40,13 @@ constexpr int kWTargetBlocks = 512;
 
 typedef float wf4 __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(256) void k_wgrad_mfma(const float* __restrict__ x, const float* __restrict__ g,
-                                                    int n, int cin, int H, int W, int cout, int tiles_w,
-                                                    int tiles_img, int64_t tiles, int KS, float* __restrict__ out) {
+template <int DT>
+__global__ __launch_bounds__(256) void k_wgrad_mfma(const typename Elt<DT>::T* __restrict__ x,
+                                                    const typename Elt<DT>::T* __restrict__ g, int n, int cin, int H,
+                                                    int W, int cout, int tiles_w, int tiles_img, int64_t tiles, int KS,
+                                                    float* __restrict__ out) {
+    using T = typename Elt<DT>::T;
+    constexpr uint32_t ESZ = uint32_t(sizeof(T));
     __shared__ float gs[kWP * kWGS];
     __shared__ float xs[kWC * kWXS];
     const int f0 = blockIdx.x * kWF, c0 = blockIdx.y * kWC, ks = blockIdx.z;
@@ -52,10 +57,17 @@ __global__ __launch_bounds__(256) void k_wgrad_mfma(const float* __restrict__ x,
     // buffer descriptors: 32-bit offsets (x and g are below 2 GiB each);
     // elements outside the image, the channels or the filters sit past the
     // range and read zero
-    const auto xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(x), int16_t(0),
-                                                      int(int64_t(n) * cin * plane * 4), 0x00020000);
-    const auto gr = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(g), int16_t(0),
-                                                      int(int64_t(n) * cout * plane * 4), 0x00020000);
+    const auto xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(x), int16_t(0),
+                                                      int(int64_t(n) * cin * plane * ESZ), 0x00020000);
+    const auto gr = __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(g), int16_t(0),
+                                                      int(int64_t(n) * cout * plane * ESZ), 0x00020000);
+    // one element, widened to fp32 (fp16 exactly)
+    auto ld = [&](__amdgpu_buffer_rsrc_t rs, uint32_t vo) -> float {
+        if constexpr (DT == DT_F32)
+            return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, int(vo), 0, 0));
+        else
+            return float(__builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(rs, int(vo), 0, 0)));
+    };
     float rg[kWGJ], rx[kWXJ];
     auto fetch = [&](int64_t t) {
         const int img = int(t / tiles_img), tt = int(t - int64_t(img) * tiles_img);
@@ -66,9 +78,9 @@ __global__ __launch_bounds__(256) void k_wgrad_mfma(const float* __restrict__ x,
             const int f = e / kWP, p = e % kWP;
             const int oh = th0 + p / kWTC, ow = tw0 + p % kWTC;
             const bool in = f0 + f < cout && oh < H && ow < W;
-            const uint32_t vo = in ? (uint32_t(img * cout + f0 + f) * uint32_t(plane) + uint32_t(oh * W + ow)) * 4u
+            const uint32_t vo = in ? (uint32_t(img * cout + f0 + f) * uint32_t(plane) + uint32_t(oh * W + ow)) * ESZ
                                    : 0x80000000u;
-            rg[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(gr, int(vo), 0, 0));
+            rg[j] = ld(gr, vo);
         }
 #pragma unroll
         for (int j = 0; j < kWXJ; ++j) {
@@ -76,9 +88,9 @@ __global__ __launch_bounds__(256) void k_wgrad_mfma(const float* __restrict__ x,
             const int c = e / kWXE, r = (e / kWXC) % kWXR, s = e % kWXC;
             const int ih = th0 + r - 1, iw = tw0 + s - 1;
             const bool in = c < kWC && c0 + c < cin && ih >= 0 && ih < H && iw >= 0 && iw < W;
-            const uint32_t vo = in ? (uint32_t(img * cin + c0 + c) * uint32_t(plane) + uint32_t(ih * W + iw)) * 4u
+            const uint32_t vo = in ? (uint32_t(img * cin + c0 + c) * uint32_t(plane) + uint32_t(ih * W + iw)) * ESZ
                                    : 0x80000000u;
-            rx[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xr, int(vo), 0, 0));
+            rx[j] = ld(xr, vo);
         }
     };
     auto stage = [&]() {
@@ -189,10 +201,17 @@ size_t dense_wgrad_mfma_workspace(const DenseWPlan& p, int cin, int cout) {
     return p.KS > 1 ? size_t(p.KS) * size_t(cout) * size_t(cin) * 9 * sizeof(float) : 0;
 }
 
-hipError_t launch_dense_wgrad_mfma(const DenseWPlan& p, const float* x, const float* g, int n, int cin, int h,
-                                   int w, int cout, float* dst, hipStream_t stream) {
-    hipLaunchKernelGGL(k_wgrad_mfma, dim3(unsigned(p.fb), unsigned(p.cb), unsigned(p.KS)), dim3(256), 0, stream, x, g,
-                       n, cin, h, w, cout, p.tiles_w, p.tiles_img, p.tiles, p.KS, dst);
+hipError_t launch_dense_wgrad_mfma(const DenseWPlan& p, int dtype, const void* x, const void* g, int n, int cin,
+                                   int h, int w, int cout, float* dst, hipStream_t stream) {
+    const dim3 grid(unsigned(p.fb), unsigned(p.cb), unsigned(p.KS));
+    if (dtype == DT_F16)
+        hipLaunchKernelGGL(k_wgrad_mfma<DT_F16>, grid, dim3(256), 0, stream, static_cast<const uint16_t*>(x),
+                           static_cast<const uint16_t*>(g), n, cin, h, w, cout, p.tiles_w, p.tiles_img, p.tiles, p.KS,
+                           dst);
+    else
+        hipLaunchKernelGGL(k_wgrad_mfma<DT_F32>, grid, dim3(256), 0, stream, static_cast<const float*>(x),
+                           static_cast<const float*>(g), n, cin, h, w, cout, p.tiles_w, p.tiles_img, p.tiles, p.KS,
+                           dst);
     return hipGetLastError();
 }
 
