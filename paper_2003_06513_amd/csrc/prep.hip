@@ -69,6 +69,34 @@ constexpr size_t kSelHistOff = 0;   // 256 x u32
 constexpr size_t kSelStateOff = 1024;
 constexpr size_t kSelCountOff = 1280;
 
+// The digit of one radix pass, by threads 0..255 of the block (every thread
+// of the block calls it): with S(d) the number of candidate keys whose digit
+// is d or more, the digit is the largest d >= 1 with S(d) >= r (r = kernels
+// still to keep), else 0 -- the first digit from the top at which the
+// running count reaches r -- and S(d + 1) keys rank above it.  Suffix sums
+// in LDS instead of a serial walk over the 256 bins.  Returns the digit and
+// sets *above (both valid in every thread).
+__device__ __forceinline__ int sel_digit(const uint32_t* hist, int64_t r, uint64_t* sfx, int* s_d, int64_t* above) {
+    const int t = threadIdx.x;
+    if (t < 256) sfx[t] = hist[t];
+    if (t == 0) {
+        sfx[256] = 0;
+        *s_d = 0;
+    }
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+        const uint64_t v = t < 256 && t + off < 256 ? sfx[t + off] : 0u;
+        __syncthreads();
+        if (t < 256) sfx[t] += v;
+        __syncthreads();
+    }
+    if (t >= 1 && t < 256 && int64_t(sfx[t]) >= r) atomicMax(s_d, t);
+    __syncthreads();
+    const int d = *s_d;
+    *above = int64_t(sfx[d + 1]);
+    return d;
+}
+
 __global__ __launch_bounds__(256) void k_sel_init(uint32_t* __restrict__ hist, SelState* __restrict__ st,
                                                   int64_t keep) {
     hist[threadIdx.x] = 0;
@@ -98,20 +126,16 @@ __global__ __launch_bounds__(256) void k_sel_hist(const uint64_t* __restrict__ k
 
 __global__ __launch_bounds__(256) void k_sel_pick(uint32_t* __restrict__ hist, SelState* __restrict__ st,
                                                   int shift) {
+    __shared__ uint64_t sfx[257];
+    __shared__ int s_d;
+    const int64_t r = st->remaining;
+    int64_t above;
+    const int d = sel_digit(hist, r, sfx, &s_d, &above);
     if (threadIdx.x == 0) {
-        const int64_t r = st->remaining;
-        int64_t above = 0;
-        int d = 255;
-        for (; d > 0; --d) {
-            const int64_t c = hist[d];
-            if (above + c >= r) break;
-            above += c;
-        }
         st->remaining = r - above;
         st->prefix |= uint64_t(d) << shift;
         st->mask |= uint64_t(255) << shift;
     }
-    __syncthreads();
     hist[threadIdx.x] = 0;
 }
 
@@ -202,8 +226,8 @@ __global__ __launch_bounds__(256) void k_sel_mark(const uint64_t* __restrict__ k
 // The whole selection in one workgroup of 1024 threads, for layers of at
 // most kSelOneBlockMax kernels, where the passes above would be bound by
 // their 19 launches: the same 8 radix passes (histogram of the keys that
-// match the digits found so far, then the digit by the same scan from the
-// top), then the same index-ordered rank of the keys equal to the threshold
+// match the digits found so far, then the same digit), then the same
+// index-ordered rank of the keys equal to the threshold
 // -- each thread owns a contiguous run of indices -- so the keep mask is the
 // same bit for bit.
 constexpr int64_t kSelOneBlockMax = 65536;
@@ -212,8 +236,10 @@ __global__ __launch_bounds__(1024) void k_sel_one(const uint64_t* __restrict__ k
                                                   uint8_t* __restrict__ out) {
     __shared__ uint32_t hist[256];
     __shared__ uint32_t part[1024];
+    __shared__ uint64_t sfx[257];
     __shared__ uint64_t s_prefix, s_mask;
     __shared__ int64_t s_rem;
+    __shared__ int s_d;
     const int t = threadIdx.x;
     if (t == 0) {
         s_prefix = 0;
@@ -229,15 +255,11 @@ __global__ __launch_bounds__(1024) void k_sel_one(const uint64_t* __restrict__ k
             if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
         }
         __syncthreads();
+        const int64_t r = s_rem;
+        int64_t above;
+        const int d = sel_digit(hist, r, sfx, &s_d, &above);
+        __syncthreads();   // every thread has read s_rem, s_d and sfx
         if (t == 0) {
-            const int64_t r = s_rem;
-            int64_t above = 0;
-            int d = 255;
-            for (; d > 0; --d) {
-                const int64_t c = hist[d];
-                if (above + c >= r) break;
-                above += c;
-            }
             s_rem = r - above;
             s_prefix = prefix | (uint64_t(d) << shift);
             s_mask = mask | (uint64_t(255) << shift);
