@@ -77,14 +77,15 @@ __global__ __launch_bounds__(256) void k_conv_simple(const typename Elt<DT>::T* 
 
 // The dense 3x3 convolution of layers with at most 8 input channels (one
 // LDS stage: K = 9 cin <= 72 leaves the matrix cores idle and the layer is
-// bound by writing its output), on the vector ALUs: a block computes a 32x16
-// output tile (two rows per thread, ty and ty + 16) for 8 filters of one
+// bound by writing its output), on the vector ALUs: a block computes a 16x32
+// (rows x columns) output tile (two rows per thread, ty and ty + 8) for 8 filters of one
 // image.  Input channels are staged through LDS 8 at a time with a
 // 1-pixel halo; the 8 weights of a (channel, tap) sit side by side, so two
 // 16-byte LDS reads (the same address in every lane) give them all: 16 FMAs
 // per 2 input reads and 2 weight reads.  Only the channels present are run.
-constexpr int kDTH = 32;  // tile rows
-constexpr int kDTW = 16;  // tile columns
+constexpr int kDTH = 16;  // tile rows
+constexpr int kDTW = 32;  // tile columns: a row of a wave's store is 128 bytes (fp32)
+constexpr int kDHalf = kDTH / 2;   // a thread's second row
 constexpr int kDF = 8;    // filters per block
 constexpr int kDC = 8;    // channels per stage
 
@@ -127,7 +128,7 @@ __global__ __launch_bounds__(256) void k_dense(const typename Elt<DT>::T* __rest
 #pragma unroll
             for (int q = 0; q < 9; ++q) {
                 const float x0 = xs[c][ty + q / 3][tx + q % 3];
-                const float x1 = xs[c][ty + 16 + q / 3][tx + q % 3];
+                const float x1 = xs[c][ty + kDHalf + q / 3][tx + q % 3];
                 const float4 wa = *reinterpret_cast<const float4*>(&ws[c][q][0]);
                 const float4 wb = *reinterpret_cast<const float4*>(&ws[c][q][4]);
                 const float wv[kDF] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
@@ -143,7 +144,7 @@ __global__ __launch_bounds__(256) void k_dense(const typename Elt<DT>::T* __rest
     if (ow >= W) return;
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
-        const int oh = th0 + ty + 16 * half;
+        const int oh = th0 + ty + kDHalf * half;
         if (oh >= H) break;
 #pragma unroll
         for (int g = 0; g < kDF; ++g) {
