@@ -1,6 +1,7 @@
 // The dense weight gradient of a 3x3 layer (stride 1, zero padding 1) on the
 // matrix cores, for the primal step of the data-free ADMM loop (Sec. 4.3,
-// Eq. 4):
+// Eq. 4) and, gathered at the kept taps, for the masked gradient of batch-1
+// layers (Sec. 3.3):
 //   dW[f][c][q] = sum over images and pixels p of g[n, f, p] x[n, c, p + off(q)]
 // is a GEMM with M = filters, N = (tap, input channel) and K = pixels,
 // computed by fp32 MFMA 16x16x4 (fp16 x and g are widened exactly as they
