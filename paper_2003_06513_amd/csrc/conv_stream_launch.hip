@@ -83,7 +83,14 @@ bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
         const int64_t U = int64_t(a.n) * RB;
         const int64_t sgroups = (U + S - 1) / S;
         const bool aligned64 = a.dtype == DT_F32 && a.w % 16 == 0 && a.w >= 64;
-        if (aligned64 || sgroups * a.cout >= kWideMinWaves) {
+        // fp32 rows of 28 columns: a wave holds whole 28-row images (8 bands
+        // of 4 rows); where 8 shares of each filter make about 4096 waves
+        // (deep layers at small batch) the wide form takes them.  Measured
+        // on the batch-1 VGG-16 28x28 layers: 8 shares beat the one-column
+        // staged form by 6-8 % (2 shares lose).
+        const bool rows28 = a.dtype == DT_F32 && a.w == 28 && a.cin >= 16 * kMaxSplit &&
+                            sgroups * a.cout * kMaxSplit >= 4096;
+        if (aligned64 || rows28 || sgroups * a.cout >= kWideMinWaves) {
             g.cols_mode = 0;
             g.seg_len = seg_len;
             g.S = S;
@@ -94,7 +101,8 @@ bool plan_conv_stream(const PatTable& tab, const ConvArgs& a, Geo& g) {
             // shares only below about one wave per SIMD (at 112-224 columns
             // one share measured fastest)
             g.KS = 1;
-            while (g.KS < kMaxSplit && sgroups * a.cout * g.KS < 1024 && a.cin >= 16 * g.KS) g.KS *= 2;
+            const int64_t target = rows28 && sgroups * a.cout < kWideMinWaves ? 4096 : 1024;
+            while (g.KS < kMaxSplit && sgroups * a.cout * g.KS < target && a.cin >= 16 * g.KS) g.KS *= 2;
             g.FW = g.KS >= 4 ? 1 : 4 / g.KS;
             if (g.FW > a.cout) g.FW = a.cout;
             g.groups_x = (a.cout + g.FW - 1) / g.FW;
