@@ -129,3 +129,19 @@ def test_r8_with_several_segments_is_never_planned():
                             if cfg["kernel"] == 0:
                                 assert not (cfg["rows_per_lane"] == 8 and cfg["segments_per_wave"] > 1), \
                                     (dt, n, cin, cout, hw, pool, algo, cfg)
+
+
+def test_deep_28_column_layers_take_the_wide_form_with_shares():
+    """fp32 rows of 28 columns with 128+ input channels at small batch take
+    the 4-column form with 8 shares (a wave holds whole images; measured on
+    the batch-1 VGG-16 28x28 layers), shallow ones and fp16 keep their
+    forms."""
+    codes = [c for c in range(512) if bin(c).count("1") == 4 and (c >> 4) & 1][:8]
+    def cfg(cin, cout, n, dtype):
+        L = B.Layer(cout, cin, codes, (cout * cin) // 3, dtype)
+        return B.conv3x3_config(L, dtype, n, 28, 28, False, 1, 0)
+    for cin, cout in ((256, 512), (512, 512)):
+        c = cfg(cin, cout, 1, B.PSC_F32)
+        assert (c["kernel"], c["cols_per_lane"], c["shares"]) == (1, 4, 8)
+    assert cfg(64, 64, 1, B.PSC_F32)["cols_per_lane"] == 1        # too few channels for 8 shares
+    assert cfg(128, 128, 1, B.PSC_F16)["cols_per_lane"] == 1      # fp16 keeps the one-column form
