@@ -51,6 +51,7 @@ struct RGeo {
     int x_bytes;    // bytes of x (the buffer range), below 2^31
     int keep;
     int relu;
+    int staged;     // fp32, stride 2 on 8 x 8 or stride 1 on 16 x 16 planes: the planes go through LDS
     int8_t shape[kMaxPatterns];  // centre+3 shape index of each library pattern, -1 = other mask
     uint16_t mask[kMaxPatterns];
 };
@@ -296,14 +297,16 @@ __device__ __forceinline__ void run_rows(const RowCtx& c, int k, int e, float (&
     }
 }
 
-template <int DT, int W, int ST, int MASK>
-__device__ __forceinline__ void run_shape_rows(const RowCtx& c, int k, int e, float (&acc)[W / ST]) {
-    constexpr int Q0 = NthBit<MASK, 0>::value(), Q1 = NthBit<MASK, 1>::value();
-    constexpr int Q2 = NthBit<MASK, 2>::value(), Q3 = NthBit<MASK, 3>::value();
-    // the taps that read the DPP source row through DPP go last: the others
-    // put FMAs between the settle and the DPP reads
-    constexpr int DR = 0;   // ky of the taps read by DPP (the row above)
-    run_rows<DT, W, ST>(c, k, e, acc, [](float (&a)[W / ST], const RowVals<W, ST>& x, const float (&w)[4]) {
+// The four taps of a fixed centre+3 mask.  The taps that read the DPP source
+// row through DPP go last: the others put FMAs between the settle and the DPP
+// reads.
+template <int W, int ST, int MASK>
+struct ShapeTaps {
+    __device__ __forceinline__ void operator()(float (&a)[W / ST], const RowVals<W, ST>& x,
+                                               const float (&w)[4]) const {
+        constexpr int Q0 = NthBit<MASK, 0>::value(), Q1 = NthBit<MASK, 1>::value();
+        constexpr int Q2 = NthBit<MASK, 2>::value(), Q3 = NthBit<MASK, 3>::value();
+        constexpr int DR = 0;   // ky of the taps read by DPP (the row above)
         if constexpr (Q0 / 3 != DR && (ST == 2 || Q0 / 3 == 1)) tap_row<Q0, W, ST>(a, x, w[0]);
         if constexpr (Q1 / 3 != DR && (ST == 2 || Q1 / 3 == 1)) tap_row<Q1, W, ST>(a, x, w[1]);
         if constexpr (Q2 / 3 != DR && (ST == 2 || Q2 / 3 == 1)) tap_row<Q2, W, ST>(a, x, w[2]);
@@ -312,30 +315,44 @@ __device__ __forceinline__ void run_shape_rows(const RowCtx& c, int k, int e, fl
         if constexpr (!(Q1 / 3 != DR && (ST == 2 || Q1 / 3 == 1))) tap_row<Q1, W, ST>(a, x, w[1]);
         if constexpr (!(Q2 / 3 != DR && (ST == 2 || Q2 / 3 == 1))) tap_row<Q2, W, ST>(a, x, w[2]);
         if constexpr (!(Q3 / 3 != DR && (ST == 2 || Q3 / 3 == 1))) tap_row<Q3, W, ST>(a, x, w[3]);
-    });
-}
+    }
+};
 
 // Any 4-of-9 mask: each tap is chosen per kernel by a uniform branch.
-template <int DT, int W, int ST>
-__device__ __forceinline__ void run_generic_rows(unsigned mask, const RowCtx& c, int k, int e,
-                                                 float (&acc)[W / ST]) {
-    int q0 = 4, q1 = 4, q2 = 4, q3 = 4, seen = 0;
+template <int W, int ST>
+struct GenericTaps {
+    int q0 = 4, q1 = 4, q2 = 4, q3 = 4;
+    __device__ __forceinline__ explicit GenericTaps(unsigned mask) {
+        int seen = 0;
 #pragma unroll
-    for (int q = 0; q < 9; ++q) {
-        if ((mask >> q) & 1u) {
-            if (seen == 0) q0 = q;
-            else if (seen == 1) q1 = q;
-            else if (seen == 2) q2 = q;
-            else if (seen == 3) q3 = q;
-            ++seen;
+        for (int q = 0; q < 9; ++q) {
+            if ((mask >> q) & 1u) {
+                if (seen == 0) q0 = q;
+                else if (seen == 1) q1 = q;
+                else if (seen == 2) q2 = q;
+                else if (seen == 3) q3 = q;
+                ++seen;
+            }
         }
     }
-    run_rows<DT, W, ST>(c, k, e, acc, [=](float (&a)[W / ST], const RowVals<W, ST>& x, const float (&w)[4]) {
+    __device__ __forceinline__ void operator()(float (&a)[W / ST], const RowVals<W, ST>& x,
+                                               const float (&w)[4]) const {
         tap_row_dyn<W, ST>(q0, a, x, w[0]);
         tap_row_dyn<W, ST>(q1, a, x, w[1]);
         tap_row_dyn<W, ST>(q2, a, x, w[2]);
         tap_row_dyn<W, ST>(q3, a, x, w[3]);
-    });
+    }
+};
+
+template <int DT, int W, int ST, int MASK>
+__device__ __forceinline__ void run_shape_rows(const RowCtx& c, int k, int e, float (&acc)[W / ST]) {
+    run_rows<DT, W, ST>(c, k, e, acc, ShapeTaps<W, ST, MASK>{});
+}
+
+template <int DT, int W, int ST>
+__device__ __forceinline__ void run_generic_rows(unsigned mask, const RowCtx& c, int k, int e,
+                                                 float (&acc)[W / ST]) {
+    run_rows<DT, W, ST>(c, k, e, acc, GenericTaps<W, ST>(mask));
 }
 
 #define PSC_ROWS_CASE(I) \
@@ -361,7 +378,166 @@ __device__ __forceinline__ void run_pattern_rows(int shape, unsigned mask, const
 #undef PSC_ROWS_CASE8
 #undef PSC_ROWS_CASE
 
-template <int DT, int W, int ST>
+// ------------------------------------------------------------ LDS-staged rows
+// Two fp32 geometries in which each lane needs 64 contiguous bytes of its
+// image: stride 2 on 8 x 8 planes (12 images a wave, input rows 2r and 2r+1)
+// and stride 1 on 16 x 16 planes (3 images a wave, row r).  Loaded directly,
+// each 16-byte load of the wave touches 24 128-byte lines for 1 KiB of data.
+// Staged, the wave copies the channel planes of a kernel (3 KiB, whole
+// planes) into its own LDS area with three 1 KiB buffer-to-LDS loads of 8
+// lines each, and every lane then reads its 64 bytes with four 16-byte LDS
+// reads.  The copy of the next kernel overlaps the current kernel's FMAs (two
+// copies, as in the staged one-column form); no other wave touches the area,
+// so no barrier is needed.
+//
+// A plane is NCH chunks of 16 bytes; lane r of an image needs chunks 4r ..
+// 4r+3 and reads chunk 4r + j in its j-th read.  Image s keeps that chunk at
+// position 4r + ((j + s + r/4) & 3) of its block, so that in one read the
+// lanes of neighbouring rows and images hit different LDS banks.
+template <int W, int ST>
+struct Stage {
+    static constexpr int H = W;                     // square planes only
+    static constexpr int OH = H / ST;
+    static constexpr int S = 64 / (OH + 1);         // images per wave
+    static constexpr int PLANE = H * W * 4;         // bytes of one fp32 channel plane
+    static constexpr int NCH = PLANE / 16;          // chunks per plane
+    static constexpr int LC = ST * W / 4;           // chunks a lane reads
+    static constexpr int ZERO = S * PLANE;          // offset of the bytes padding lanes read (zero)
+    static constexpr int COPY = ZERO + 16 * LC;     // bytes between the two copies
+    static constexpr int WAVE = 2 * COPY;           // LDS bytes per wave
+    static constexpr int ND = S * NCH / 64;         // buffer-to-LDS loads per kernel
+    static_assert(LC == 4 && S * NCH == 64 * ND, "whole planes in whole 1 KiB loads, 64 bytes a lane");
+};
+
+constexpr bool staged_geometry(int dtype, int w, int h, int stride) {
+    return dtype == DT_F32 && h == w && ((stride == 2 && w == 8) || (stride == 1 && w == 16));
+}
+
+template <int W, int ST>
+struct RowLds {
+    cs::Meta m;
+    __amdgpu_buffer_rsrc_t xr;         // x, bounded to its size
+    uint32_t vo[Stage<W, ST>::ND];     // load j: byte offset in x (channel 0) of the chunk this lane moves, 2^31 past the batch
+    uint32_t area;                     // LDS address of this wave's area (wave-uniform)
+};
+
+// Copy the planes of channel ci into copy B.  A buffer-to-LDS load writes
+// lane L's 16 bytes at its LDS base + 16 L; load j covers positions 64 j ..
+// 64 j + 63 of the wave's chunks.  Images past the batch read zero (offset
+// 2^31, past the buffer range).
+template <int W, int ST, int B>
+__device__ __forceinline__ void dma_stage(const RowLds<W, ST>& c, int ci) {
+#if defined(__HIP_DEVICE_COMPILE__)   // the 16-byte form exists only for the gfx950 device pass
+    using G = Stage<W, ST>;
+    const int soff = __builtin_amdgcn_readfirstlane(ci * G::PLANE);
+#pragma unroll
+    for (int j = 0; j < G::ND; ++j) {
+        cs::lds_void_t* dst = (cs::lds_void_t*)(uintptr_t)(c.area + uint32_t(B * G::COPY + j * 1024));
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(c.xr, dst, 16, c.vo[j], soff, 0, 0);
+    }
+#endif
+}
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// One kernel whose planes sit (or are arriving) in copy B: wait for them,
+// start the copy of kernel k+1 (channel ci; also across the pattern segment's
+// end) into the other copy, read this lane's rows and run the FMAs with the
+// weights w of kernel k; then refill w and ci with the weights of kernel k+2
+// and the channel of kernel k+3, for the next trip of the same copy.
+template <int W, int ST, int B, class TapFn>
+__device__ __forceinline__ void stage_trip(const RowLds<W, ST>& c, const uint32_t (&lo)[4], int k, int s1,
+                                           float (&w)[4], int& ci, float (&acc)[W / ST], TapFn taps) {
+    using G = Stage<W, ST>;
+    const int last = s1 - 1;
+    __builtin_amdgcn_s_waitcnt(cs::kWaitVm0);            // planes of kernel k are in LDS
+    asm volatile("" ::: "memory");
+    if (k + 1 < s1) dma_stage<W, ST, B ^ 1>(c, ci);      // planes of kernel k+1
+    f32x4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        v[j] = *(const __attribute__((address_space(3))) f32x4*)(uintptr_t)(lo[j] + B * G::COPY);
+    __builtin_amdgcn_s_waitcnt(cs::kWaitLgkm0);          // rows in registers
+    asm volatile("" ::: "memory");
+    RowVals<W, ST> x;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        if constexpr (ST == 2) {
+            x.e[t] = v[0][t], x.e[4 + t] = v[1][t];
+            x.o[t] = v[2][t], x.o[4 + t] = v[3][t];
+        } else {
+            x.e[t] = v[0][t], x.e[4 + t] = v[1][t], x.e[8 + t] = v[2][t], x.e[12 + t] = v[3][t];
+        }
+    }
+    if constexpr (ST == 2) settle_row<W>(x.o);
+    else settle_row<W>(x.e);
+    taps(acc, x, w);
+    // the FMAs stay ahead of the next trip's wait: moved past it, they would
+    // wait for the copy just started
+#pragma unroll
+    for (int t = 0; t < W / ST; ++t) asm volatile("" : "+v"(acc[t]));
+    cs::meta_w<DT_F32>(c.m, k + 2 <= last ? k + 2 : last, w);
+    ci = cs::meta_ci(c.m, k + 3 <= last ? k + 3 : last);
+}
+
+// Kernels [k, e) of one pattern segment of the share that ends at s1, the
+// first one's planes in copy B0; returns the copy that kernel e's planes go
+// to.  Each copy has its own weight and channel registers, refilled two
+// kernels ahead.
+template <int W, int ST, int B0, class TapFn>
+__device__ __forceinline__ int stage_pairs(const RowLds<W, ST>& c, const uint32_t (&lo)[4], int k, int e, int s1,
+                                           float (&acc)[W / ST], TapFn taps) {
+    const int last = s1 - 1;
+    float wA[4], wB[4];
+    cs::meta_w<DT_F32>(c.m, k, wA);
+    cs::meta_w<DT_F32>(c.m, k + 1 <= last ? k + 1 : last, wB);
+    int ciA = cs::meta_ci(c.m, k + 1 <= last ? k + 1 : last);
+    int ciB = cs::meta_ci(c.m, k + 2 <= last ? k + 2 : last);
+    while (k + 1 < e) {
+        stage_trip<W, ST, B0>(c, lo, k, s1, wA, ciA, acc, taps);
+        stage_trip<W, ST, B0 ^ 1>(c, lo, k + 1, s1, wB, ciB, acc, taps);
+        k += 2;
+    }
+    if (k < e) {
+        stage_trip<W, ST, B0>(c, lo, k, s1, wA, ciA, acc, taps);
+        return B0 ^ 1;
+    }
+    return B0;
+}
+
+template <int W, int ST, class TapFn>
+__device__ __forceinline__ int stage_kernels(const RowLds<W, ST>& c, const uint32_t (&lo)[4], int k, int e, int s1,
+                                             int par, float (&acc)[W / ST], TapFn taps) {
+    return par == 0 ? stage_pairs<W, ST, 0>(c, lo, k, e, s1, acc, taps)
+                    : stage_pairs<W, ST, 1>(c, lo, k, e, s1, acc, taps);
+}
+
+#define PSC_STG_CASE(I) \
+    case I: return stage_kernels<W, ST>(c, lo, k, e, s1, par, acc, ShapeTaps<W, ST, kCentre3.code[I]>{});
+#define PSC_STG_CASE8(I)                                                                            \
+    PSC_STG_CASE(I) PSC_STG_CASE(I + 1) PSC_STG_CASE(I + 2) PSC_STG_CASE(I + 3)                     \
+    PSC_STG_CASE(I + 4) PSC_STG_CASE(I + 5) PSC_STG_CASE(I + 6) PSC_STG_CASE(I + 7)
+
+template <int W, int ST>
+__device__ __forceinline__ int stage_pattern(int shape, unsigned mask, const RowLds<W, ST>& c,
+                                             const uint32_t (&lo)[4], int k, int e, int s1, int par,
+                                             float (&acc)[W / ST]) {
+    switch (shape) {
+        PSC_STG_CASE8(0)
+        PSC_STG_CASE8(8)
+        PSC_STG_CASE8(16)
+        PSC_STG_CASE8(24)
+        PSC_STG_CASE8(32)
+        PSC_STG_CASE8(40)
+        PSC_STG_CASE8(48)
+        default: return stage_kernels<W, ST>(c, lo, k, e, s1, par, acc, GenericTaps<W, ST>(mask));
+    }
+}
+#undef PSC_STG_CASE8
+#undef PSC_STG_CASE
+
+// STG: the LDS-staged form (fp32: stride 2 on 8 x 8 planes, stride 1 on 16 x 16).
+template <int DT, int W, int ST, bool STG>
 __global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __restrict__ x,
                                                    const int32_t* __restrict__ perm,
                                                    const int32_t* __restrict__ seg_ptr,
@@ -372,7 +548,8 @@ __global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __
     using E = Elt<DT>;
     constexpr int ESZ = int(sizeof(typename E::T));
     constexpr int OW = W / ST;                // output columns (stride 2: W even)
-    extern __shared__ float psc_rows_red[];   // KS > 1: [KS][OW][64] partial sums
+    // KS > 1: [KS][OW][64] partial sums; STG: first the waves' staging areas
+    extern __shared__ float psc_rows_red[];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
@@ -403,7 +580,56 @@ __global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __
 #pragma unroll
     for (int c = 0; c < OW; ++c) acc[c] = 0.f;
 
-    if (has_filter) {
+    if constexpr (STG) {
+        using G = Stage<W, ST>;
+        static_assert(staged_geometry(DT, W, W, ST), "no staged form for this geometry");
+        // this wave's area: copy 0 of the planes, 64 zero bytes, copy 1, 64
+        // zero bytes; a padding lane reads the zero bytes after its copy
+        const uint32_t area = uint32_t(uintptr_t((const __attribute__((address_space(3))) void*)psc_rows_red)) +
+                              uint32_t(wave * G::WAVE);
+        if (lane < 16) {
+            *(__attribute__((address_space(3))) float*)(uintptr_t)(area + G::ZERO + lane * 4) = 0.f;
+            *(__attribute__((address_space(3))) float*)(uintptr_t)(area + G::COPY + G::ZERO + lane * 4) = 0.f;
+        }
+        // LDS address (copy 0) of the chunk this lane reads in each of its 4 reads
+        uint32_t lo[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            lo[j] = s < G::S && r < G::OH
+                        ? area + uint32_t(s * G::PLANE + 16 * (4 * r + ((j + s + (r >> 2)) & 3)))
+                        : area + uint32_t(G::ZERO + 16 * j);
+        if (has_filter) {
+            const int* segp = seg_ptr + i * (g.m + 1);
+            const int f0 = segp[0], f1 = segp[g.m];
+            const int len = f1 - f0;
+            const int s0 = f0 + len * sp / g.KS, s1 = f0 + len * (sp + 1) / g.KS;
+            RowLds<W, ST> ctx;
+            ctx.m = cs::Meta{cs::scalar_rsrc(cin_idx, g.keep * 4), cs::scalar_rsrc(vals, g.keep * 4 * ESZ)};
+            ctx.xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<typename E::T*>(x), int16_t(0), g.x_bytes,
+                                                       0x00020000);
+            ctx.area = __builtin_amdgcn_readfirstlane(area);
+            // load j, lane L: position q of image slot t's block, holding
+            // chunk 4 rr + ((q - t - rr/4) & 3) of the plane (rr = q / 4)
+#pragma unroll
+            for (int j = 0; j < G::ND; ++j) {
+                const int pos = 64 * j + lane, t = pos / G::NCH, q = pos - t * G::NCH, rr = q >> 2;
+                const int chunk = 4 * rr + ((q - t - (rr >> 2)) & 3);
+                const int im = grp * G::S + t;
+                ctx.vo[j] = im < g.n ? uint32_t(im * g.cin * G::PLANE + chunk * 16) : 0x80000000u;
+            }
+            if (s0 < s1) {
+                dma_stage<W, ST, 0>(ctx, cs::meta_ci(ctx.m, s0));
+                int par = 0;
+                for (int p = 0; p < g.m; ++p) {
+                    int k0 = segp[p], k1 = segp[p + 1];
+                    k0 = k0 < s0 ? s0 : k0;
+                    k1 = k1 > s1 ? s1 : k1;                 // malformed pointers stay in the share
+                    if (k0 < k1) par = stage_pattern<W, ST>(g.shape[p], g.mask[p], ctx, lo, k0, k1, s1, par, acc);
+                }
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(cs::kWaitVm0);        // no copy into LDS is left in flight
+    } else if (has_filter) {
         const int* segp = seg_ptr + i * (g.m + 1);
         const int f0 = segp[0], f1 = segp[g.m];
         // share sp: the sp-th of KS equal contiguous ranges of the filter's kernels
@@ -430,6 +656,8 @@ __global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __
     // ---- add the KS partial sums of each filter in share order
     if (g.KS > 1) {
         float (*red)[OW][64] = reinterpret_cast<float (*)[OW][64]>(psc_rows_red);
+        // the partial sums reuse the staging areas: wait until every wave is done
+        if constexpr (STG) __syncthreads();
         for (int slot = 0; slot < g.FW; ++slot) {
             if (slot == gf) {
 #pragma unroll
@@ -466,8 +694,18 @@ template <int DT, int W, int ST>
 hipError_t launch_rows(const PackedView& pk, const ConvArgs& a, const RGeo& g, hipStream_t stream) {
     using T = typename Elt<DT>::T;
     const int waves = g.FW * g.KS;
-    const size_t smem = g.KS > 1 ? size_t(g.KS) * (W / ST) * 64 * sizeof(float) : 0;
-    hipLaunchKernelGGL((k_conv_rows<DT, W, ST>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)), smem,
+    const size_t red = g.KS > 1 ? size_t(g.KS) * (W / ST) * 64 * sizeof(float) : 0;
+    if constexpr (staged_geometry(DT, W, W, ST)) {
+        if (g.staged) {
+            const size_t stage = size_t(waves) * Stage<W, ST>::WAVE;
+            hipLaunchKernelGGL((k_conv_rows<DT, W, ST, true>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)),
+                               stage > red ? stage : red, stream, static_cast<const T*>(a.x), pk.filter_perm,
+                               pk.seg_ptr, pk.cin_idx, static_cast<const T*>(pk.values),
+                               static_cast<const T*>(a.bias), static_cast<T*>(a.y), g);
+            return hipGetLastError();
+        }
+    }
+    hipLaunchKernelGGL((k_conv_rows<DT, W, ST, false>), dim3(unsigned(g.nblocks)), dim3(unsigned(waves * 64)), red,
                        stream, static_cast<const T*>(a.x), pk.filter_perm, pk.seg_ptr, pk.cin_idx,
                        static_cast<const T*>(pk.values), static_cast<const T*>(a.bias), static_cast<T*>(a.y), g);
     return hipGetLastError();

@@ -73,6 +73,7 @@ bool plan_conv_rows(const PatTable& tab, const ConvArgs& a, RGeo& g) {
             for (int t = 0; t < 56; ++t)
                 if (kCentre3.code[t] == tab.mask[p]) g.shape[p] = int8_t(t);
     }
+    g.staged = staged_geometry(a.dtype, a.w, a.h, a.stride);
     g.seg_len = g.OH + 1;
     g.S = 64 / g.seg_len;
     g.groups = (a.n + g.S - 1) / g.S;
@@ -106,7 +107,7 @@ bool prefer_conv_rows(const PatTable& tab, const ConvArgs& a) {
 bool describe_conv_rows(const PatTable& tab, const ConvArgs& a, ConvForm& out) {
     RGeo g;
     if (!plan_conv_rows(tab, a, g)) return false;
-    out = ConvForm{4, 0, 1, g.OW, g.S, 1, g.KS, g.FW, g.nblocks, g.FW * g.KS * 64};
+    out = ConvForm{4, g.staged, 1, g.OW, g.S, 1, g.KS, g.FW, g.nblocks, g.FW * g.KS * 64};
     return true;
 }
 

@@ -191,25 +191,32 @@ def form_cases():
                         n, cin, cout, h, w, dt, False, 2, 0))
         # the one-row-per-lane kernel (algo 2) at every compiled width: ragged
         # image groups, a partial wave, split filters, rows unequal to columns,
+        # fp32 16 x 16 planes through LDS (a ragged last group, one partial
+        # wave, 2 and 4 shares),
         # and (fp16, width 7, odd cin and n) the last row of x read through a
         # window that reaches past the end of x
         rows_shapes = ((13, 5, 6, 4, 4), (1, 40, 5, 4, 4), (9, 7, 5, 7, 7), (5, 3, 4, 7, 7), (3, 33, 6, 7, 7),
                        (8, 16, 9, 8, 8), (4, 24, 4, 5, 8), (5, 6, 7, 14, 14), (2, 48, 3, 13, 14),
-                       (4, 10, 6, 16, 16), (1, 64, 4, 11, 16), (3, 9, 5, 28, 28), (1, 40, 3, 20, 28))
+                       (4, 10, 6, 16, 16), (1, 64, 4, 11, 16), (3, 9, 5, 28, 28), (1, 40, 3, 20, 28),
+                       (1, 64, 4, 16, 16), (7, 40, 5, 16, 16))
         for n, cin, cout, h, w in rows_shapes:
             if dt == B.PSC_F16 and (w & 1) and w != 7:
                 continue
             L = B.Layer(cout, cin, list(FORM_MASKS), cin * cout // 2, dt)
             cfg = B.conv3x3_config(L, dt, n, h, w, False, 1, 2)
-            out.append((("rows", cfg["kernel"], w, cfg["shares"] > 1), n, cin, cout, h, w, dt, False, 1, 2))
+            out.append((("rows", cfg["kernel"], w, cfg["shares"] > 1, cfg["staged"]), n, cin, cout, h, w, dt,
+                        False, 1, 2))
         # its stride-2 form: every compiled width, odd and even heights (the
         # last output row's odd input row past the image), ragged groups,
-        # split filters
+        # split filters; fp32 8 x 8 planes go through LDS: a ragged last
+        # group (images past the batch), one partial wave, and 2 and 4 shares
+        # (their sums reuse the staging areas)
         for n, cin, cout, h, w in ((13, 5, 6, 8, 8), (2, 40, 5, 7, 8), (9, 7, 5, 16, 16), (1, 48, 4, 15, 16),
-                                   (4, 9, 5, 32, 32), (1, 40, 3, 31, 32)):
+                                   (4, 9, 5, 32, 32), (1, 40, 3, 31, 32), (1, 48, 4, 8, 8), (25, 70, 9, 8, 8)):
             L = B.Layer(cout, cin, list(FORM_MASKS), cin * cout // 2, dt)
             cfg = B.conv3x3_config(L, dt, n, h, w, False, 2, 2)
-            out.append((("rows2", cfg["kernel"], w, cfg["shares"] > 1), n, cin, cout, h, w, dt, False, 2, 2))
+            out.append((("rows2", cfg["kernel"], w, cfg["shares"] > 1, cfg["staged"]), n, cin, cout, h, w, dt,
+                        False, 2, 2))
         # the wide form below 64 columns and in fp16, which the automatic
         # choice takes only for grids of 6144+ waves: many filters over few
         # channels keep the oracle cheap; ragged bands, a pooled epilogue,
