@@ -51,7 +51,7 @@ struct RGeo {
     int x_bytes;    // bytes of x (the buffer range), below 2^31
     int keep;
     int relu;
-    int staged;     // fp32, stride 2 on 8 x 8 or stride 1 on 16 x 16 planes: the planes go through LDS
+    int staged;     // fp32, stride 1 on 16 x 16, stride 2 on 8 x 8 and 16 x 16 planes: the planes go through LDS
     int8_t shape[kMaxPatterns];  // centre+3 shape index of each library pattern, -1 = other mask
     uint16_t mask[kMaxPatterns];
 };
@@ -379,21 +379,24 @@ __device__ __forceinline__ void run_pattern_rows(int shape, unsigned mask, const
 #undef PSC_ROWS_CASE
 
 // ------------------------------------------------------------ LDS-staged rows
-// Two fp32 geometries in which each lane needs 64 contiguous bytes of its
-// image: stride 2 on 8 x 8 planes (12 images a wave, input rows 2r and 2r+1)
-// and stride 1 on 16 x 16 planes (3 images a wave, row r).  Loaded directly,
-// each 16-byte load of the wave touches 24 128-byte lines for 1 KiB of data.
-// Staged, the wave copies the channel planes of a kernel (3 KiB, whole
-// planes) into its own LDS area with three 1 KiB buffer-to-LDS loads of 8
-// lines each, and every lane then reads its 64 bytes with four 16-byte LDS
-// reads.  The copy of the next kernel overlaps the current kernel's FMAs (two
-// copies, as in the staged one-column form); no other wave touches the area,
-// so no barrier is needed.
+// Three fp32 geometries in which each lane needs whole rows of its image
+// that lie 64 or 128 bytes apart from its neighbours': stride 1 on 16 x 16
+// planes (3 images a wave, row r, 64 bytes), stride 2 on 8 x 8 (12 images,
+// input rows 2r and 2r+1, 64 bytes) and on 16 x 16 (7 images, 128 bytes).
+// Loaded directly, each 16-byte load of the wave touches 24 or more
+// 128-byte lines per KiB.  Staged, the wave copies the channel planes of a
+// kernel (3 or 7 KiB, whole planes) into its own LDS area with 1 KiB
+// buffer-to-LDS loads of 8 lines each, and every lane then reads its rows
+// with 16-byte LDS reads.  The copy of the next kernel overlaps the current
+// kernel's FMAs.  With two copies it starts before this kernel's reads;
+// with one (7 KiB planes, to keep 20+ waves per CU) right after them.  No
+// other wave touches the area, so no barrier is needed.
 //
-// A plane is NCH chunks of 16 bytes; lane r of an image needs chunks 4r ..
-// 4r+3 and reads chunk 4r + j in its j-th read.  Image s keeps that chunk at
-// position 4r + ((j + s + r/4) & 3) of its block, so that in one read the
-// lanes of neighbouring rows and images hit different LDS banks.
+// A plane is NCH chunks of 16 bytes; lane r of an image needs the LC chunks
+// LC r .. LC r + LC-1 and reads chunk LC r + j in its j-th read.  Image s
+// keeps that chunk at position LC r + ((j + s + r / (16 / LC)) mod LC) of
+// its block, so that in one read the lanes of neighbouring rows and images
+// hit different LDS banks.
 template <int W, int ST>
 struct Stage {
     static constexpr int H = W;                     // square planes only
@@ -402,15 +405,17 @@ struct Stage {
     static constexpr int PLANE = H * W * 4;         // bytes of one fp32 channel plane
     static constexpr int NCH = PLANE / 16;          // chunks per plane
     static constexpr int LC = ST * W / 4;           // chunks a lane reads
+    static constexpr int RD = 16 / LC;              // rows per step of the rotation
     static constexpr int ZERO = S * PLANE;          // offset of the bytes padding lanes read (zero)
-    static constexpr int COPY = ZERO + 16 * LC;     // bytes between the two copies
-    static constexpr int WAVE = 2 * COPY;           // LDS bytes per wave
+    static constexpr int COPY = ZERO + 16 * LC;     // bytes between the copies
+    static constexpr int NB = LC == 4 ? 2 : 1;      // copies
+    static constexpr int WAVE = NB * COPY;          // LDS bytes per wave
     static constexpr int ND = S * NCH / 64;         // buffer-to-LDS loads per kernel
-    static_assert(LC == 4 && S * NCH == 64 * ND, "whole planes in whole 1 KiB loads, 64 bytes a lane");
+    static_assert((LC == 4 || LC == 8) && S * NCH == 64 * ND, "whole planes in whole 1 KiB loads");
 };
 
 constexpr bool staged_geometry(int dtype, int w, int h, int stride) {
-    return dtype == DT_F32 && h == w && ((stride == 2 && w == 8) || (stride == 1 && w == 16));
+    return dtype == DT_F32 && h == w && ((stride == 2 && (w == 8 || w == 16)) || (stride == 1 && w == 16));
 }
 
 template <int W, int ST>
@@ -421,7 +426,7 @@ struct RowLds {
     uint32_t area;                     // LDS address of this wave's area (wave-uniform)
 };
 
-// Copy the planes of channel ci into copy B.  A buffer-to-LDS load writes
+// Copy the planes of channel ci into copy B (0 when there is one copy).  A buffer-to-LDS load writes
 // lane L's 16 bytes at its LDS base + 16 L; load j covers positions 64 j ..
 // 64 j + 63 of the wave's chunks.  Images past the batch read zero (offset
 // 2^31, past the buffer range).
@@ -446,29 +451,34 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 // weights w of kernel k; then refill w and ci with the weights of kernel k+2
 // and the channel of kernel k+3, for the next trip of the same copy.
 template <int W, int ST, int B, class TapFn>
-__device__ __forceinline__ void stage_trip(const RowLds<W, ST>& c, const uint32_t (&lo)[4], int k, int s1,
-                                           float (&w)[4], int& ci, float (&acc)[W / ST], TapFn taps) {
+__device__ __forceinline__ void stage_trip(const RowLds<W, ST>& c, const uint32_t (&lo)[Stage<W, ST>::LC], int k,
+                                           int s1, float (&w)[4], int& ci, float (&acc)[W / ST], TapFn taps) {
     using G = Stage<W, ST>;
+    constexpr int LC = G::LC;
+    constexpr int BR = G::NB == 2 ? B : 0;               // the copy this kernel's planes sit in
     const int last = s1 - 1;
     __builtin_amdgcn_s_waitcnt(cs::kWaitVm0);            // planes of kernel k are in LDS
     asm volatile("" ::: "memory");
-    if (k + 1 < s1) dma_stage<W, ST, B ^ 1>(c, ci);      // planes of kernel k+1
-    f32x4 v[4];
+    if constexpr (G::NB == 2)
+        if (k + 1 < s1) dma_stage<W, ST, BR ^ 1>(c, ci); // planes of kernel k+1
+    f32x4 v[LC];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-        v[j] = *(const __attribute__((address_space(3))) f32x4*)(uintptr_t)(lo[j] + B * G::COPY);
+    for (int j = 0; j < LC; ++j)
+        v[j] = *(const __attribute__((address_space(3))) f32x4*)(uintptr_t)(lo[j] + BR * G::COPY);
     __builtin_amdgcn_s_waitcnt(cs::kWaitLgkm0);          // rows in registers
     asm volatile("" ::: "memory");
+    // one copy: it is free again once the rows are in registers
+    if constexpr (G::NB == 1)
+        if (k + 1 < s1) dma_stage<W, ST, 0>(c, ci);      // planes of kernel k+1
+    // chunks 0 .. LC/ST - 1 hold the (even) row, stride 2: then the odd row
     RowVals<W, ST> x;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        if constexpr (ST == 2) {
-            x.e[t] = v[0][t], x.e[4 + t] = v[1][t];
-            x.o[t] = v[2][t], x.o[4 + t] = v[3][t];
-        } else {
-            x.e[t] = v[0][t], x.e[4 + t] = v[1][t], x.e[8 + t] = v[2][t], x.e[12 + t] = v[3][t];
+    for (int j = 0; j < LC; ++j)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            if (ST == 1 || j < LC / 2) x.e[4 * j + t] = v[j][t];
+            else x.o[4 * (j - LC / 2) + t] = v[j][t];
         }
-    }
     if constexpr (ST == 2) settle_row<W>(x.o);
     else settle_row<W>(x.e);
     taps(acc, x, w);
@@ -485,8 +495,8 @@ __device__ __forceinline__ void stage_trip(const RowLds<W, ST>& c, const uint32_
 // to.  Each copy has its own weight and channel registers, refilled two
 // kernels ahead.
 template <int W, int ST, int B0, class TapFn>
-__device__ __forceinline__ int stage_pairs(const RowLds<W, ST>& c, const uint32_t (&lo)[4], int k, int e, int s1,
-                                           float (&acc)[W / ST], TapFn taps) {
+__device__ __forceinline__ int stage_pairs(const RowLds<W, ST>& c, const uint32_t (&lo)[Stage<W, ST>::LC], int k,
+                                           int e, int s1, float (&acc)[W / ST], TapFn taps) {
     const int last = s1 - 1;
     float wA[4], wB[4];
     cs::meta_w<DT_F32>(c.m, k, wA);
@@ -506,8 +516,8 @@ __device__ __forceinline__ int stage_pairs(const RowLds<W, ST>& c, const uint32_
 }
 
 template <int W, int ST, class TapFn>
-__device__ __forceinline__ int stage_kernels(const RowLds<W, ST>& c, const uint32_t (&lo)[4], int k, int e, int s1,
-                                             int par, float (&acc)[W / ST], TapFn taps) {
+__device__ __forceinline__ int stage_kernels(const RowLds<W, ST>& c, const uint32_t (&lo)[Stage<W, ST>::LC], int k,
+                                             int e, int s1, int par, float (&acc)[W / ST], TapFn taps) {
     return par == 0 ? stage_pairs<W, ST, 0>(c, lo, k, e, s1, acc, taps)
                     : stage_pairs<W, ST, 1>(c, lo, k, e, s1, acc, taps);
 }
@@ -520,7 +530,7 @@ __device__ __forceinline__ int stage_kernels(const RowLds<W, ST>& c, const uint3
 
 template <int W, int ST>
 __device__ __forceinline__ int stage_pattern(int shape, unsigned mask, const RowLds<W, ST>& c,
-                                             const uint32_t (&lo)[4], int k, int e, int s1, int par,
+                                             const uint32_t (&lo)[Stage<W, ST>::LC], int k, int e, int s1, int par,
                                              float (&acc)[W / ST]) {
     switch (shape) {
         PSC_STG_CASE8(0)
@@ -536,7 +546,7 @@ __device__ __forceinline__ int stage_pattern(int shape, unsigned mask, const Row
 #undef PSC_STG_CASE8
 #undef PSC_STG_CASE
 
-// STG: the LDS-staged form (fp32: stride 2 on 8 x 8 planes, stride 1 on 16 x 16).
+// STG: the LDS-staged form (fp32: stride 1 on 16 x 16 planes, stride 2 on 8 x 8 and 16 x 16).
 template <int DT, int W, int ST, bool STG>
 __global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __restrict__ x,
                                                    const int32_t* __restrict__ perm,
@@ -583,20 +593,21 @@ __global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __
     if constexpr (STG) {
         using G = Stage<W, ST>;
         static_assert(staged_geometry(DT, W, W, ST), "no staged form for this geometry");
-        // this wave's area: copy 0 of the planes, 64 zero bytes, copy 1, 64
-        // zero bytes; a padding lane reads the zero bytes after its copy
+        constexpr int LC = G::LC;
+        // this wave's area: per copy the planes, then 16 LC zero bytes that
+        // padding lanes read
         const uint32_t area = uint32_t(uintptr_t((const __attribute__((address_space(3))) void*)psc_rows_red)) +
                               uint32_t(wave * G::WAVE);
-        if (lane < 16) {
-            *(__attribute__((address_space(3))) float*)(uintptr_t)(area + G::ZERO + lane * 4) = 0.f;
-            *(__attribute__((address_space(3))) float*)(uintptr_t)(area + G::COPY + G::ZERO + lane * 4) = 0.f;
-        }
-        // LDS address (copy 0) of the chunk this lane reads in each of its 4 reads
-        uint32_t lo[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int b = 0; b < G::NB; ++b)
+            if (lane < 4 * LC)
+                *(__attribute__((address_space(3))) float*)(uintptr_t)(area + b * G::COPY + G::ZERO + lane * 4) = 0.f;
+        // LDS address (copy 0) of the chunk this lane reads in each of its LC reads
+        uint32_t lo[LC];
+#pragma unroll
+        for (int j = 0; j < LC; ++j)
             lo[j] = s < G::S && r < G::OH
-                        ? area + uint32_t(s * G::PLANE + 16 * (4 * r + ((j + s + (r >> 2)) & 3)))
+                        ? area + uint32_t(s * G::PLANE + 16 * (LC * r + ((j + s + r / G::RD) & (LC - 1))))
                         : area + uint32_t(G::ZERO + 16 * j);
         if (has_filter) {
             const int* segp = seg_ptr + i * (g.m + 1);
@@ -609,11 +620,11 @@ __global__ __launch_bounds__(512) void k_conv_rows(const typename Elt<DT>::T* __
                                                        0x00020000);
             ctx.area = __builtin_amdgcn_readfirstlane(area);
             // load j, lane L: position q of image slot t's block, holding
-            // chunk 4 rr + ((q - t - rr/4) & 3) of the plane (rr = q / 4)
+            // chunk LC rr + ((q - t - rr / RD) mod LC) of the plane (rr = q / LC)
 #pragma unroll
             for (int j = 0; j < G::ND; ++j) {
-                const int pos = 64 * j + lane, t = pos / G::NCH, q = pos - t * G::NCH, rr = q >> 2;
-                const int chunk = 4 * rr + ((q - t - (rr >> 2)) & 3);
+                const int pos = 64 * j + lane, t = pos / G::NCH, q = pos - t * G::NCH, rr = q / LC;
+                const int chunk = LC * rr + ((q - t - rr / G::RD) & (LC - 1));
                 const int im = grp * G::S + t;
                 ctx.vo[j] = im < g.n ? uint32_t(im * g.cin * G::PLANE + chunk * 16) : 0x80000000u;
             }

@@ -100,7 +100,7 @@ bool plan_conv_rows(const PatTable& tab, const ConvArgs& a, RGeo& g) {
 bool prefer_conv_rows(const PatTable& tab, const ConvArgs& a) {
     RGeo g;
     if (!plan_conv_rows(tab, a, g) || a.n < g.S) return false;
-    if (a.stride == 2) return a.w == 8;
+    if (a.stride == 2) return a.w == 8 || g.staged;
     return a.w <= 16 || int64_t(g.groups) * a.cout >= 8192;
 }
 

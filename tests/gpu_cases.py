@@ -208,11 +208,12 @@ def form_cases():
                         False, 1, 2))
         # its stride-2 form: every compiled width, odd and even heights (the
         # last output row's odd input row past the image), ragged groups,
-        # split filters; fp32 8 x 8 planes go through LDS: a ragged last
-        # group (images past the batch), one partial wave, and 2 and 4 shares
-        # (their sums reuse the staging areas)
+        # split filters; fp32 8 x 8 and 16 x 16 planes go through LDS: a
+        # ragged last group (images past the batch), one partial wave, and 2
+        # and 4 shares (their sums reuse the staging areas)
         for n, cin, cout, h, w in ((13, 5, 6, 8, 8), (2, 40, 5, 7, 8), (9, 7, 5, 16, 16), (1, 48, 4, 15, 16),
-                                   (4, 9, 5, 32, 32), (1, 40, 3, 31, 32), (1, 48, 4, 8, 8), (25, 70, 9, 8, 8)):
+                                   (4, 9, 5, 32, 32), (1, 40, 3, 31, 32), (1, 48, 4, 8, 8), (25, 70, 9, 8, 8),
+                                   (1, 48, 4, 16, 16), (15, 70, 9, 16, 16)):
             L = B.Layer(cout, cin, list(FORM_MASKS), cin * cout // 2, dt)
             cfg = B.conv3x3_config(L, dt, n, h, w, False, 2, 2)
             out.append((("rows2", cfg["kernel"], w, cfg["shares"] > 1, cfg["staged"]), n, cin, cout, h, w, dt,
