@@ -94,9 +94,10 @@ bool plan_conv_rows(const PatTable& tab, const ConvArgs& a, RGeo& g) {
 // the column-per-lane kernels spend R+2 single-element loads per 4R FMAs
 // (measured 1.5-4.7x faster there); 28-column rows (about 200 VGPRs, two
 // waves per SIMD) only in grids of many waves, where they were measured
-// slightly ahead.  Stride 2 only on 8-column inputs: wider rows put the
-// lanes of one 16-byte load 128 or 256 bytes apart, one cache line each,
-// and measured slower than the column-per-lane stride-2 kernel.
+// slightly ahead.  Stride 2 on 8-column inputs and on fp32 16 x 16 planes
+// (staged through LDS); other wider rows put the lanes of one 16-byte load
+// 128 or 256 bytes apart, one cache line each, and measured slower than the
+// column-per-lane stride-2 kernel.
 bool prefer_conv_rows(const PatTable& tab, const ConvArgs& a) {
     RGeo g;
     if (!plan_conv_rows(tab, a, g) || a.n < g.S) return false;
