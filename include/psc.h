@@ -196,9 +196,11 @@ psc_status psc_conv3x3_fwd_pool2(const psc_layer *layer, const psc_packed *packe
  *   y[n,f,i,j] = sigma(b[f] + sum over kept (ci, p) of f of
  *                sum_{(r,s) in p} v * x[n, ci, stride*i + r - 1, stride*j + s - 1])
  * with out-of-image taps reading zero.  stride 1 is psc_conv3x3_fwd_algo.
- * Stride 2 with algo 0 or 3 runs the tuned stride-2 kernel for even widths
- * of at most 126 columns (the one-output-per-lane kernel otherwise, and
- * always with algo 1); algo 2 the one-row-per-lane kernel.  Other
+ * Stride 2 with algo 0 runs the one-row-per-lane kernel when the batch
+ * fills a wave with whole images of 8 columns, or of 16 x 16 in fp32;
+ * otherwise, and always with algo 3, the tuned stride-2 kernel for even
+ * widths of at most 126 columns (the one-output-per-lane kernel otherwise,
+ * and always with algo 1); algo 2 the one-row-per-lane kernel.  Other
  * conventions and errors as in psc_conv3x3_fwd_algo; a stride other than 1
  * or 2 returns PSC_ERR_ARG. */
 psc_status psc_conv3x3_fwd_strided(const psc_layer *layer, const psc_packed *packed,
@@ -317,7 +319,8 @@ typedef struct psc_conv_config {
                                      (2 when w is a multiple of 4)
                                   4: one output row per lane (all w columns) */
     int32_t staged;            /* 0: input rows loaded straight into registers,
-                                  1: staged through LDS, one run per wave,
+                                  1: staged through LDS, one run per wave
+                                     (kernel 4: the wave's whole planes),
                                   2: staged through LDS, several runs per wave */
     int32_t rows_per_lane;     /* output rows per lane */
     int32_t cols_per_lane;     /* output columns per lane */
