@@ -145,3 +145,26 @@ def test_deep_28_column_layers_take_the_wide_form_with_shares():
         assert (c["kernel"], c["cols_per_lane"], c["shares"]) == (1, 4, 8)
     assert cfg(64, 64, 1, B.PSC_F32)["cols_per_lane"] == 1        # too few channels for 8 shares
     assert cfg(128, 128, 1, B.PSC_F16)["cols_per_lane"] == 1      # fp16 keeps the one-column form
+
+
+def test_row_kernel_stages_whole_planes_on_three_fp32_geometries():
+    """At batch 256 the automatic choice runs the one-row-per-lane kernel
+    with whole channel planes copied through LDS on fp32 16x16 at stride 1
+    and on 8x8 and 16x16 at stride 2 (the CIFAR ResNet-18 shapes); fp16 and
+    non-square planes of the same widths load their rows directly, and 32x32
+    at stride 2 keeps the stride-2 kernel."""
+    codes = [c for c in range(512) if bin(c).count("1") == 4 and (c >> 4) & 1][:6]
+    def cfg(cin, cout, h, w, stride, dtype, n=256):
+        L = B.Layer(cout, cin, codes, (cout * cin) * 3 // 10, dtype)
+        return B.conv3x3_config(L, dtype, n, h, w, False, stride, 0)
+    for cin, cout, hw, stride in ((128, 128, 16, 1), (256, 512, 8, 2), (128, 256, 16, 2)):
+        c = cfg(cin, cout, hw, hw, stride, B.PSC_F32)
+        assert (c["kernel"], c["staged"], c["rows_per_lane"]) == (4, 1, 1), (cin, cout, hw, stride, c)
+        assert c["cols_per_lane"] == hw // stride
+    for cin, cout, h, w, stride, dtype in ((256, 512, 8, 8, 2, B.PSC_F16), (128, 128, 16, 16, 1, B.PSC_F16),
+                                           (128, 128, 15, 16, 1, B.PSC_F32), (256, 256, 8, 8, 1, B.PSC_F32)):
+        c = cfg(cin, cout, h, w, stride, dtype)
+        assert c["kernel"] == 4 and c["staged"] == 0, (cin, cout, h, w, stride, dtype, c)
+    assert cfg(64, 128, 32, 32, 2, B.PSC_F32)["kernel"] == 3
+    # batches that do not fill a wave with whole images stay off the row kernel
+    assert cfg(128, 256, 16, 16, 2, B.PSC_F32, n=2)["kernel"] == 3
